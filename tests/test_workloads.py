@@ -1,0 +1,60 @@
+"""The seeded input generator: determinism, per-row regeneration, storage rounding."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+
+
+def test_bf16_rounding_matches_torch():
+    g = np.random.default_rng(0)
+    x = np.concatenate([g.normal(0, 10, 100000), g.normal(0, 1e-3, 1000), [0.0, -0.0, 1e30, -1e-30]]).astype(np.float32)
+    ours = W.bf16_bits_from_f32(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(ours, ref)
+    assert np.array_equal(W.f32_from_bf16_bits(ours), torch.from_numpy(x).to(torch.bfloat16).float().numpy())
+
+
+@pytest.mark.parametrize("name", ["tiny", "c2"])
+def test_bulk_equals_per_row_and_is_deterministic(name):
+    cfg = W.CONFIGS[name]
+    a = W.generate(cfg, seed=1)
+    b = W.generate(cfg, seed=1, threads=1)
+    for k in ("draft", "target", "drafted", "uniforms"):
+        assert np.array_equal(a[k], b[k])
+    K = cfg.k_max
+    for r in (0, cfg.draft_rows - 1):
+        assert np.array_equal(a["draft"][r], W.draft_row(cfg, 1, r))
+        bb, i = divmod(r, K)
+        assert np.array_equal(a["target"][bb * (K + 1) + i], W.target_row(cfg, 1, bb, i))
+        assert a["drafted"][bb, i] == W.drafted_id(cfg, 1, r)
+    assert np.array_equal(a["target"][K], W.target_row(cfg, 1, 0, K))
+    c = W.generate(cfg, seed=2)
+    assert not np.array_equal(a["draft"], c["draft"])
+
+
+def test_uniform_lattice_and_tiny_drafts():
+    cfg = W.CONFIGS["tiny"]
+    d = W.generate(cfg, 0)
+    u = d["uniforms"].astype(np.float64)
+    assert ((u >= 0) & (u < 1)).all()
+    assert np.array_equal(u * 2 ** 24, np.floor(u * 2 ** 24))
+    for i in range(cfg.k_max):
+        assert d["drafted"][0, i] == int(np.argmax(d["draft"][i]))
+
+
+def test_c3_independent_rows_and_c4_regimes():
+    c3 = W.CONFIGS["c3"]
+    assert len(W._c3_indep_rows(c3, 0)) == round(0.2 * c3.dense_target_rows)
+    c4 = W.CONFIGS["c4"]
+    regs = [W._c4_regime(c4, 0, r) for r in range(c4.draft_rows)]
+    counts = np.bincount(regs)
+    assert counts.tolist() == [c4.draft_rows // 3, c4.draft_rows // 3, c4.draft_rows - 2 * (c4.draft_rows // 3)]
+
+
+def test_pack_ragged():
+    K = 4
+    pad = np.arange(3 * (K + 1)).reshape(3, K + 1)
+    k = np.array([1, 4, 2])
+    out = W.pack_ragged(k, K, pad)
+    assert out.tolist() == [0, 4, 5, 6, 7, 8, 9, 10, 11, 14]
