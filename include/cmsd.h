@@ -1,0 +1,199 @@
+/*
+ * cmsd.h - confidence-modulated speculative decoding: the vocabulary-wide logit
+ * pass (arXiv 2508.15371, Sec. III.B), as a C ABI over gfx950 HIP kernels.
+ *
+ * Three calls, in the order one decoding iteration uses them:
+ *
+ *   cmsd_confidence  per drafter row: softmax normaliser, entropy, top-1/top-2
+ *                    margins and the unified confidence C     (Sec. III.B(1))
+ *   cmsd_draft_len   per sequence: adaptive draft length k_b from the mean
+ *                    confidence, plus packed target-row offsets (Sec. III.B(b))
+ *   cmsd_verify      per drafted position: confidence-modulated acceptance,
+ *                    accepted-prefix length, and the final token sampled from
+ *                    the residual (or bonus) distribution     (Sec. III.A, III.B(c))
+ *
+ * Conventions shared by every call
+ *   - All array pointers are DEVICE pointers (hipMalloc / torch CUDA tensors);
+ *     params structs are HOST pointers read during the call.  The caller owns
+ *     every buffer; the library keeps no state and allocates no memory.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Calls
+ *     only enqueue work and return; results are ready when the stream is.
+ *   - Argument errors are detected on the host before anything is enqueued and
+ *     returned as CMSD_ERR_ARG / CMSD_ERR_DTYPE; in that case no output is
+ *     touched.  CMSD_ERR_LAUNCH reports a failed kernel launch.
+ *   - Device-resident indices (draft lengths, offsets, drafted ids) cannot be
+ *     checked on the host; the kernels check them and report a violation per
+ *     sequence through the outputs (see cmsd_verify) without reading out of
+ *     bounds.
+ *   - Logit preconditions (not checked): every row has at least one finite
+ *     entry; entries are finite with |z| < 2^127, or -inf (masked tokens); no
+ *     NaN or +inf.  Violations give unspecified values, never a fault.
+ *   - Logit dtypes: CMSD_F32 (float) or CMSD_BF16 (raw bfloat16, 2 bytes).
+ *     Pointers must be aligned to the element size; rows need no other
+ *     alignment (an unaligned head and tail are read element-wise).
+ *   - Results are deterministic: fixed reduction orders, no float atomics.
+ */
+#ifndef CMSD_H
+#define CMSD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CMSD_OK = 0,
+  CMSD_ERR_ARG = 1,    /* invalid size, pointer or parameter            */
+  CMSD_ERR_DTYPE = 2,  /* unknown logit dtype                            */
+  CMSD_ERR_LAUNCH = 3  /* the HIP runtime refused a launch               */
+} cmsd_status;
+
+typedef enum { CMSD_F32 = 0, CMSD_BF16 = 1 } cmsd_dtype;
+
+typedef enum {
+  CMSD_MODE_STANDARD = 0, /* standard speculative sampling only            */
+  CMSD_MODE_CM = 1        /* plus the confidence-modulated gate (OR-ed)     */
+} cmsd_mode;
+
+/* Weights of the unified confidence, Sec. III.B(1): C = lambda_ent*(1 - H/ln V)
+ * + lambda_margin*sigmoid(beta_margin*(z1 - z2)) + lambda_soft*min(1, (P1-P2)/(1-1/V)).
+ * Each lambda in [0,1], |sum - 1| <= 1e-6; beta_margin finite and > 0. */
+typedef struct {
+  float lambda_ent;
+  float lambda_margin;
+  float lambda_soft;
+  float beta_margin;
+} cmsd_conf_params;
+
+/* Draft-length clip, Sec. III.B(b): k = min(k_max, max(k_min, floor(alpha*Cbar*k_max))).
+ * 1 <= k_min <= k_max <= 4096, 0 < alpha <= 1. */
+typedef struct {
+  int32_t k_min;
+  int32_t k_max;
+  float alpha;
+} cmsd_draft_params;
+
+/* Verification, Sec. III.B(c): tau_t = tau_base + gamma*(1 - C_t); the gate passes
+ * when the drafted token is within the target's top_beta and its log-prob gap to the
+ * target's top-1 is <= tau_t.  mode is a cmsd_mode; top_beta >= 0 (0 disables the
+ * gate); tau_base, gamma finite (gamma may be negative). */
+typedef struct {
+  int32_t mode;
+  int32_t top_beta;
+  float tau_base;
+  float gamma;
+} cmsd_verify_params;
+
+/* One record per drafter row (32 bytes), written by cmsd_confidence. */
+typedef struct {
+  float max_logit;    /* z^(1)                                                  */
+  float sum_exp;      /* A = sum_v exp(z_v - z^(1)); log-normaliser = max_logit + ln A */
+  float entropy;      /* H = -sum p ln p, nats (Sec. III.B(1), entropy)           */
+  float margin_soft;  /* P^(1) - P^(2) in [0,1] (softmax margin)                  */
+  float margin_logit; /* z^(1) - z^(2) >= 0, +inf with a single finite logit      */
+  float conf;         /* unified confidence C_t (Sec. III.B(1), ensemble)         */
+  int32_t top1;       /* lowest index attaining z^(1)                             */
+  uint32_t flags;     /* bit 0: the row contains -inf entries                     */
+} cmsd_row_stats;
+
+/* One record per packed target row (16 bytes), written by cmsd_verify. */
+typedef struct {
+  float max_logit;    /* max of the target row                                    */
+  float sum_exp;      /* sum_v exp(z_v - max)                                     */
+  int32_t n_greater;  /* min(#{v : z_v > z_drafted}, top_beta); -1 on the final row */
+  int32_t accept;     /* 1 accepted, 0 rejected, -1 final row, -2 invalid input   */
+} cmsd_target_stats;
+
+/*
+ * cmsd_confidence - reduce each logit row to its cmsd_row_stats (Sec. III.B(1):
+ * entropy, logit margin, softmax margin, unified confidence).
+ *
+ *   logits      device, n_rows rows of `vocab` logits; row r starts at element
+ *               r*row_stride.  dtype CMSD_F32 or CMSD_BF16.
+ *   n_rows      >= 0 (0: nothing is enqueued).  For a draft of k_max positions
+ *               over B sequences, n_rows = B*k_max with row b*k_max+i = position i.
+ *   vocab       >= 2 and < 2^31; row_stride >= vocab (elements).
+ *   params      host; see cmsd_conf_params.
+ *   stats       device, n_rows records (output).
+ * Errors: CMSD_ERR_ARG (null pointer, bad size, misaligned pointer, bad params),
+ *         CMSD_ERR_DTYPE, CMSD_ERR_LAUNCH.
+ */
+cmsd_status cmsd_confidence(const void* logits, int32_t dtype, int64_t n_rows, int64_t vocab,
+                            int64_t row_stride, const cmsd_conf_params* params,
+                            cmsd_row_stats* stats, void* stream);
+
+/*
+ * cmsd_draft_len - adaptive draft length per sequence (Sec. III.B(b)).
+ *
+ *   stats           device, batch*k_max records from cmsd_confidence (row b*k_max+i).
+ *   batch           >= 0.
+ *   params          host; k_max must equal the number of drafter rows per sequence.
+ *                   The window mean runs over all k_max positions.
+ *   draft_len       device, batch int32 (output): k_b in [k_min, k_max].
+ *   target_offsets  device, batch+1 int32 (output): exclusive prefix sum of k_b+1,
+ *                   i.e. the first packed target row of each sequence; entry
+ *                   [batch] is the total number of target rows.
+ * The mean and product are formed in double precision, left to right.
+ * Errors: CMSD_ERR_ARG, CMSD_ERR_LAUNCH.
+ */
+cmsd_status cmsd_draft_len(const cmsd_row_stats* stats, int32_t batch, const cmsd_draft_params* params,
+                           int32_t* draft_len, int32_t* target_offsets, void* stream);
+
+/*
+ * cmsd_verify - confidence-modulated verification (Sec. III.B(c)) of every drafted
+ * position, accepted-prefix length (halt at the first rejection, Sec. III.A), and
+ * the final token: on a rejection at position c, a sample from the residual
+ * max(0, p_t - p_d) of target and drafter rows c; when all k_b drafts pass, a
+ * sample from target row k_b.
+ *
+ * A position is accepted when u < p_t(y)/p_d(y) (standard speculative sampling)
+ * or, in CMSD_MODE_CM, when the gate passes: #{v: z_t,v > z_t,y} < top_beta and
+ * z_t^(1) - z_t,y <= tau_base + gamma*(1 - C).
+ *
+ *   draft_logits    device, batch*k_max drafter rows (row b*k_max+i), stride
+ *                   draft_stride >= vocab elements (the rows cmsd_confidence saw).
+ *   draft_stats     device, batch*k_max records from cmsd_confidence.
+ *   target_logits   device, target_rows packed rows, stride target_stride >= vocab:
+ *                   sequence b owns rows target_offsets[b] .. target_offsets[b]+k_b,
+ *                   row target_offsets[b]+i scoring position i, the last one the
+ *                   row after the final draft.  Dense layouts pass
+ *                   target_offsets[b] = b*(k_max+1) and draft_len[b] = k_max.
+ *   target_rows     number of rows allocated in target_logits, uniforms and
+ *                   target_stats (>= target_offsets[batch]).
+ *   target_offsets  device, batch+1 int32 (as written by cmsd_draft_len).
+ *   draft_len       device, batch int32, each in [0, k_max].
+ *   drafted         device, batch*k_max int32 token ids (entries i >= k_b unused).
+ *   uniforms        device, target_rows floats in [0,1), packed like the target rows:
+ *                   slot i < k_b is the accept test of position i, slot k_b the
+ *                   final sample.
+ *   dtype           logit dtype of both logit arrays.
+ *   batch >= 0, k_max in [1, 4096], vocab in [2, 2^31).
+ *   params          host; see cmsd_verify_params.
+ *   target_stats    device, target_rows records (output; rows beyond
+ *                   target_offsets[batch] untouched).
+ *   n_accepted      device, batch int32 (output): accepted prefix length c_b in
+ *                   [0, k_b]; -1 if the sequence's device inputs are invalid
+ *                   (offsets inconsistent with draft_len or target_rows, draft_len
+ *                   out of range, drafted id outside [0, vocab)).
+ *   next_token      device, batch int32 (output): the final token; -1 when invalid.
+ * Errors: CMSD_ERR_ARG, CMSD_ERR_DTYPE, CMSD_ERR_LAUNCH.
+ */
+cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cmsd_row_stats* draft_stats,
+                        const void* target_logits, int64_t target_stride, int64_t target_rows,
+                        const int32_t* target_offsets, const int32_t* draft_len, const int32_t* drafted,
+                        const float* uniforms, int32_t dtype, int32_t batch, int32_t k_max, int64_t vocab,
+                        const cmsd_verify_params* params, cmsd_target_stats* target_stats,
+                        int32_t* n_accepted, int32_t* next_token, void* stream);
+
+/* Human-readable name of a status code (static string). */
+const char* cmsd_status_string(cmsd_status s);
+
+/* Library ABI version, (major << 16) | minor. */
+int32_t cmsd_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CMSD_H */

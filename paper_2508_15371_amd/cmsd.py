@@ -1,0 +1,172 @@
+"""ctypes binding of ``libcmsd.so`` (include/cmsd.h).
+
+Argument marshalling only: the functions below check tensor shapes/dtypes, turn
+torch tensors into device pointers and the current HIP stream into a handle, and
+call the C entry points of the same name.  Every step of the computation runs in
+the library's HIP kernels; there is no fallback.  Importing this module raises
+``ImportError`` when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import re
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcmsd.so")
+HEADER = os.path.join(os.path.dirname(_HERE), "include", "cmsd.h")
+
+CMSD_OK, CMSD_ERR_ARG, CMSD_ERR_DTYPE, CMSD_ERR_LAUNCH = 0, 1, 2, 3
+CMSD_F32, CMSD_BF16 = 0, 1
+CMSD_MODE_STANDARD, CMSD_MODE_CM = 0, 1
+
+STATS_FIELDS = ("max_logit", "sum_exp", "entropy", "margin_soft", "margin_logit", "conf", "top1", "flags")
+TSTATS_FIELDS = ("max_logit", "sum_exp", "n_greater", "accept")
+
+
+class ConfParams(C.Structure):
+    _fields_ = [("lambda_ent", C.c_float), ("lambda_margin", C.c_float), ("lambda_soft", C.c_float),
+                ("beta_margin", C.c_float)]
+
+
+class DraftParams(C.Structure):
+    _fields_ = [("k_min", C.c_int32), ("k_max", C.c_int32), ("alpha", C.c_float)]
+
+
+class VerifyParams(C.Structure):
+    _fields_ = [("mode", C.c_int32), ("top_beta", C.c_int32), ("tau_base", C.c_float), ("gamma", C.c_float)]
+
+
+class CmsdError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn}: status {status} ({_lib.cmsd_status_string(status).decode()})")
+        self.status = status
+
+
+def _load() -> C.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built: run `python -m paper_2508_15371_amd.build`")
+    lib = C.CDLL(LIB_PATH)
+    vp, i32, i64 = C.c_void_p, C.c_int32, C.c_int64
+    lib.cmsd_confidence.argtypes = [vp, i32, i64, i64, i64, C.POINTER(ConfParams), vp, vp]
+    lib.cmsd_confidence.restype = C.c_int
+    lib.cmsd_draft_len.argtypes = [vp, i32, C.POINTER(DraftParams), vp, vp, vp]
+    lib.cmsd_draft_len.restype = C.c_int
+    lib.cmsd_verify.argtypes = [vp, i64, vp, vp, i64, i64, vp, vp, vp, vp, i32, i32, i32, i64,
+                                C.POINTER(VerifyParams), vp, vp, vp, vp]
+    lib.cmsd_verify.restype = C.c_int
+    lib.cmsd_status_string.argtypes = [C.c_int]
+    lib.cmsd_status_string.restype = C.c_char_p
+    lib.cmsd_version.argtypes = []
+    lib.cmsd_version.restype = C.c_int32
+    return lib
+
+
+_lib = _load()
+
+
+def lib() -> C.CDLL:
+    """The loaded ``libcmsd.so`` (raw entry points, ``argtypes`` set)."""
+    return _lib
+
+
+def header_symbols() -> list[str]:
+    """Entry points declared in include/cmsd.h."""
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:cmsd_status|const char\*|int32_t)\s+(cmsd_\w+)\s*\(", txt, re.M)))
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return CMSD_F32
+    if t.dtype == torch.bfloat16:
+        return CMSD_BF16
+    raise TypeError(f"logits must be float32 or bfloat16, got {t.dtype}")
+
+
+def _rows(t: torch.Tensor, name: str) -> tuple[int, int, int]:
+    """(rows, vocab, row_stride) of a [rows, V] logit matrix with unit inner stride."""
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError(f"{name} must be a 2-D [rows, vocab] tensor with unit inner stride")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    return t.shape[0], t.shape[1], t.stride(0)
+
+
+def _check(fn: str, status: int) -> None:
+    if status != CMSD_OK:
+        raise CmsdError(fn, status)
+
+
+def cmsd_confidence(logits: torch.Tensor, stats: torch.Tensor | None = None, *,
+                    lambdas=(1 / 3, 1 / 3, 1 / 3), beta_margin: float = 1.0, stream=None) -> torch.Tensor:
+    """Per-row stats of ``logits`` [rows, V] -> float32 [rows, 8] (columns STATS_FIELDS;
+    ``top1`` and ``flags`` hold int32 bits: read them with ``.view(torch.int32)``)."""
+    n, V, st = _rows(logits, "logits")
+    if stats is None:
+        stats = torch.empty((n, 8), dtype=torch.float32, device=logits.device)
+    p = ConfParams(float(lambdas[0]), float(lambdas[1]), float(lambdas[2]), float(beta_margin))
+    _check("cmsd_confidence", _lib.cmsd_confidence(_ptr(logits), _dtype_code(logits), n, V, st, C.byref(p),
+                                                   _ptr(stats), _stream(stream)))
+    return stats
+
+
+def cmsd_draft_len(stats: torch.Tensor, batch: int, *, k_min: int, k_max: int, alpha: float,
+                   draft_len: torch.Tensor | None = None, target_offsets: torch.Tensor | None = None,
+                   stream=None) -> tuple[torch.Tensor, torch.Tensor]:
+    """Draft lengths [batch] int32 and packed target offsets [batch+1] int32 from the
+    drafter stats of batch*k_max rows."""
+    dev = stats.device
+    if draft_len is None:
+        draft_len = torch.empty(batch, dtype=torch.int32, device=dev)
+    if target_offsets is None:
+        target_offsets = torch.empty(batch + 1, dtype=torch.int32, device=dev)
+    p = DraftParams(int(k_min), int(k_max), float(alpha))
+    _check("cmsd_draft_len", _lib.cmsd_draft_len(_ptr(stats), int(batch), C.byref(p), _ptr(draft_len),
+                                                 _ptr(target_offsets), _stream(stream)))
+    return draft_len, target_offsets
+
+
+def cmsd_verify(draft_logits: torch.Tensor, draft_stats: torch.Tensor, target_logits: torch.Tensor,
+                target_offsets: torch.Tensor, draft_len: torch.Tensor, drafted: torch.Tensor,
+                uniforms: torch.Tensor, *, batch: int, k_max: int, mode: int = CMSD_MODE_CM, top_beta: int = 3,
+                tau_base: float = 0.1, gamma: float = 1.0, target_stats: torch.Tensor | None = None,
+                n_accepted: torch.Tensor | None = None, next_token: torch.Tensor | None = None,
+                stream=None) -> tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Verification of every drafted position; returns (n_accepted [batch] int32,
+    next_token [batch] int32, target_stats float32 [target_rows, 4] with int32 bits in
+    columns 2 and 3)."""
+    _, V, dst = _rows(draft_logits, "draft_logits")
+    trows, V2, tst = _rows(target_logits, "target_logits")
+    if V2 != V or target_logits.dtype != draft_logits.dtype:
+        raise ValueError("draft and target logits must share vocab size and dtype")
+    dev = target_logits.device
+    if target_stats is None:
+        target_stats = torch.empty((trows, 4), dtype=torch.float32, device=dev)
+    if n_accepted is None:
+        n_accepted = torch.empty(batch, dtype=torch.int32, device=dev)
+    if next_token is None:
+        next_token = torch.empty(batch, dtype=torch.int32, device=dev)
+    for name, t, dt in (("target_offsets", target_offsets, torch.int32), ("draft_len", draft_len, torch.int32),
+                        ("drafted", drafted, torch.int32), ("uniforms", uniforms, torch.float32)):
+        if t.dtype != dt or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {dt} tensor")
+    p = VerifyParams(int(mode), int(top_beta), float(tau_base), float(gamma))
+    _check("cmsd_verify", _lib.cmsd_verify(
+        _ptr(draft_logits), dst, _ptr(draft_stats), _ptr(target_logits), tst, trows,
+        _ptr(target_offsets), _ptr(draft_len), _ptr(drafted), _ptr(uniforms), _dtype_code(target_logits),
+        int(batch), int(k_max), V, C.byref(p), _ptr(target_stats), _ptr(n_accepted), _ptr(next_token),
+        _stream(stream)))
+    return n_accepted, next_token, target_stats

@@ -1,0 +1,1019 @@
+// cmsd.hip - gfx950 kernels and C ABI for the logit pass of confidence-modulated
+// speculative decoding (arXiv 2508.15371, Sec. III.B).  Interface: include/cmsd.h.
+//
+// Kernels (all bandwidth-bound streaming reductions; no MFMA):
+//   k_confidence   one workgroup per drafter row: single streaming pass with an
+//                  online max / sum-exp / sum(e*(z-m)) reduction, top-1 and top-2
+//                  tracking at chunk granularity, DPP wave reductions, LDS only for
+//                  the cross-wave combine; epilogue forms H, margins and C.
+//   k_draft_len    one workgroup: per-sequence mean confidence, clipped floor,
+//                  exclusive scan of k_b + 1 into packed target-row offsets.
+//   k_target_rows  one workgroup per packed target row: max / sum-exp of the row,
+//                  scalar (ballot + s_bcnt1) count of logits above the drafted
+//                  token's, and the acceptance decision of that position.
+//   k_final        one workgroup per sequence: ballot-based first-reject scan, then
+//                  an inverse-CDF sample from the residual (or bonus) row using a
+//                  per-thread contiguous span, a workgroup scan and a wave-level
+//                  locate that reproduces the scan's sums bit for bit.
+//
+// Numerics: exponentials are evaluated as 2^(z*log2e - m*log2e) with one FMA and
+// v_exp_f32; per-thread partial sums are fp32 over 32-element chunks, the
+// cross-thread combines and every decision-side formula are fp64.  Reductions have
+// a fixed order, so results are bit-reproducible run to run.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "cmsd.h"
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr double kLn2 = 0.69314718055994530942;
+constexpr float kNegBig = -3.0e38f;  // finite "minus infinity" for the scaled running max
+
+// ----------------------------------------------------------------------------- logit element types
+struct Bf16 { uint16_t bits; };
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  static constexpr int VEC = 4;   // elements per 16-byte vector
+  static constexpr int U = 8;     // vectors per thread per chunk (32 elements)
+  __device__ static float load(const float* p) { return *p; }
+  __device__ static void unpack(const uint4& v, float* f) {
+    f[0] = __uint_as_float(v.x); f[1] = __uint_as_float(v.y);
+    f[2] = __uint_as_float(v.z); f[3] = __uint_as_float(v.w);
+  }
+};
+template <> struct Elem<Bf16> {
+  static constexpr int VEC = 8;
+  static constexpr int U = 4;     // 32 elements per chunk
+  __device__ static float load(const Bf16* p) { return __uint_as_float(uint32_t(p->bits) << 16); }
+  __device__ static void unpack(const uint4& v, float* f) {
+    f[0] = __uint_as_float(v.x << 16); f[1] = __uint_as_float(v.x & 0xffff0000u);
+    f[2] = __uint_as_float(v.y << 16); f[3] = __uint_as_float(v.y & 0xffff0000u);
+    f[4] = __uint_as_float(v.z << 16); f[5] = __uint_as_float(v.z & 0xffff0000u);
+    f[6] = __uint_as_float(v.w << 16); f[7] = __uint_as_float(v.w & 0xffff0000u);
+  }
+};
+
+// Row geometry: `head` leading elements before the first 16-byte boundary, `nvec`
+// aligned 16-byte vectors, `tail` trailing elements.
+struct Geom {
+  int head;
+  int tail;
+  int64_t nvec;
+};
+
+template <typename T>
+__device__ __forceinline__ Geom row_geom(const T* row, int64_t V) {
+  constexpr int VEC = Elem<T>::VEC;
+  const int mis = int(reinterpret_cast<uintptr_t>(row) & 15u);
+  int64_t head = mis ? (16 - mis) / int(sizeof(T)) : 0;
+  if (head > V) head = V;
+  const int64_t rest = V - head;
+  Geom g;
+  g.head = int(head);
+  g.nvec = rest / VEC;
+  g.tail = int(rest - g.nvec * VEC);
+  return g;
+}
+
+__device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// ----------------------------------------------------------------------------- wave / block reductions
+// Wave64 all-reduce: DPP quad permutes and row mirrors inside each 16-lane row,
+// then the four row results are combined through readlane (uniform result).
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) { return __int_as_float(dpp_i<CTRL>(__float_as_int(v))); }
+template <int CTRL>
+__device__ __forceinline__ double dpp_d(double v) {
+  const int2 p = *reinterpret_cast<int2*>(&v);
+  int2 r;
+  r.x = dpp_i<CTRL>(p.x);
+  r.y = dpp_i<CTRL>(p.y);
+  return *reinterpret_cast<double*>(&r);
+}
+__device__ __forceinline__ float rl_f(float v, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l)); }
+__device__ __forceinline__ double rl_d(double v, int l) {
+  const int2 p = *reinterpret_cast<int2*>(&v);
+  int2 r;
+  r.x = __builtin_amdgcn_readlane(p.x, l);
+  r.y = __builtin_amdgcn_readlane(p.y, l);
+  return *reinterpret_cast<double*>(&r);
+}
+
+struct OpMax { __device__ float operator()(float a, float b) const { return fmaxf(a, b); } };
+struct OpSumD { __device__ double operator()(double a, double b) const { return a + b; } };
+struct OpSumI { __device__ int operator()(int a, int b) const { return a + b; } };
+struct OpMinI { __device__ int operator()(int a, int b) const { return a < b ? a : b; } };
+struct OpMaxI { __device__ int operator()(int a, int b) const { return a > b ? a : b; } };
+
+template <typename Op>
+__device__ __forceinline__ float wave_all_f(float v, Op op) {
+  v = op(v, dpp_f<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = op(v, dpp_f<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = op(v, dpp_f<0x141>(v));  // row_half_mirror
+  v = op(v, dpp_f<0x140>(v));  // row_mirror
+  return op(op(rl_f(v, 0), rl_f(v, 16)), op(rl_f(v, 32), rl_f(v, 48)));
+}
+template <typename Op>
+__device__ __forceinline__ double wave_all_d(double v, Op op) {
+  v = op(v, dpp_d<0xB1>(v));
+  v = op(v, dpp_d<0x4E>(v));
+  v = op(v, dpp_d<0x141>(v));
+  v = op(v, dpp_d<0x140>(v));
+  return op(op(rl_d(v, 0), rl_d(v, 16)), op(rl_d(v, 32), rl_d(v, 48)));
+}
+template <typename Op>
+__device__ __forceinline__ int wave_all_i(int v, Op op) {
+  v = op(v, dpp_i<0xB1>(v));
+  v = op(v, dpp_i<0x4E>(v));
+  v = op(v, dpp_i<0x141>(v));
+  v = op(v, dpp_i<0x140>(v));
+  return op(op(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 16)),
+            op(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48)));
+}
+
+// Block all-reduce through LDS: one slot per wave, combined in wave order by every
+// thread (so every thread holds the same, order-fixed result).  `slot` must hold
+// BD/64 elements; the leading barrier protects the slot from a previous use.
+template <int BD, typename Op>
+__device__ __forceinline__ float block_all_f(float v, Op op, float* slot) {
+  constexpr int NW = BD / 64;
+  const float w = wave_all_f(v, op);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) slot[threadIdx.x >> 6] = w;
+  __syncthreads();
+  float r = slot[0];
+#pragma unroll
+  for (int i = 1; i < NW; ++i) r = op(r, slot[i]);
+  return r;
+}
+template <int BD, typename Op>
+__device__ __forceinline__ double block_all_d(double v, Op op, double* slot) {
+  constexpr int NW = BD / 64;
+  const double w = wave_all_d(v, op);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) slot[threadIdx.x >> 6] = w;
+  __syncthreads();
+  double r = slot[0];
+#pragma unroll
+  for (int i = 1; i < NW; ++i) r = op(r, slot[i]);
+  return r;
+}
+template <int BD, typename Op>
+__device__ __forceinline__ int block_all_i(int v, Op op, int* slot) {
+  constexpr int NW = BD / 64;
+  const int w = wave_all_i(v, op);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) slot[threadIdx.x >> 6] = w;
+  __syncthreads();
+  int r = slot[0];
+#pragma unroll
+  for (int i = 1; i < NW; ++i) r = op(r, slot[i]);
+  return r;
+}
+
+// ----------------------------------------------------------------------------- streaming row state
+// Online normaliser in base-2 units relative to a running scaled max ms = fl(max*log2e):
+//   A = sum 2^x,  T = sum 2^x * x,  x = z*log2e - ms.
+// When ms grows by -d (d <= 0) the partial sums rescale as A' = 2^d A and
+// T' = 2^d (T + d A).  T becomes NaN exactly when the row holds a -inf logit
+// (0 * -inf); that case is redone with a guarded pass in the epilogue.
+struct NormState {
+  float ms = kNegBig;
+  float A = 0.f;
+  float T = 0.f;
+};
+
+template <int N, bool GUARD, bool WITH_T>
+__device__ __forceinline__ void norm_chunk(NormState& s, const float* f, uint32_t valid, float cmax) {
+  const float ms_new = fmaxf(s.ms, cmax * kLog2e);
+  const float d = s.ms - ms_new;
+  const float sc = fexp2(d);
+  float cs = 0.f, ct = 0.f;
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    float x = fmaf(f[j], kLog2e, -ms_new);
+    float e = fexp2(x);
+    if (GUARD) {
+      const bool ok = (valid >> j) & 1u;
+      e = ok ? e : 0.f;
+      x = ok ? x : 0.f;
+    }
+    cs += e;
+    if (WITH_T) ct = fmaf(e, x, ct);
+  }
+  if (WITH_T) s.T = fmaf(sc, fmaf(d, s.A, s.T), ct);
+  s.A = fmaf(s.A, sc, cs);
+  s.ms = ms_new;
+}
+
+template <int N>
+__device__ __forceinline__ float chunk_max(const float* f) {
+  float m = f[0];
+#pragma unroll
+  for (int j = 1; j < N; ++j) m = fmaxf(m, f[j]);
+  return m;
+}
+
+// Drafter-row state: normaliser plus the top-2 of chunk maxima and the first chunk
+// (in this thread's index order) that attains the thread's maximum.
+struct ConfState {
+  NormState n;
+  float t1 = -INFINITY;
+  float t2 = -INFINITY;
+  int gid = -1;
+};
+
+template <int N, bool GUARD>
+__device__ __forceinline__ void conf_chunk(ConfState& s, const float* f, uint32_t valid, int cid) {
+  const float cmax = chunk_max<N>(f);
+  s.gid = cmax > s.t1 ? cid : s.gid;
+  s.t2 = __builtin_amdgcn_fmed3f(s.t1, s.t2, cmax);
+  s.t1 = fmaxf(s.t1, cmax);
+  norm_chunk<N, GUARD, true>(s.n, f, valid, cmax);
+}
+
+__device__ __forceinline__ void conf_one(ConfState& s, float z, int cid) {
+  float f[1] = {z};
+  conf_chunk<1, false>(s, f, 1u, cid);
+}
+
+// Enumerates the elements of one chunk of thread t (chunk ids: 0 head element,
+// 1..nr full rounds, nr+1 the partial round, nr+2 the tail element) and returns the
+// lowest index holding `m` plus the largest other value in that chunk.
+template <typename T, int BD>
+__device__ void rescan_chunk(const T* row, const Geom& g, int64_t nr, int cid, float m, int64_t& idx, float& other) {
+  using E = Elem<T>;
+  constexpr int VEC = E::VEC, U = E::U;
+  const int t = threadIdx.x;
+  idx = INT64_MAX;
+  other = -INFINITY;
+  auto visit = [&](int64_t i, float z) {
+    if (idx == INT64_MAX && z == m) idx = i;
+    else other = fmaxf(other, z);
+  };
+  if (cid == 0) {
+    if (t < g.head) visit(t, E::load(row + t));
+  } else if (cid == nr + 2) {
+    const int64_t base = g.head + g.nvec * VEC;
+    if (t < g.tail) visit(base + t, E::load(row + base + t));
+  } else if (cid >= 1 && cid <= nr + 1) {
+    const uint4* vp = reinterpret_cast<const uint4*>(row + g.head);
+    for (int u = 0; u < U; ++u) {
+      const int64_t j = (int64_t)(cid - 1) * U * BD + (int64_t)u * BD + t;
+      if (j < g.nvec) {
+        float f[VEC];
+        E::unpack(vp[j], f);
+        for (int e = 0; e < VEC; ++e) visit(g.head + j * VEC + e, f[e]);
+      }
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------- K1 confidence
+struct ConfArgs {
+  float l_ent, l_margin, l_soft, beta_m;
+};
+
+template <typename T, int BD>
+__global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits, int64_t n_rows, int64_t V,
+                                                   int64_t stride, ConfArgs a, cmsd_row_stats* __restrict__ out) {
+  using E = Elem<T>;
+  constexpr int VEC = E::VEC, U = E::U, N = VEC * U;
+  __shared__ double sd[BD / 64];
+  __shared__ float sf[BD / 64];
+  __shared__ int si[BD / 64];
+  __shared__ float s_other;
+  const int t = threadIdx.x;
+
+  for (int64_t r = blockIdx.x; r < n_rows; r += gridDim.x) {
+    const T* row = logits + r * stride;
+    const Geom g = row_geom(row, V);
+    const uint4* vp = reinterpret_cast<const uint4*>(row + g.head);
+    const int64_t per_round = (int64_t)U * BD;
+    const int64_t nr = g.nvec / per_round;
+
+    ConfState s;
+    if (t < g.head) conf_one(s, E::load(row + t), 0);
+
+    // full rounds, next round's loads issued before the current one is consumed
+    uint4 nxt[U];
+    if (nr > 0) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) nxt[u] = vp[u * BD + t];
+    }
+    for (int64_t k = 0; k < nr; ++k) {
+      uint4 cur[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) cur[u] = nxt[u];
+      if (k + 1 < nr) {
+        const uint4* q = vp + (k + 1) * per_round;
+#pragma unroll
+        for (int u = 0; u < U; ++u) nxt[u] = q[u * BD + t];
+      }
+      float f[N];
+#pragma unroll
+      for (int u = 0; u < U; ++u) E::unpack(cur[u], f + u * VEC);
+      conf_chunk<N, false>(s, f, 0xffffffffu, int(k + 1));
+    }
+    // partial round
+    const int64_t rb = nr * per_round;
+    if (rb < g.nvec) {
+      float f[N];
+      uint32_t valid = 0;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t j = rb + (int64_t)u * BD + t;
+        if (j < g.nvec) {
+          E::unpack(vp[j], f + u * VEC);
+          valid |= ((1u << VEC) - 1u) << (u * VEC);
+        } else {
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) f[u * VEC + e] = -INFINITY;
+        }
+      }
+      conf_chunk<N, true>(s, f, valid, int(nr + 1));
+    }
+    const int64_t tail0 = g.head + g.nvec * VEC;
+    if (t < g.tail) conf_one(s, E::load(row + tail0 + t), int(nr + 2));
+
+    // ---- epilogue: row max, first index of the max, second logit, normaliser
+    const float m = block_all_f<BD>(s.t1, OpMax(), sf);
+    const float ms_row = m * kLog2e;
+    const float d = s.n.ms - ms_row;
+    const float sc = fexp2(d);
+    const double Ad = (double)(s.n.A * sc);
+    const double Td = (double)(sc * fmaf(d, s.n.A, s.n.T));
+    const bool is_max = s.t1 == m;
+    int64_t idx = INT64_MAX;
+    float other = -INFINITY;
+    if (is_max) rescan_chunk<T, BD>(row, g, nr, s.gid, m, idx, other);
+    const float contrib = is_max ? s.t2 : s.t1;
+    const int idx32 = idx == INT64_MAX ? INT32_MAX : int(idx);
+
+    const double A = block_all_d<BD>(Ad, OpSumD(), sd);
+    double Tsum = block_all_d<BD>(Td, OpSumD(), sd);
+    const float cmx = block_all_f<BD>(contrib, OpMax(), sf);
+    const int nmax = block_all_i<BD>(is_max ? 1 : 0, OpSumI(), si);
+    const int top1 = block_all_i<BD>(idx32, OpMinI(), si);
+    if (idx32 == top1 && is_max) s_other = other;
+    uint32_t flags = 0;
+    if (Tsum != Tsum) {
+      // the row holds -inf logits: recompute T skipping them
+      flags |= 1u;
+      float tl = 0.f;
+      auto acc = [&](float z) {
+        if (z > -INFINITY) {
+          const float x = fmaf(z, kLog2e, -ms_row);
+          tl = fmaf(fexp2(x), x, tl);
+        }
+      };
+      if (t < g.head) acc(E::load(row + t));
+      for (int64_t j = t; j < g.nvec; j += BD) {
+        float f[VEC];
+        E::unpack(vp[j], f);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc(f[e]);
+      }
+      if (t < g.tail) acc(E::load(row + tail0 + t));
+      Tsum = block_all_d<BD>((double)tl, OpSumD(), sd);
+    }
+    __syncthreads();
+    if (t == 0) {
+      const float z2 = nmax >= 2 ? m : fmaxf(cmx, s_other);
+      const double Vd = (double)V;
+      const double Tn = Tsum * kLn2;
+      double H = log(A) - Tn / A;
+      H = H < 0.0 ? 0.0 : H;
+      const double dm = (double)m, dz2 = (double)z2;
+      const double margin = z2 == -INFINITY ? INFINITY : dm - dz2;
+      const double msoft = z2 == -INFINITY ? 1.0 / A : -expm1(dz2 - dm) / A;
+      const double c_ent = 1.0 - H / log(Vd);
+      const double tm = (double)a.beta_m * margin;
+      const double c_m = tm == INFINITY ? 1.0 : 1.0 / (1.0 + exp(-tm));
+      const double c_s = fmin(1.0, msoft / (1.0 - 1.0 / Vd));
+      const double C = (double)a.l_ent * c_ent + (double)a.l_margin * c_m + (double)a.l_soft * c_s;
+      cmsd_row_stats o;
+      o.max_logit = m;
+      o.sum_exp = (float)A;
+      o.entropy = (float)H;
+      o.margin_soft = (float)msoft;
+      o.margin_logit = (float)margin;
+      o.conf = (float)C;
+      o.top1 = top1;
+      o.flags = flags;
+      out[r] = o;
+    }
+    __syncthreads();
+  }
+}
+
+// ----------------------------------------------------------------------------- K2 draft length
+constexpr int kDraftBD = 1024;
+
+__global__ __launch_bounds__(kDraftBD) void k_draft_len(const cmsd_row_stats* __restrict__ stats, int B, int k_min,
+                                                        int k_max, float alpha, int32_t* __restrict__ k_out,
+                                                        int32_t* __restrict__ off_out) {
+  __shared__ int s_w[kDraftBD / 64];
+  const int t = threadIdx.x;
+  const int lane = t & 63, w = t >> 6;
+  int carry = 0;
+  for (int base = 0; base < B; base += kDraftBD) {
+    const int b = base + t;
+    int kb = 0;
+    if (b < B) {
+      const cmsd_row_stats* p = stats + (int64_t)b * k_max;
+      double s = 0.0;
+      for (int i = 0; i < k_max; ++i) s += (double)p[i].conf;
+      const double x = (double)alpha * (s / (double)k_max) * (double)k_max;
+      const double fl = floor(x);
+      int kf = fl < (double)k_min ? k_min : (fl > (double)k_max ? k_max : (int)fl);
+      kb = kf;
+      k_out[b] = kb;
+    }
+    // exclusive scan of (k_b + 1) over the tile: wave scan by shuffles, then wave totals
+    const int v = b < B ? kb + 1 : 0;
+    int incl = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int up = __shfl_up(incl, o);
+      if (lane >= o) incl += up;
+    }
+    __syncthreads();
+    if (lane == 63) s_w[w] = incl;
+    __syncthreads();
+    int wpre = 0, tot = 0;
+    for (int i = 0; i < kDraftBD / 64; ++i) {
+      if (i < w) wpre += s_w[i];
+      tot += s_w[i];
+    }
+    if (b < B) off_out[b] = carry + wpre + incl - v;
+    carry += tot;
+  }
+  if (t == 0) off_out[B] = carry;
+}
+
+// ----------------------------------------------------------------------------- K3 target rows
+struct VerifyArgs {
+  const void* draft;
+  int64_t dstride;
+  const cmsd_row_stats* dstats;
+  const void* target;
+  int64_t tstride;
+  int64_t target_rows;
+  const int32_t* off;
+  const int32_t* klen;
+  const int32_t* drafted;
+  const float* unif;
+  int B;
+  int k_max;
+  int64_t V;
+  int mode;
+  int beta;
+  float tau_base;
+  float gamma;
+  cmsd_target_stats* tstats;
+  int32_t* n_acc;
+  int32_t* next_tok;
+};
+
+struct TargetState {
+  NormState n;
+  float t1 = -INFINITY;
+};
+
+template <int N, bool GUARD, bool COUNT>
+__device__ __forceinline__ void target_chunk(TargetState& s, const float* f, uint32_t valid, float gz, int beta,
+                                             int& wcnt) {
+  const float cmax = chunk_max<N>(f);
+  s.t1 = fmaxf(s.t1, cmax);
+  norm_chunk<N, GUARD, false>(s.n, f, valid, cmax);
+  if (COUNT) {
+    // wave-uniform: skip chunks where no lane holds a logit above the drafted one,
+    // and stop once this wave alone has seen top_beta of them
+    if (wcnt < beta && __ballot(cmax > gz) != 0ull) {
+#pragma unroll
+      for (int j = 0; j < N; ++j) wcnt += __popcll(__ballot(f[j] > gz));
+    }
+  }
+}
+
+template <typename T, int BD, bool COUNT>
+__device__ __forceinline__ void target_stream(const T* row, const Geom& g, float gz, int beta, TargetState& s,
+                                              int& wcnt) {
+  using E = Elem<T>;
+  constexpr int VEC = E::VEC, U = E::U, N = VEC * U;
+  const int t = threadIdx.x;
+  const uint4* vp = reinterpret_cast<const uint4*>(row + g.head);
+  const int64_t per_round = (int64_t)U * BD;
+  const int64_t nr = g.nvec / per_round;
+  {
+    float f[1] = {t < g.head ? E::load(row + t) : -INFINITY};
+    target_chunk<1, true, COUNT>(s, f, t < g.head ? 1u : 0u, gz, beta, wcnt);
+  }
+  uint4 nxt[U];
+  if (nr > 0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) nxt[u] = vp[u * BD + t];
+  }
+  for (int64_t k = 0; k < nr; ++k) {
+    uint4 cur[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) cur[u] = nxt[u];
+    if (k + 1 < nr) {
+      const uint4* q = vp + (k + 1) * per_round;
+#pragma unroll
+      for (int u = 0; u < U; ++u) nxt[u] = q[u * BD + t];
+    }
+    float f[N];
+#pragma unroll
+    for (int u = 0; u < U; ++u) E::unpack(cur[u], f + u * VEC);
+    target_chunk<N, false, COUNT>(s, f, 0xffffffffu, gz, beta, wcnt);
+  }
+  const int64_t rb = nr * per_round;
+  if (rb < g.nvec) {
+    float f[N];
+    uint32_t valid = 0;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t j = rb + (int64_t)u * BD + t;
+      if (j < g.nvec) {
+        E::unpack(vp[j], f + u * VEC);
+        valid |= ((1u << VEC) - 1u) << (u * VEC);
+      } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) f[u * VEC + e] = -INFINITY;
+      }
+    }
+    target_chunk<N, true, COUNT>(s, f, valid, gz, beta, wcnt);
+  }
+  {
+    const int64_t tail0 = g.head + g.nvec * VEC;
+    float f[1] = {t < g.tail ? E::load(row + tail0 + t) : -INFINITY};
+    target_chunk<1, true, COUNT>(s, f, t < g.tail ? 1u : 0u, gz, beta, wcnt);
+  }
+}
+
+template <typename T, int BD>
+__global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
+  using E = Elem<T>;
+  __shared__ double sd[BD / 64];
+  __shared__ float sf[BD / 64];
+  __shared__ int si[BD / 64];
+  const int t = threadIdx.x;
+  const int64_t r = blockIdx.x;
+  const int total = a.off[a.B];
+  if (r >= total || r >= a.target_rows) return;
+
+  // sequence owning row r: number of offsets[1..B] that are <= r
+  int cnt = 0;
+  for (int j = 1 + t; j <= a.B; j += BD) cnt += a.off[j] <= r ? 1 : 0;
+  int b = block_all_i<BD>(cnt, OpSumI(), si);
+  b = b < a.B ? b : a.B - 1;
+  const int64_t off_b = a.off[b], off_b1 = a.off[b + 1];
+  const int kb = a.klen[b];
+  cmsd_target_stats* o = a.tstats + r;
+  const bool layout_ok = kb >= 0 && kb <= a.k_max && off_b >= 0 && off_b <= r && r < off_b1 &&
+                         off_b1 == off_b + kb + 1 && off_b1 <= a.target_rows;
+  if (!layout_ok) {
+    if (t == 0) *o = cmsd_target_stats{NAN, NAN, -1, -2};
+    return;
+  }
+  const int i = int(r - off_b);
+  const bool has_draft = i < kb;
+  const T* trow = reinterpret_cast<const T*>(a.target) + r * a.tstride;
+  int y = 0;
+  float gz = -INFINITY, zd = -INFINITY, cm = 0.f, dm = 0.f, dA = 1.f;
+  if (has_draft) {
+    const int64_t drow = (int64_t)b * a.k_max + i;
+    y = a.drafted[drow];
+    if (y < 0 || (int64_t)y >= a.V) {
+      if (t == 0) *o = cmsd_target_stats{NAN, NAN, -1, -2};
+      return;
+    }
+    gz = E::load(trow + y);
+    zd = E::load(reinterpret_cast<const T*>(a.draft) + drow * a.dstride + y);
+    const cmsd_row_stats ds = a.dstats[drow];
+    cm = ds.conf;
+    dm = ds.max_logit;
+    dA = ds.sum_exp;
+  }
+  const Geom g = row_geom(trow, a.V);
+  TargetState s;
+  int wcnt = 0;
+  const bool count = has_draft && a.mode == CMSD_MODE_CM && a.beta > 0;
+  if (count)
+    target_stream<T, BD, true>(trow, g, gz, a.beta, s, wcnt);
+  else
+    target_stream<T, BD, false>(trow, g, gz, a.beta, s, wcnt);
+
+  const float m = block_all_f<BD>(s.t1, OpMax(), sf);
+  const float ms_row = m * kLog2e;
+  const float sc = fexp2(s.n.ms - ms_row);
+  const double A = block_all_d<BD>((double)(s.n.A * sc), OpSumD(), sd);
+  const int ngt = block_all_i<BD>((t & 63) == 0 ? wcnt : 0, OpSumI(), si);
+  if (t == 0) {
+    cmsd_target_stats res;
+    res.max_logit = m;
+    res.sum_exp = (float)A;
+    if (!has_draft) {
+      res.n_greater = -1;
+      res.accept = -1;
+    } else {
+      // standard speculative sampling: u < p_t(y) / p_d(y), in logs and fp64
+      const double lpt = gz == -INFINITY ? -INFINITY : ((double)gz - (double)m) - log(A);
+      const double lpd = zd == -INFINITY ? -INFINITY : ((double)zd - (double)dm) - log((double)dA);
+      const float u = a.unif[r];
+      bool stoch;
+      if (lpt == -INFINITY) stoch = false;
+      else if (u == 0.f || lpd == -INFINITY) stoch = true;
+      else stoch = log((double)u) < lpt - lpd;
+      // confidence-modulated gate: top-beta inclusion and gap <= tau_base + gamma (1 - C)
+      const int ng = count ? (ngt < a.beta ? ngt : a.beta) : 0;
+      const double gap = gz == -INFINITY ? INFINITY : (double)m - (double)gz;
+      const double tau = (double)a.tau_base + (double)a.gamma * (1.0 - (double)cm);
+      const bool gate = count && ngt < a.beta && gap <= tau;
+      res.n_greater = ng;
+      res.accept = (stoch || (a.mode == CMSD_MODE_CM && gate)) ? 1 : 0;
+    }
+    *o = res;
+  }
+}
+
+// ----------------------------------------------------------------------------- K4 final token
+constexpr int kFinalBD = 1024;
+constexpr int kFinalG = 4;  // units loaded per batch in the span passes
+
+// A unit is the head (unit 0), one 16-byte vector (1..nvec) or the tail (nvec+1).
+template <typename T>
+__device__ __forceinline__ int unit_load(const T* row, const Geom& g, int64_t u, float* f) {
+  using E = Elem<T>;
+  constexpr int VEC = E::VEC;
+  if (u >= 1 && u <= g.nvec) {
+    E::unpack(reinterpret_cast<const uint4*>(row + g.head)[u - 1], f);
+    return VEC;
+  }
+  if (u == 0) {
+    for (int e = 0; e < VEC; ++e) f[e] = e < g.head ? E::load(row + e) : -INFINITY;
+    return g.head;
+  }
+  const int64_t base = g.head + g.nvec * VEC;
+  for (int e = 0; e < VEC; ++e) f[e] = e < g.tail ? E::load(row + base + e) : -INFINITY;
+  return g.tail;
+}
+template <typename T>
+__device__ __forceinline__ int64_t unit_first(const Geom& g, int64_t u) {
+  return u == 0 ? 0 : (u <= g.nvec ? g.head + (u - 1) * Elem<T>::VEC : g.head + g.nvec * Elem<T>::VEC);
+}
+// Elements [first, first+n) of a second row whose 16-byte phase may differ from the
+// row that defines the units: one vector load when aligned, element loads otherwise.
+template <typename T>
+__device__ __forceinline__ void range_load(const T* row, int64_t first, int n, float* f) {
+  using E = Elem<T>;
+  const T* p = row + first;
+  if (n == E::VEC && (reinterpret_cast<uintptr_t>(p) & 15u) == 0) {
+    E::unpack(*reinterpret_cast<const uint4*>(p), f);
+    return;
+  }
+  for (int e = 0; e < E::VEC; ++e) f[e] = e < n ? E::load(p + e) : -INFINITY;
+}
+
+// Sampling weights of one element.  RESID: max(0, e_t - rho*e_d); otherwise e_t.
+template <bool RESID>
+__device__ __forceinline__ double q_weight(float zt, float zd, float mst, float msd, double rho) {
+  const double et = (double)fexp2(fmaf(zt, kLog2e, -mst));
+  if (!RESID) return et;
+  const double ed = (double)fexp2(fmaf(zd, kLog2e, -msd));
+  const double q = fma(-rho, ed, et);
+  return q > 0.0 ? q : 0.0;
+}
+
+template <typename T, bool RESID>
+__device__ __forceinline__ double unit_sum(const T* trow, const T* drow, const Geom& g, int64_t u, float mst,
+                                           float msd, double rho) {
+  constexpr int VEC = Elem<T>::VEC;
+  float ft[VEC], fd[VEC];
+  const int n = unit_load(trow, g, u, ft);
+  if (RESID) range_load(drow, unit_first<T>(g, u), n, fd);
+  double s = 0.0;
+  for (int e = 0; e < n; ++e) s += q_weight<RESID>(ft[e], RESID ? fd[e] : 0.f, mst, msd, rho);
+  return s;
+}
+
+// Inverse-CDF sample over one row (or row pair).  Returns the token id, or -1 when
+// the total weight is zero (only possible for RESID).
+template <typename T, bool RESID>
+__device__ int sample_span(const T* trow, const T* drow, int64_t V, float mst, float msd, double rho, float u,
+                           double* sd, int* si, double* s_sc) {
+  constexpr int BD = kFinalBD;
+  constexpr int VEC = Elem<T>::VEC;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const Geom g = row_geom(trow, V);  // units follow the target row; the drafter row is read by range
+  const int64_t nu = g.nvec + 2;
+  const int64_t ulo = (int64_t)t * nu / BD, uhi = (int64_t)(t + 1) * nu / BD;
+
+  // per-thread sequential sum of its units, in unit order
+  double s = 0.0;
+  for (int64_t u0 = ulo; u0 < uhi; u0 += kFinalG) {
+    double us[kFinalG];
+#pragma unroll
+    for (int k = 0; k < kFinalG; ++k)
+      us[k] = (u0 + k < uhi) ? unit_sum<T, RESID>(trow, drow, g, u0 + k, mst, msd, rho) : 0.0;
+#pragma unroll
+    for (int k = 0; k < kFinalG; ++k)
+      if (u0 + k < uhi) s += us[k];
+  }
+  // exclusive scan over threads: wave scan by shuffles, then wave totals in order
+  double incl = s;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const double up = __shfl_up(incl, o);
+    if (lane >= o) incl += up;
+  }
+  double excl_w = __shfl_up(incl, 1);
+  if (lane == 0) excl_w = 0.0;
+  __syncthreads();
+  if (lane == 63) sd[w] = incl;
+  __syncthreads();
+  double wpre = 0.0;
+  for (int i = 0; i < w; ++i) wpre += sd[i];
+  const double excl = wpre + excl_w;
+  const double end = excl + s;
+  // R = end of the last thread holding weight; x = u R
+  const int tlast = block_all_i<BD>(s > 0.0 ? t : -1, OpMaxI(), si);
+  if (tlast < 0) return -1;
+  if (t == tlast) s_sc[0] = end;
+  __syncthreads();
+  const double R = s_sc[0];
+  const double x = (double)u * R;
+  const int tstar = block_all_i<BD>((s > 0.0 && end > x) ? t : INT32_MAX, OpMinI(), si);
+  if (t == tstar) s_sc[1] = excl;
+  __syncthreads();
+  int y = -1;
+  if (w == 0) {
+    // locate inside thread tstar's span with the same summation order
+    const double base = s_sc[1];
+    const int64_t lo = (int64_t)tstar * nu / BD, hi = (int64_t)(tstar + 1) * nu / BD;
+    double P = 0.0;
+    int64_t uj = -1;
+    for (int64_t ub = lo; ub < hi && uj < 0; ub += 64) {
+      const double v = (ub + lane < hi) ? unit_sum<T, RESID>(trow, drow, g, ub + lane, mst, msd, rho) : 0.0;
+      for (int l = 0; l < 64 && ub + l < hi; ++l) {
+        const double vl = rl_d(v, l);
+        const double Pn = P + vl;
+        if (vl > 0.0 && base + Pn > x) {
+          uj = ub + l;
+          break;
+        }
+        P = Pn;
+      }
+    }
+    if (uj >= 0) {
+      float ft[VEC], fd[VEC];
+      const int n = unit_load(trow, g, uj, ft);
+      const int64_t first = unit_first<T>(g, uj);
+      if (RESID) range_load(drow, first, n, fd);
+      double Q = 0.0;
+      for (int e = 0; e < n; ++e) {
+        const double q = q_weight<RESID>(ft[e], RESID ? fd[e] : 0.f, mst, msd, rho);
+        Q += q;
+        if (q > 0.0 && base + (P + Q) > x) {
+          y = int(first + e);
+          break;
+        }
+      }
+    }
+    if (lane == 0) si[0] = y;
+  }
+  __syncthreads();
+  y = si[0];
+  __syncthreads();
+  return y;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kFinalBD) void k_final(VerifyArgs a) {
+  using E = Elem<T>;
+  constexpr int BD = kFinalBD;
+  __shared__ double sd[BD / 64];
+  __shared__ int si[BD / 64];
+  __shared__ double s_sc[2];
+  __shared__ int s_nacc;
+  const int t = threadIdx.x, lane = t & 63;
+  const int b = blockIdx.x;
+  if (b >= a.B) return;
+  const int64_t off = a.off[b], off1 = a.off[b + 1];
+  const int kb = a.klen[b];
+  const bool ok = kb >= 0 && kb <= a.k_max && off >= 0 && off1 == off + kb + 1 && off1 <= a.target_rows;
+  if (!ok) {
+    if (t == 0) {
+      a.n_acc[b] = -1;
+      a.next_tok[b] = -1;
+    }
+    return;
+  }
+  // first rejected position by ballots over the accept flags (wave 0)
+  if (t < 64) {
+    int nacc = kb;
+    bool bad = a.tstats[off + kb].accept != -1;
+    for (int base = 0; base < kb; base += 64) {
+      const int i = base + lane;
+      const int acc = i < kb ? a.tstats[off + i].accept : 1;
+      const unsigned long long rej = __ballot(acc == 0);
+      if (__ballot(acc != 0 && acc != 1) != 0ull) bad = true;
+      if (rej != 0ull && nacc == kb) nacc = base + __builtin_ctzll(rej);
+    }
+    if (lane == 0) s_nacc = bad ? -1 : nacc;
+  }
+  __syncthreads();
+  const int nacc = s_nacc;
+  if (nacc < 0) {
+    if (t == 0) {
+      a.n_acc[b] = -1;
+      a.next_tok[b] = -1;
+    }
+    return;
+  }
+  const float u = a.unif[off + kb];
+  const T* tbase = reinterpret_cast<const T*>(a.target);
+  const T* dbase = reinterpret_cast<const T*>(a.draft);
+  int y = -1;
+  if (nacc < kb) {
+    const int64_t tr = off + nacc, dr = (int64_t)b * a.k_max + nacc;
+    const T* trow = tbase + tr * a.tstride;
+    const T* drow = dbase + dr * a.dstride;
+    const float mst = a.tstats[tr].max_logit * kLog2e;
+    const float msd = a.dstats[dr].max_logit * kLog2e;
+    // fresh, mutually consistent normalisers of both rows: rho = A_t / A_d
+    const Geom gt = row_geom(trow, a.V);
+    const int64_t nu = gt.nvec + 2;
+    const int64_t ulo = (int64_t)t * nu / BD, uhi = (int64_t)(t + 1) * nu / BD;
+    double st = 0.0, sdd = 0.0;
+    for (int64_t u0 = ulo; u0 < uhi; u0 += kFinalG) {
+      float at[kFinalG], ad[kFinalG];
+#pragma unroll
+      for (int k = 0; k < kFinalG; ++k) {
+        at[k] = 0.f;
+        ad[k] = 0.f;
+        if (u0 + k < uhi) {
+          float ft[E::VEC], fd[E::VEC];
+          const int n = unit_load(trow, gt, u0 + k, ft);
+          range_load(drow, unit_first<T>(gt, u0 + k), n, fd);
+          for (int e = 0; e < n; ++e) {
+            at[k] += fexp2(fmaf(ft[e], kLog2e, -mst));
+            ad[k] += fexp2(fmaf(fd[e], kLog2e, -msd));
+          }
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < kFinalG; ++k) {
+        st += (double)at[k];
+        sdd += (double)ad[k];
+      }
+    }
+    const double At = block_all_d<BD>(st, OpSumD(), sd);
+    const double Ad = block_all_d<BD>(sdd, OpSumD(), sd);
+    const double rho = At / Ad;
+    y = sample_span<T, true>(trow, drow, a.V, mst, msd, rho, u, sd, si, s_sc);
+    if (y == -1) y = sample_span<T, false>(trow, trow, a.V, mst, mst, 0.0, u, sd, si, s_sc);
+  } else {
+    const int64_t tr = off + kb;
+    const T* trow = tbase + tr * a.tstride;
+    const float mst = a.tstats[tr].max_logit * kLog2e;
+    y = sample_span<T, false>(trow, trow, a.V, mst, mst, 0.0, u, sd, si, s_sc);
+  }
+  if (t == 0) {
+    a.n_acc[b] = nacc;
+    a.next_tok[b] = y;
+  }
+}
+
+// ----------------------------------------------------------------------------- host helpers
+bool finite_f(float x) { return x == x && x != INFINITY && x != -INFINITY; }
+bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+cmsd_status launched() { return hipGetLastError() == hipSuccess ? CMSD_OK : CMSD_ERR_LAUNCH; }
+
+constexpr int kConfBD = 256;
+constexpr int kRowBD = 256;
+
+}  // namespace
+
+// ----------------------------------------------------------------------------- C ABI
+extern "C" {
+
+const char* cmsd_status_string(cmsd_status s) {
+  switch (s) {
+    case CMSD_OK: return "ok";
+    case CMSD_ERR_ARG: return "invalid argument";
+    case CMSD_ERR_DTYPE: return "unknown logit dtype";
+    case CMSD_ERR_LAUNCH: return "kernel launch failed";
+  }
+  return "unknown status";
+}
+
+int32_t cmsd_version(void) { return (1 << 16) | 0; }
+
+cmsd_status cmsd_confidence(const void* logits, int32_t dtype, int64_t n_rows, int64_t vocab, int64_t row_stride,
+                            const cmsd_conf_params* params, cmsd_row_stats* stats, void* stream) {
+  if (dtype != CMSD_F32 && dtype != CMSD_BF16) return CMSD_ERR_DTYPE;
+  if (!params) return CMSD_ERR_ARG;
+  if (n_rows < 0 || n_rows > INT32_MAX || vocab < 2 || vocab > INT32_MAX || row_stride < vocab) return CMSD_ERR_ARG;
+  const float l1 = params->lambda_ent, l2 = params->lambda_margin, l3 = params->lambda_soft;
+  if (!(l1 >= 0.f && l1 <= 1.f && l2 >= 0.f && l2 <= 1.f && l3 >= 0.f && l3 <= 1.f)) return CMSD_ERR_ARG;
+  if (fabs((double)l1 + (double)l2 + (double)l3 - 1.0) > 1e-6) return CMSD_ERR_ARG;
+  if (!finite_f(params->beta_margin) || !(params->beta_margin > 0.f)) return CMSD_ERR_ARG;
+  const size_t es = dtype == CMSD_F32 ? 4 : 2;
+  if (n_rows == 0) return CMSD_OK;
+  if (!logits || !stats || !aligned(logits, es) || !aligned(stats, 4)) return CMSD_ERR_ARG;
+  if (row_stride > INT64_MAX / n_rows) return CMSD_ERR_ARG;
+  const ConfArgs a{l1, l2, l3, params->beta_margin};
+  const dim3 grid((unsigned)n_rows), block(kConfBD);
+  if (dtype == CMSD_F32)
+    hipLaunchKernelGGL((k_confidence<float, kConfBD>), grid, block, 0, as_stream(stream),
+                       static_cast<const float*>(logits), n_rows, vocab, row_stride, a, stats);
+  else
+    hipLaunchKernelGGL((k_confidence<Bf16, kConfBD>), grid, block, 0, as_stream(stream),
+                       static_cast<const Bf16*>(logits), n_rows, vocab, row_stride, a, stats);
+  return launched();
+}
+
+cmsd_status cmsd_draft_len(const cmsd_row_stats* stats, int32_t batch, const cmsd_draft_params* params,
+                           int32_t* draft_len, int32_t* target_offsets, void* stream) {
+  if (!params || batch < 0) return CMSD_ERR_ARG;
+  const int k_min = params->k_min, k_max = params->k_max;
+  if (k_min < 1 || k_min > k_max || k_max > 4096) return CMSD_ERR_ARG;
+  if (!finite_f(params->alpha) || !(params->alpha > 0.f) || !(params->alpha <= 1.f)) return CMSD_ERR_ARG;
+  if ((int64_t)batch * (k_max + 1) > INT32_MAX) return CMSD_ERR_ARG;
+  if (!target_offsets || !aligned(target_offsets, 4)) return CMSD_ERR_ARG;
+  if (batch > 0 && (!stats || !draft_len || !aligned(stats, 4) || !aligned(draft_len, 4))) return CMSD_ERR_ARG;
+  hipLaunchKernelGGL(k_draft_len, dim3(1), dim3(kDraftBD), 0, as_stream(stream), stats, batch, k_min, k_max,
+                     params->alpha, draft_len, target_offsets);
+  return launched();
+}
+
+cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cmsd_row_stats* draft_stats,
+                        const void* target_logits, int64_t target_stride, int64_t target_rows,
+                        const int32_t* target_offsets, const int32_t* draft_len, const int32_t* drafted,
+                        const float* uniforms, int32_t dtype, int32_t batch, int32_t k_max, int64_t vocab,
+                        const cmsd_verify_params* params, cmsd_target_stats* target_stats, int32_t* n_accepted,
+                        int32_t* next_token, void* stream) {
+  if (dtype != CMSD_F32 && dtype != CMSD_BF16) return CMSD_ERR_DTYPE;
+  if (!params) return CMSD_ERR_ARG;
+  if (batch < 0 || k_max < 1 || k_max > 4096 || vocab < 2 || vocab > INT32_MAX) return CMSD_ERR_ARG;
+  if (params->mode != CMSD_MODE_STANDARD && params->mode != CMSD_MODE_CM) return CMSD_ERR_ARG;
+  if (params->top_beta < 0 || !finite_f(params->tau_base) || !finite_f(params->gamma)) return CMSD_ERR_ARG;
+  if (batch == 0) return CMSD_OK;
+  if (target_rows < 1 || target_rows > INT32_MAX) return CMSD_ERR_ARG;
+  if (draft_stride < vocab || target_stride < vocab) return CMSD_ERR_ARG;
+  if ((int64_t)batch * k_max > INT32_MAX) return CMSD_ERR_ARG;
+  const size_t es = dtype == CMSD_F32 ? 4 : 2;
+  if (!draft_logits || !draft_stats || !target_logits || !target_offsets || !draft_len || !drafted || !uniforms ||
+      !target_stats || !n_accepted || !next_token)
+    return CMSD_ERR_ARG;
+  if (!aligned(draft_logits, es) || !aligned(target_logits, es) || !aligned(draft_stats, 4) ||
+      !aligned(target_offsets, 4) || !aligned(draft_len, 4) || !aligned(drafted, 4) || !aligned(uniforms, 4) ||
+      !aligned(target_stats, 4) || !aligned(n_accepted, 4) || !aligned(next_token, 4))
+    return CMSD_ERR_ARG;
+  VerifyArgs a;
+  a.draft = draft_logits;
+  a.dstride = draft_stride;
+  a.dstats = draft_stats;
+  a.target = target_logits;
+  a.tstride = target_stride;
+  a.target_rows = target_rows;
+  a.off = target_offsets;
+  a.klen = draft_len;
+  a.drafted = drafted;
+  a.unif = uniforms;
+  a.B = batch;
+  a.k_max = k_max;
+  a.V = vocab;
+  a.mode = params->mode;
+  a.beta = params->top_beta;
+  a.tau_base = params->tau_base;
+  a.gamma = params->gamma;
+  a.tstats = target_stats;
+  a.n_acc = n_accepted;
+  a.next_tok = next_token;
+  const hipStream_t st = as_stream(stream);
+  if (dtype == CMSD_F32) {
+    hipLaunchKernelGGL((k_target_rows<float, kRowBD>), dim3((unsigned)target_rows), dim3(kRowBD), 0, st, a);
+    if (launched() != CMSD_OK) return CMSD_ERR_LAUNCH;
+    hipLaunchKernelGGL((k_final<float>), dim3((unsigned)batch), dim3(kFinalBD), 0, st, a);
+  } else {
+    hipLaunchKernelGGL((k_target_rows<Bf16, kRowBD>), dim3((unsigned)target_rows), dim3(kRowBD), 0, st, a);
+    if (launched() != CMSD_OK) return CMSD_ERR_LAUNCH;
+    hipLaunchKernelGGL((k_final<Bf16>), dim3((unsigned)batch), dim3(kFinalBD), 0, st, a);
+  }
+  return launched();
+}
+
+}  // extern "C"

@@ -1,0 +1,74 @@
+"""One decoding iteration of the logit pass: confidence -> draft length -> verify.
+
+``LogitPass`` preallocates every output once, then ``run`` enqueues the three C
+entry points on one stream (no host synchronisation, no allocation), so it can be
+timed or captured as is.  Only marshalling happens here.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import torch
+
+from . import cmsd
+
+
+@dataclass
+class Params:
+    lambdas: tuple = (1 / 3, 1 / 3, 1 / 3)
+    beta_margin: float = 1.0
+    k_min: int = 1
+    alpha: float = 1.0
+    mode: int = cmsd.CMSD_MODE_CM
+    top_beta: int = 3
+    tau_base: float = 0.1
+    gamma: float = 1.0
+
+
+class LogitPass:
+    """Buffers and calls for B sequences of k_max drafted positions over vocab V.
+
+    ``dense=True``: the verifier scored all k_max+1 positions of every sequence, so
+    verify runs with k_b = k_max and offsets b*(k_max+1) (the draft lengths are still
+    computed and returned).  ``dense=False``: verify consumes the device-computed
+    k_b and offsets; the caller supplies target rows and uniforms packed by those
+    offsets (``target_rows`` allocated rows, at most B*(k_max+1)).
+    """
+
+    def __init__(self, B: int, k_max: int, V: int, device, params: Params | None = None,
+                 dense: bool = True, target_rows: int | None = None):
+        self.B, self.k_max, self.V = B, k_max, V
+        self.p = params or Params()
+        self.dense = dense
+        dev = torch.device(device)
+        self.target_rows = target_rows or B * (k_max + 1)
+        self.stats = torch.empty((B * k_max, 8), dtype=torch.float32, device=dev)
+        self.k = torch.empty(B, dtype=torch.int32, device=dev)
+        self.off = torch.empty(B + 1, dtype=torch.int32, device=dev)
+        self.k_dense = torch.full((B,), k_max, dtype=torch.int32, device=dev)
+        self.off_dense = (torch.arange(B + 1, dtype=torch.int32, device=dev) * (k_max + 1)).contiguous()
+        self.tstats = torch.empty((self.target_rows, 4), dtype=torch.float32, device=dev)
+        self.n_acc = torch.empty(B, dtype=torch.int32, device=dev)
+        self.next_tok = torch.empty(B, dtype=torch.int32, device=dev)
+
+    def confidence(self, draft: torch.Tensor, stream=None) -> None:
+        cmsd.cmsd_confidence(draft, self.stats, lambdas=self.p.lambdas, beta_margin=self.p.beta_margin,
+                             stream=stream)
+
+    def draft_len(self, stream=None) -> None:
+        cmsd.cmsd_draft_len(self.stats, self.B, k_min=self.p.k_min, k_max=self.k_max, alpha=self.p.alpha,
+                            draft_len=self.k, target_offsets=self.off, stream=stream)
+
+    def verify(self, draft: torch.Tensor, target: torch.Tensor, drafted: torch.Tensor, uniforms: torch.Tensor,
+               stream=None) -> None:
+        k, off = (self.k_dense, self.off_dense) if self.dense else (self.k, self.off)
+        cmsd.cmsd_verify(draft, self.stats, target, off, k, drafted, uniforms, batch=self.B, k_max=self.k_max,
+                         mode=self.p.mode, top_beta=self.p.top_beta, tau_base=self.p.tau_base,
+                         gamma=self.p.gamma, target_stats=self.tstats, n_accepted=self.n_acc,
+                         next_token=self.next_tok, stream=stream)
+
+    def run(self, draft, target, drafted, uniforms, stream=None) -> None:
+        """confidence + draft_len + verify, enqueued on ``stream``."""
+        self.confidence(draft, stream)
+        self.draft_len(stream)
+        self.verify(draft, target, drafted, uniforms, stream)

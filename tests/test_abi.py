@@ -1,0 +1,95 @@
+"""The C ABI on the host: the library loads, exports every declared entry point, and
+rejects invalid arguments before enqueuing anything (no GPU needed: these calls
+return before any HIP call)."""
+import ctypes as C
+
+import pytest
+
+cm = pytest.importorskip("paper_2508_15371_amd.cmsd")
+
+P = 0x10000          # fake, aligned device addresses: never dereferenced on these paths
+
+
+def test_exports_every_declared_symbol():
+    syms = cm.header_symbols()
+    assert set(syms) >= {"cmsd_confidence", "cmsd_draft_len", "cmsd_verify", "cmsd_status_string", "cmsd_version"}
+    lib = cm.lib()
+    for s in syms:
+        assert hasattr(lib, s), s
+    assert lib.cmsd_version() >> 16 == 1
+    assert lib.cmsd_status_string(0) == b"ok"
+    assert lib.cmsd_status_string(1) == b"invalid argument"
+
+
+def _conf(**kw):
+    a = dict(logits=P, dtype=cm.CMSD_BF16, n=4, V=1024, stride=1024, p=cm.ConfParams(0.25, 0.25, 0.5, 1.0), out=P)
+    a.update(kw)
+    return cm.lib().cmsd_confidence(a["logits"], a["dtype"], a["n"], a["V"], a["stride"],
+                                    C.byref(a["p"]) if a["p"] is not None else None, a["out"], None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(dtype=5), cm.CMSD_ERR_DTYPE),
+    (dict(p=None), cm.CMSD_ERR_ARG),
+    (dict(V=1), cm.CMSD_ERR_ARG),
+    (dict(stride=1000), cm.CMSD_ERR_ARG),
+    (dict(n=-1), cm.CMSD_ERR_ARG),
+    (dict(logits=None), cm.CMSD_ERR_ARG),
+    (dict(out=None), cm.CMSD_ERR_ARG),
+    (dict(logits=P + 1), cm.CMSD_ERR_ARG),                       # misaligned bf16 pointer
+    (dict(p=cm.ConfParams(0.5, 0.5, 0.5, 1.0)), cm.CMSD_ERR_ARG),  # weights do not sum to 1
+    (dict(p=cm.ConfParams(-0.1, 0.6, 0.5, 1.0)), cm.CMSD_ERR_ARG),
+    (dict(p=cm.ConfParams(0.25, 0.25, 0.5, 0.0)), cm.CMSD_ERR_ARG),  # beta_margin must be > 0
+    (dict(p=cm.ConfParams(0.25, 0.25, 0.5, float("inf"))), cm.CMSD_ERR_ARG),
+    (dict(n=0, logits=None, out=None), cm.CMSD_OK),             # empty input: nothing enqueued
+])
+def test_confidence_argument_errors(kw, want):
+    assert _conf(**kw) == want
+
+
+@pytest.mark.parametrize("k_min,k_max,alpha,batch,want", [
+    (0, 8, 1.0, 4, cm.CMSD_ERR_ARG),
+    (9, 8, 1.0, 4, cm.CMSD_ERR_ARG),
+    (1, 5000, 1.0, 4, cm.CMSD_ERR_ARG),
+    (1, 8, 0.0, 4, cm.CMSD_ERR_ARG),
+    (1, 8, 1.5, 4, cm.CMSD_ERR_ARG),
+    (1, 8, float("nan"), 4, cm.CMSD_ERR_ARG),
+    (1, 8, 1.0, -1, cm.CMSD_ERR_ARG),
+])
+def test_draft_len_argument_errors(k_min, k_max, alpha, batch, want):
+    p = cm.DraftParams(k_min, k_max, alpha)
+    assert cm.lib().cmsd_draft_len(P, batch, C.byref(p), P, P, None) == want
+
+
+def _verify(**kw):
+    a = dict(dl=P, ds=1024, dst=P, tl=P, ts=1024, trows=90, off=P, k=P, dr=P, u=P, dtype=cm.CMSD_BF16,
+             B=10, K=8, V=1024, p=cm.VerifyParams(1, 3, 0.1, 1.0), tst=P, na=P, nt=P)
+    a.update(kw)
+    return cm.lib().cmsd_verify(a["dl"], a["ds"], a["dst"], a["tl"], a["ts"], a["trows"], a["off"], a["k"],
+                                a["dr"], a["u"], a["dtype"], a["B"], a["K"], a["V"],
+                                C.byref(a["p"]) if a["p"] is not None else None, a["tst"], a["na"], a["nt"],
+                                None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(dtype=9), cm.CMSD_ERR_DTYPE),
+    (dict(p=None), cm.CMSD_ERR_ARG),
+    (dict(p=cm.VerifyParams(2, 3, 0.1, 1.0)), cm.CMSD_ERR_ARG),
+    (dict(p=cm.VerifyParams(1, -1, 0.1, 1.0)), cm.CMSD_ERR_ARG),
+    (dict(p=cm.VerifyParams(1, 3, float("inf"), 1.0)), cm.CMSD_ERR_ARG),
+    (dict(p=cm.VerifyParams(1, 3, 0.1, float("nan"))), cm.CMSD_ERR_ARG),
+    (dict(K=0), cm.CMSD_ERR_ARG),
+    (dict(K=5000), cm.CMSD_ERR_ARG),
+    (dict(V=1), cm.CMSD_ERR_ARG),
+    (dict(ds=1000), cm.CMSD_ERR_ARG),
+    (dict(ts=1000), cm.CMSD_ERR_ARG),
+    (dict(trows=0), cm.CMSD_ERR_ARG),
+    (dict(B=-2), cm.CMSD_ERR_ARG),
+    (dict(u=None), cm.CMSD_ERR_ARG),
+    (dict(na=None), cm.CMSD_ERR_ARG),
+    (dict(tl=P + 1), cm.CMSD_ERR_ARG),
+    (dict(dr=P + 2), cm.CMSD_ERR_ARG),
+    (dict(B=0, dl=None, tl=None), cm.CMSD_OK),
+])
+def test_verify_argument_errors(kw, want):
+    assert _verify(**kw) == want

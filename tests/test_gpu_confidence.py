@@ -1,0 +1,107 @@
+"""GPU parity of cmsd_confidence (Sec. III.B(1)) against the oracle, through the C ABI."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import cmsd_oracle as O
+from tests import harness as Hn
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def cm():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2508_15371_amd import cmsd
+    return cmsd
+
+
+def _invariant_rows(V: int, g: np.random.Generator) -> list:
+    rows = []
+    rows.append(np.full(V, 0.5))                                  # uniform
+    z = np.full(V, -math.inf); z[g.integers(0, V)] = 1.0; rows.append(z)     # one-hot, masked
+    z = np.full(V, -800.0); z[V - 1] = 0.0; rows.append(z)        # one-hot by a huge gap
+    for d in (0.0, 0.5, 3.0):                                     # two finite logits
+        z = np.full(V, -math.inf); z[0] = 2.0 + d; z[V // 2] = 2.0; rows.append(z)
+    z = g.integers(-2, 2, V).astype(np.float64); rows.append(z)  # heavy ties
+    z = g.normal(0, 3, V); z[g.random(V) < 0.3] = -math.inf; z[int(np.argmax(z))] = 9.0; rows.append(z)
+    z = g.normal(0, 1, V); z[[3 % V, (V - 2) % V]] = 7.0; rows.append(z)      # duplicate max
+    rows.append(g.normal(0, 0.01, V))                            # nearly flat
+    rows.append(g.normal(0, 20, V))                              # very sharp
+    z = g.normal(0, 1, V); z[V - 1] = 30.0; rows.append(z)        # max in the tail
+    return rows
+
+
+def _store(rows, dtype):
+    x = np.stack(rows).astype(np.float32)
+    return x if dtype == "f32" else W.bf16_bits_from_f32(x)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("V", [2, 3, 7, 8, 9, 31, 255, 1023, 1024, 1025, 4099, 32000, 50257, 131072 + 17])
+@pytest.mark.parametrize("pad", [0, 5])
+def test_invariant_rows(cm, dtype, V, pad):
+    g = np.random.default_rng(V * 7 + pad)
+    stored = _store(_invariant_rows(V, g), dtype)
+    n = stored.shape[0]
+    buf = np.zeros((n, V + pad), dtype=stored.dtype)
+    buf[:, :V] = stored
+    dev = torch.device("cuda:0")
+    tdev = Hn.to_device(buf, dtype, dev)[:, :V]
+    lam = (0.2, 0.5, 0.3)
+    st = cm.cmsd_confidence(tdev, lambdas=lam, beta_margin=0.7)
+    torch.cuda.synchronize()
+    gs = Hn.stats_np(st)
+    t = Hn.Tally()
+    lam32 = tuple(Hn.f32(x) for x in lam)
+    for r in range(n):
+        Hn.check_row_stats(t, gs, r, Hn.decode(stored[r], dtype), V, lam32, Hn.f32(0.7))
+    t.assert_ok()
+
+
+def _sample_rows(cfg, k):
+    n = cfg.draft_rows
+    if n <= k:
+        return list(range(n))
+    g = np.random.default_rng(cfg.cid)
+    return sorted(set([0, n - 1] + g.choice(n, k, replace=False).tolist()))
+
+
+@pytest.mark.parametrize("name,nsample", [("tiny", 99), ("c2", 99), ("c3", 512), ("c4", 40), ("c5", 48)])
+def test_config_rows(cm, name, nsample):
+    cfg = W.CONFIGS[name]
+    print(f"[confidence parity] {name}", flush=True)
+    d = Hn.workload(name, 0)
+    dev = torch.device("cuda:0")
+    draft = d["draft_dev"]
+    st = cm.cmsd_confidence(draft)
+    torch.cuda.synchronize()
+    gs = Hn.stats_np(st)
+    t = Hn.Tally()
+    lam = tuple(Hn.f32(1 / 3) for _ in range(3))
+    for r in _sample_rows(cfg, nsample):
+        Hn.check_row_stats(t, gs, r, Hn.decode(d["draft"][r], cfg.dtype), cfg.V, lam, 1.0)
+    t.assert_ok()
+
+
+def test_repeat_bitwise_identical(cm):
+    d = Hn.workload("c3", 0)
+    a = cm.cmsd_confidence(d["draft_dev"]).clone()
+    b = cm.cmsd_confidence(d["draft_dev"]).clone()
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+def test_empty_and_errors(cm):
+    dev = torch.device("cuda:0")
+    x = torch.zeros((0, 100), device=dev)
+    st = cm.cmsd_confidence(x)
+    assert st.shape == (0, 8)
+    with pytest.raises(cm.CmsdError):
+        cm.cmsd_confidence(torch.zeros((4, 1), device=dev))            # V < 2
+    with pytest.raises(cm.CmsdError):
+        cm.cmsd_confidence(torch.zeros((4, 16), device=dev), lambdas=(0.5, 0.5, 0.5))

@@ -1,0 +1,226 @@
+"""GPU parity of cmsd_draft_len (Sec. III.B(b)) and cmsd_verify (Sec. III.A, III.B(c))
+against the oracle, through the C ABI, on the five workloads and edge cases."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import cmsd_oracle as O
+from tests import harness as Hn
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def mods():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2508_15371_amd import cmsd, pipeline
+    return cmsd, pipeline
+
+
+def _params(pipeline, mode):
+    P = Hn.PARAMS
+    return pipeline.Params(lambdas=P["lambdas"], beta_margin=P["beta_margin"], k_min=P["k_min"], alpha=P["alpha"],
+                           mode=mode, top_beta=P["top_beta"], tau_base=P["tau_base"], gamma=P["gamma"])
+
+
+def _run(mods, name, mode, seed=0):
+    cmsd, pipeline = mods
+    cfg = W.CONFIGS[name]
+    d = Hn.workload(name, seed)
+    lp = pipeline.LogitPass(cfg.B, cfg.k_max, cfg.V, "cuda:0", _params(pipeline, mode), dense=not cfg.ragged)
+    lp.confidence(d["draft_dev"])
+    lp.draft_len()
+    if cfg.ragged:
+        target = W.pack_device(d["target_dev"], lp.k, lp.off, cfg.k_max)
+        unif = W.pack_device(d["unif_dev"], lp.k, lp.off, cfg.k_max)
+    else:
+        target, unif = d["target_dev"], d["unif_dev"]
+    lp.verify(d["draft_dev"], target, d["drafted_dev"], unif)
+    torch.cuda.synchronize()
+    return cfg, d, lp
+
+
+def _sample_seqs(cfg, n):
+    if cfg.B <= n:
+        return list(range(cfg.B))
+    g = np.random.default_rng(100 + cfg.cid)
+    return sorted(set([0, cfg.B - 1] + g.choice(cfg.B, n, replace=False).tolist()))
+
+
+def _check_draft_len(t, cfg, d, gs, k_gpu, off_gpu, seqs):
+    K = cfg.k_max
+    P = Hn.PARAMS
+    # stage isolation: the oracle's draft length on the GPU's confidences is bit-exact
+    Cg = gs["C"].astype(np.float64).reshape(cfg.B, K)
+    k_o, off_o, _ = O.draft_len(Cg, P["k_min"], K, Hn.f32(P["alpha"]))
+    t.value("k(stage)", np.array_equal(k_o, k_gpu), (k_o[:8], k_gpu[:8]))
+    t.value("off(stage)", np.array_equal(off_o, off_gpu), (off_o[:8], off_gpu[:8]))
+    # end to end on sampled sequences: the oracle's own confidences
+    for b in seqs:
+        C = np.array([[Hn.oracle_conf(Hn.decode(d["draft"][b * K + i], cfg.dtype), cfg.V) for i in range(K)]])
+        kb, _, sl = O.draft_len(C, P["k_min"], K, Hn.f32(P["alpha"]))
+        t.decision(f"k[{b}]", int(k_gpu[b]), int(kb[0]), float(sl[0]))
+
+
+def _verify_check(mods, name, mode, nseq):
+    cfg, d, lp = _run(mods, name, mode)
+    K, V = cfg.k_max, cfg.V
+    gs = Hn.stats_np(lp.stats)
+    ts = Hn.tstats_np(lp.tstats)
+    k_gpu = lp.k.cpu().numpy()
+    off_gpu = lp.off.cpu().numpy()
+    n_acc = lp.n_acc.cpu().numpy()
+    nxt = lp.next_tok.cpu().numpy()
+    t = Hn.Tally()
+    seqs = _sample_seqs(cfg, nseq)
+    _check_draft_len(t, cfg, d, gs, k_gpu, off_gpu, seqs[: max(4, len(seqs) // 2)])
+    for b in seqs:
+        kb = int(k_gpu[b]) if cfg.ragged else K
+        toff = int(off_gpu[b]) if cfg.ragged else b * (K + 1)
+        zd = [Hn.decode(d["draft"][b * K + i], cfg.dtype) for i in range(K)]
+        pos = list(range(kb)) + [K]
+        zt = [Hn.decode(d["target"][b * (K + 1) + i], cfg.dtype) for i in pos]
+        unif = [float(d["uniforms"][b, i]) for i in pos]
+        C = [Hn.oracle_conf(z, V) for z in zd]
+        Hn.check_sequence(t, b, zt, zd, d["drafted"][b], unif, C, kb, mode, Hn.PARAMS, ts, toff,
+                          int(n_acc[b]), int(nxt[b]))
+    print(f"[verify parity] {name} mode={mode}: checked={t.checked} exceptions={t.exceptions} "
+          f"mean n_acc={n_acc.mean():.3f} mean k={k_gpu.mean():.3f}", flush=True)
+    t.assert_ok()
+    return t
+
+
+@pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM])
+@pytest.mark.parametrize("name,nseq", [("tiny", 1), ("c2", 8), ("c3", 64), ("c4", 6), ("c5", 24)])
+def test_verify_configs(mods, name, nseq, mode):
+    print(f"[verify parity] start {name} mode={mode}", flush=True)
+    _verify_check(mods, name, mode, nseq)
+
+
+def test_verify_repeat_bitwise_identical(mods):
+    cfg, d, lp = _run(mods, "c3", O.MODE_CM)
+    a = (lp.n_acc.clone(), lp.next_tok.clone(), lp.tstats.clone())
+    cfg, d, lp2 = _run(mods, "c3", O.MODE_CM)
+    assert torch.equal(a[0], lp2.n_acc) and torch.equal(a[1], lp2.next_tok)
+    assert torch.equal(a[2].view(torch.int32), lp2.tstats.view(torch.int32))
+
+
+# ----------------------------------------------------------------------------- edge cases
+def _small_case(g, B, K, V, dtype, scale=2.0):
+    zd = (g.normal(0, scale, (B * K, V))).astype(np.float32)
+    zt = (g.normal(0, scale, (B * (K + 1), V))).astype(np.float32)
+    for b in range(B):
+        for i in range(K):
+            zt[b * (K + 1) + i] = zd[b * K + i] + g.normal(0, 0.5, V).astype(np.float32)
+    store = (lambda x: x) if dtype == "f32" else W.bf16_bits_from_f32
+    drafted = np.array([[int(np.argmax(Hn.decode(store(zd[b * K + i]), dtype) + g.gumbel(size=V)))
+                         for i in range(K)] for b in range(B)], dtype=np.int32)
+    unif = (g.integers(0, 1 << 24, (B, K + 1)) * 2.0 ** -24).astype(np.float32)
+    return store(zd), store(zt), drafted, unif
+
+
+def _run_small(mods, zd, zt, drafted, unif, k, dtype, B, K, V, mode=O.MODE_CM, top_beta=3, tau_base=0.1,
+               gamma=1.0, off=None):
+    cmsd, _ = mods
+    dev = torch.device("cuda:0")
+    dd = Hn.to_device(zd, dtype, dev)
+    td = Hn.to_device(zt, dtype, dev)
+    st = cmsd.cmsd_confidence(dd)
+    if off is None:
+        off = np.concatenate([[0], np.cumsum(np.asarray(k) + 1)]).astype(np.int32)
+    n_acc, nxt, ts = cmsd.cmsd_verify(
+        dd, st, td, torch.from_numpy(off).to(dev), torch.from_numpy(np.asarray(k, dtype=np.int32)).to(dev),
+        torch.from_numpy(drafted.reshape(-1)).to(dev), torch.from_numpy(unif.reshape(-1)).to(dev),
+        batch=B, k_max=K, mode=mode, top_beta=top_beta, tau_base=tau_base, gamma=gamma)
+    torch.cuda.synchronize()
+    return Hn.stats_np(st), n_acc.cpu().numpy(), nxt.cpu().numpy(), Hn.tstats_np(ts)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("V", [2, 5, 64, 1000, 4097, 32003])
+@pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM])
+def test_ragged_lengths_small_vocab(mods, dtype, V, mode):
+    # packed target rows with every draft length 0..K (k_b = 0: bonus sample only)
+    g = np.random.default_rng(V + 31 * mode)
+    B, K = 6, 5
+    zd, zt_pad, drafted, unif_pad = _small_case(g, B, K, V, dtype)
+    k = np.array([0, 1, 5, 3, 2, 4], dtype=np.int32)
+    zt = W.pack_ragged(k, K, zt_pad.reshape(B, K + 1, V))
+    unif = W.pack_ragged(k, K, unif_pad.reshape(B, K + 1, 1)).reshape(-1)
+    off = np.concatenate([[0], np.cumsum(k + 1)]).astype(np.int32)
+    gs, n_acc, nxt, ts = _run_small(mods, zd, zt, drafted, unif, k, dtype, B, K, V, mode=mode)
+    t = Hn.Tally()
+    for b in range(B):
+        kb = int(k[b])
+        zdr = [Hn.decode(zd[b * K + i], dtype) for i in range(K)]
+        ztr = [Hn.decode(zt[off[b] + i], dtype) for i in range(kb + 1)]
+        C = [Hn.oracle_conf(z, V) for z in zdr]
+        Hn.check_sequence(t, b, ztr, zdr, drafted[b], unif[off[b]:off[b] + kb + 1], C, kb, mode, Hn.PARAMS,
+                          ts, int(off[b]), int(n_acc[b]), int(nxt[b]))
+    t.assert_ok()
+
+
+def test_equal_rows_accept_everything_and_masked_targets(mods):
+    g = np.random.default_rng(5)
+    B, K, V = 4, 6, 3000
+    zd, zt, drafted, unif = _small_case(g, B, K, V, "bf16")
+    for b in range(B):
+        for i in range(K):
+            zt[b * (K + 1) + i] = zd[b * K + i]
+    unif[:, :K] = np.float32(1.0 - 2.0 ** -24)
+    k = np.full(B, K, dtype=np.int32)
+    for mode in (O.MODE_STANDARD, O.MODE_CM):
+        _, n_acc, nxt, ts = _run_small(mods, zd, zt, drafted, unif, k, "bf16", B, K, V, mode=mode)
+        assert (n_acc == K).all()
+    # a drafted token with zero target mass is always rejected
+    zt2 = zt.copy()
+    ninf = W.bf16_bits_from_f32(np.array([-np.inf], dtype=np.float32))[0]
+    for b in range(B):
+        zt2[b * (K + 1) + 2, drafted[b, 2]] = ninf
+    unif2 = np.zeros_like(unif)
+    _, n_acc, nxt, ts = _run_small(mods, zd, zt2, drafted, unif2, k, "bf16", B, K, V, mode=O.MODE_CM,
+                                   top_beta=V, tau_base=1e30, gamma=0.0)
+    assert (n_acc == 2).all()
+    for b in range(B):
+        assert Hn.decode(zt2[b * (K + 1) + 2], "bf16")[nxt[b]] > -math.inf
+
+
+def test_invalid_device_inputs_are_reported(mods):
+    g = np.random.default_rng(6)
+    B, K, V = 4, 3, 500
+    zd, zt, drafted, unif = _small_case(g, B, K, V, "f32")
+    k = np.full(B, K, dtype=np.int32)
+    drafted_bad = drafted.copy()
+    drafted_bad[1, 1] = V            # out of range id
+    drafted_bad[2, 0] = -5
+    _, n_acc, nxt, _ = _run_small(mods, zd, zt, drafted_bad, unif, k, "f32", B, K, V)
+    assert n_acc[1] == -1 and nxt[1] == -1 and n_acc[2] == -1 and nxt[2] == -1
+    assert n_acc[0] >= 0 and n_acc[3] >= 0
+    k_bad = k.copy()
+    k_bad[3] = K + 1                 # longer than k_max
+    off = np.arange(B + 1, dtype=np.int32) * (K + 1)
+    _, n_acc, nxt, _ = _run_small(mods, zd, zt, drafted, unif, k_bad, "f32", B, K, V, off=off)
+    assert n_acc[3] == -1 and (n_acc[:3] >= 0).all()
+    off_bad = off.copy()
+    off_bad[B] = B * (K + 1) + 50    # beyond the allocated target rows
+    _, n_acc, nxt, _ = _run_small(mods, zd, zt, drafted, unif, k, "f32", B, K, V, off=off_bad)
+    assert n_acc[B - 1] == -1 and (n_acc[: B - 1] >= 0).all()
+
+
+def test_draft_len_edges(mods):
+    cmsd, _ = mods
+    dev = torch.device("cuda:0")
+    g = np.random.default_rng(8)
+    for B, K, kmin, alpha in ((0, 4, 1, 1.0), (1, 1, 1, 1.0), (3000, 16, 2, 0.61), (700, 7, 7, 0.3)):
+        C = g.uniform(0, 1, B * K).astype(np.float32)
+        st = torch.zeros((B * K, 8), dtype=torch.float32)
+        st[:, 5] = torch.from_numpy(C)
+        k, off = cmsd.cmsd_draft_len(st.to(dev), B, k_min=kmin, k_max=K, alpha=alpha)
+        torch.cuda.synchronize()
+        k_o, off_o, _ = O.draft_len(C.astype(np.float64).reshape(B, K), kmin, K, Hn.f32(alpha))
+        assert np.array_equal(k.cpu().numpy(), k_o)
+        assert np.array_equal(off.cpu().numpy(), off_o)

@@ -357,3 +357,22 @@ def pack_ragged(k: np.ndarray, k_max: int, padded_rows: np.ndarray) -> np.ndarra
         out.append(padded_rows[b, :kb])
         out.append(padded_rows[b, k_max:k_max + 1])
     return np.concatenate(out, axis=0)
+
+
+def pack_device(padded, k, off, k_max: int):
+    """Device-side packing of a padded per-sequence tensor ``[B*(k_max+1), ...]``
+    (position i of sequence b at row b*(k_max+1)+i, the final slot at i = k_max) into
+    the packed layout given device draft lengths ``k`` [B] and offsets ``off`` [B+1]:
+    packed row off[b]+i holds position i for i < k_b and the final slot at i = k_b.
+    Rows at or beyond off[B] receive arbitrary (in-bounds) copies.  Index bookkeeping
+    only, with torch gather ops (no host synchronisation)."""
+    import torch
+
+    B = k.numel()
+    R = B * (k_max + 1)
+    p = torch.arange(R, device=padded.device, dtype=torch.int64)
+    b = torch.searchsorted(off[1:].to(torch.int64).contiguous(), p, right=True).clamp_(max=B - 1)
+    i = p - off.to(torch.int64)[b]
+    kb = k.to(torch.int64)[b]
+    src = b * (k_max + 1) + torch.where((i >= 0) & (i < kb), i, torch.full_like(i, k_max))
+    return padded.index_select(0, src)
