@@ -36,6 +36,7 @@
 #ifndef CMSD_H
 #define CMSD_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -101,7 +102,8 @@ typedef struct {
 typedef struct {
   float max_logit;    /* max of the target row                                    */
   float sum_exp;      /* sum_v exp(z_v - max)                                     */
-  int32_t n_greater;  /* min(#{v : z_v > z_drafted}, top_beta); -1 on the final row */
+  int32_t n_greater;  /* CM mode: min(#{v : z_v > z_drafted}, top_beta); 0 in STANDARD
+                         mode or with top_beta = 0; -1 on the final row             */
   int32_t accept;     /* 1 accepted, 0 rejected, -1 final row, -2 invalid input   */
 } cmsd_target_stats;
 
@@ -177,6 +179,11 @@ cmsd_status cmsd_draft_len(const cmsd_row_stats* stats, int32_t batch, const cms
  *                   (offsets inconsistent with draft_len or target_rows, draft_len
  *                   out of range, drafted id outside [0, vocab)).
  *   next_token      device, batch int32 (output): the final token; -1 when invalid.
+ *   workspace       device scratch of at least cmsd_verify_workspace_bytes(batch,
+ *                   vocab) bytes, 8-byte aligned, owned by the caller; its contents
+ *                   need no initialisation and are meaningless after the call.  Calls
+ *                   that share a workspace must be ordered (same stream).
+ *   workspace_bytes its size.
  * Errors: CMSD_ERR_ARG, CMSD_ERR_DTYPE, CMSD_ERR_LAUNCH.
  */
 cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cmsd_row_stats* draft_stats,
@@ -184,7 +191,13 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
                         const int32_t* target_offsets, const int32_t* draft_len, const int32_t* drafted,
                         const float* uniforms, int32_t dtype, int32_t batch, int32_t k_max, int64_t vocab,
                         const cmsd_verify_params* params, cmsd_target_stats* target_stats,
-                        int32_t* n_accepted, int32_t* next_token, void* stream);
+                        int32_t* n_accepted, int32_t* next_token, void* workspace, size_t workspace_bytes,
+                        void* stream);
+
+/* Workspace cmsd_verify needs for `batch` sequences over `vocab` (per-sequence,
+ * per-vocabulary-slice partial sums of the final-token sample); 0 for batch <= 0
+ * or an invalid vocab. */
+size_t cmsd_verify_workspace_bytes(int32_t batch, int64_t vocab);
 
 /* Human-readable name of a status code (static string). */
 const char* cmsd_status_string(cmsd_status s);

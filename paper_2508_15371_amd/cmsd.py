@@ -55,7 +55,9 @@ def _load() -> C.CDLL:
     lib.cmsd_draft_len.argtypes = [vp, i32, C.POINTER(DraftParams), vp, vp, vp]
     lib.cmsd_draft_len.restype = C.c_int
     lib.cmsd_verify.argtypes = [vp, i64, vp, vp, i64, i64, vp, vp, vp, vp, i32, i32, i32, i64,
-                                C.POINTER(VerifyParams), vp, vp, vp, vp]
+                                C.POINTER(VerifyParams), vp, vp, vp, vp, C.c_size_t, vp]
+    lib.cmsd_verify_workspace_bytes.argtypes = [i32, i64]
+    lib.cmsd_verify_workspace_bytes.restype = C.c_size_t
     lib.cmsd_verify.restype = C.c_int
     lib.cmsd_status_string.argtypes = [C.c_int]
     lib.cmsd_status_string.restype = C.c_char_p
@@ -75,7 +77,7 @@ def lib() -> C.CDLL:
 def header_symbols() -> list[str]:
     """Entry points declared in include/cmsd.h."""
     txt = open(HEADER).read()
-    return sorted(set(re.findall(r"^\s*(?:cmsd_status|const char\*|int32_t)\s+(cmsd_\w+)\s*\(", txt, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:cmsd_status|const char\*|int32_t|size_t)\s+(cmsd_\w+)\s*\(", txt, re.M)))
 
 
 def _ptr(t: torch.Tensor | None) -> int | None:
@@ -139,12 +141,23 @@ def cmsd_draft_len(stats: torch.Tensor, batch: int, *, k_min: int, k_max: int, a
     return draft_len, target_offsets
 
 
+def cmsd_verify_workspace_bytes(batch: int, vocab: int) -> int:
+    """Bytes of device workspace cmsd_verify needs."""
+    return int(_lib.cmsd_verify_workspace_bytes(int(batch), int(vocab)))
+
+
+def verify_workspace(batch: int, vocab: int, device) -> torch.Tensor:
+    """A device workspace tensor for cmsd_verify (allocate once, reuse across calls)."""
+    n = max(8, cmsd_verify_workspace_bytes(batch, vocab))
+    return torch.empty((n + 7) // 8, dtype=torch.float64, device=device)
+
+
 def cmsd_verify(draft_logits: torch.Tensor, draft_stats: torch.Tensor, target_logits: torch.Tensor,
                 target_offsets: torch.Tensor, draft_len: torch.Tensor, drafted: torch.Tensor,
                 uniforms: torch.Tensor, *, batch: int, k_max: int, mode: int = CMSD_MODE_CM, top_beta: int = 3,
                 tau_base: float = 0.1, gamma: float = 1.0, target_stats: torch.Tensor | None = None,
                 n_accepted: torch.Tensor | None = None, next_token: torch.Tensor | None = None,
-                stream=None) -> tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+                workspace: torch.Tensor | None = None, stream=None) -> tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
     """Verification of every drafted position; returns (n_accepted [batch] int32,
     next_token [batch] int32, target_stats float32 [target_rows, 4] with int32 bits in
     columns 2 and 3)."""
@@ -159,6 +172,8 @@ def cmsd_verify(draft_logits: torch.Tensor, draft_stats: torch.Tensor, target_lo
         n_accepted = torch.empty(batch, dtype=torch.int32, device=dev)
     if next_token is None:
         next_token = torch.empty(batch, dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = verify_workspace(batch, V, dev)
     for name, t, dt in (("target_offsets", target_offsets, torch.int32), ("draft_len", draft_len, torch.int32),
                         ("drafted", drafted, torch.int32), ("uniforms", uniforms, torch.float32)):
         if t.dtype != dt or not t.is_contiguous():
@@ -168,5 +183,5 @@ def cmsd_verify(draft_logits: torch.Tensor, draft_stats: torch.Tensor, target_lo
         _ptr(draft_logits), dst, _ptr(draft_stats), _ptr(target_logits), tst, trows,
         _ptr(target_offsets), _ptr(draft_len), _ptr(drafted), _ptr(uniforms), _dtype_code(target_logits),
         int(batch), int(k_max), V, C.byref(p), _ptr(target_stats), _ptr(n_accepted), _ptr(next_token),
-        _stream(stream)))
+        _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
     return n_accepted, next_token, target_stats

@@ -648,10 +648,26 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
 }
 
 // ----------------------------------------------------------------------------- K4 final token
-constexpr int kFinalBD = 1024;
-constexpr int kFinalG = 4;  // units loaded per batch in the span passes
+// The final token of sequence b is an inverse-CDF sample over one target row (the
+// bonus row k_b when every draft passed) or over the residual max(0, p_t - p_d) of
+// the target and drafter rows at the first rejection c.  Two kernels:
+//   k_final_parts   B x S workgroups: each streams one slice of the row (pair) and
+//                   writes fp64 partials {sum e_t, sum e_d, sum q0, sum_{q0>0} e_d},
+//                   e = 2^(z log2e - m log2e), q0 = max(0, e_t - rho0 e_d) with
+//                   rho0 = A_t / A_d from the row passes.
+//   k_final_sample  one workgroup per sequence: rho = sum e_t / sum e_d from the
+//                   fresh sums, slice masses corrected to first order in rho - rho0,
+//                   a scan over slices, then an exact scan/locate inside one slice.
+// A unit is the head (unit 0), one 16-byte vector (1..nvec) or the tail (nvec+1) of
+// the target row; slices are runs of kSliceUnits units.
+constexpr int kPartBD = 256;
+constexpr int kSliceUnits = 1024;
+constexpr int kSampleBD = 256;
 
-// A unit is the head (unit 0), one 16-byte vector (1..nvec) or the tail (nvec+1).
+struct SlicePart {
+  double et, ed, q, qd;
+};
+
 template <typename T>
 __device__ __forceinline__ int unit_load(const T* row, const Geom& g, int64_t u, float* f) {
   using E = Elem<T>;
@@ -685,7 +701,126 @@ __device__ __forceinline__ void range_load(const T* row, int64_t first, int n, f
   for (int e = 0; e < E::VEC; ++e) f[e] = e < n ? E::load(p + e) : -INFINITY;
 }
 
-// Sampling weights of one element.  RESID: max(0, e_t - rho*e_d); otherwise e_t.
+// Sequence bookkeeping shared by both kernels: layout check and the first rejected
+// position, by ballots over the accept flags (wave 0 computes, LDS broadcasts).
+// Returns -1 for an invalid sequence.
+__device__ int seq_prefix(const VerifyArgs& a, int b, int64_t& off, int& kb, int* s_out) {
+  const int t = threadIdx.x, lane = t & 63;
+  off = a.off[b];
+  const int64_t off1 = a.off[b + 1];
+  kb = a.klen[b];
+  const bool ok = kb >= 0 && kb <= a.k_max && off >= 0 && off1 == off + kb + 1 && off1 <= a.target_rows;
+  if (t < 64) {
+    int nacc = -1;
+    if (ok) {
+      nacc = kb;
+      bool bad = a.tstats[off + kb].accept != -1;
+      for (int base = 0; base < kb; base += 64) {
+        const int i = base + lane;
+        const int acc = i < kb ? a.tstats[off + i].accept : 1;
+        const unsigned long long rej = __ballot(acc == 0);
+        if (__ballot(acc != 0 && acc != 1) != 0ull) bad = true;
+        if (rej != 0ull && nacc == kb) nacc = base + __builtin_ctzll(rej);
+      }
+      if (bad) nacc = -1;
+    }
+    if (lane == 0) *s_out = nacc;
+  }
+  __syncthreads();
+  const int r = *s_out;
+  __syncthreads();
+  return r;
+}
+
+// Partial sums of one unit (n elements): e_t, e_d, q0 and e_d over q0 > 0.
+template <bool RESID, int VEC>
+__device__ __forceinline__ void part_unit(const float* ft, const float* fd, int n, float mst, float msd, float rho0,
+                                          float& at, float& ad, float& aq, float& aqd) {
+  auto one = [&](int e) {
+    const float et = fexp2(fmaf(ft[e], kLog2e, -mst));
+    at += et;
+    if (RESID) {
+      const float ed = fexp2(fmaf(fd[e], kLog2e, -msd));
+      const float q = fmaxf(fmaf(-rho0, ed, et), 0.f);
+      ad += ed;
+      aq += q;
+      aqd += q > 0.f ? ed : 0.f;
+    }
+  };
+  if (n == VEC) {
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) one(e);
+  } else {
+    for (int e = 0; e < n; ++e) one(e);
+  }
+}
+
+template <typename T, bool RESID>
+__device__ __forceinline__ void parts_slice(const T* trow, const T* drow, const Geom& g, int64_t u0, float mst,
+                                            float msd, float rho0, double (&sum)[4]) {
+  using E = Elem<T>;
+  constexpr int BD = kPartBD, VEC = E::VEC, UPT = kSliceUnits / BD;
+  const int t = threadIdx.x;
+  const int64_t nu = g.nvec + 2;
+  float ft[UPT][VEC], fd[UPT][VEC];
+  int n[UPT];
+#pragma unroll
+  for (int j = 0; j < UPT; ++j) {
+    const int64_t u = u0 + (int64_t)j * BD + t;
+    n[j] = 0;
+    if (u < nu) {
+      n[j] = unit_load(trow, g, u, ft[j]);
+      if (RESID) range_load(drow, unit_first<T>(g, u), n[j], fd[j]);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < UPT; ++j) {
+    float at = 0.f, ad = 0.f, aq = 0.f, aqd = 0.f;
+    part_unit<RESID, VEC>(ft[j], fd[j], n[j], mst, msd, rho0, at, ad, aq, aqd);
+    sum[0] += (double)at;
+    sum[1] += (double)ad;
+    sum[2] += (double)aq;
+    sum[3] += (double)aqd;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, SlicePart* __restrict__ ws) {
+  constexpr int BD = kPartBD;
+  __shared__ double sd[BD / 64];
+  __shared__ int s_n;
+  const int t = threadIdx.x;
+  const int b = blockIdx.x / S, sl = blockIdx.x % S;
+  if (b >= a.B) return;
+  int64_t off;
+  int kb;
+  const int nacc = seq_prefix(a, b, off, kb, &s_n);
+  if (nacc < 0) return;
+  const bool resid = nacc < kb;
+  const int64_t tr = off + (resid ? nacc : kb);
+  const int64_t dr = (int64_t)b * a.k_max + (resid ? nacc : 0);
+  const T* trow = reinterpret_cast<const T*>(a.target) + tr * a.tstride;
+  const T* drow = reinterpret_cast<const T*>(a.draft) + dr * a.dstride;
+  const float mst = a.tstats[tr].max_logit * kLog2e;
+  const Geom g = row_geom(trow, a.V);
+  const int64_t u0 = (int64_t)sl * kSliceUnits;
+  double sum[4] = {0.0, 0.0, 0.0, 0.0};
+  if (resid) {
+    const float msd = a.dstats[dr].max_logit * kLog2e;
+    const float rho0 = (float)((double)a.tstats[tr].sum_exp / (double)a.dstats[dr].sum_exp);
+    parts_slice<T, true>(trow, drow, g, u0, mst, msd, rho0, sum);
+  } else {
+    parts_slice<T, false>(trow, trow, g, u0, mst, 0.f, 0.f, sum);
+  }
+  SlicePart p;
+  p.et = block_all_d<BD>(sum[0], OpSumD(), sd);
+  p.ed = block_all_d<BD>(sum[1], OpSumD(), sd);
+  p.q = block_all_d<BD>(sum[2], OpSumD(), sd);
+  p.qd = block_all_d<BD>(sum[3], OpSumD(), sd);
+  if (t == 0) ws[(int64_t)b * S + sl] = p;
+}
+
+// Sampling weight of one element: RESID max(0, e_t - rho e_d), else e_t (fp64).
 template <bool RESID>
 __device__ __forceinline__ double q_weight(float zt, float zd, float mst, float msd, double rho) {
   const double et = (double)fexp2(fmaf(zt, kLog2e, -mst));
@@ -707,70 +842,68 @@ __device__ __forceinline__ double unit_sum(const T* trow, const T* drow, const G
   return s;
 }
 
-// Inverse-CDF sample over one row (or row pair).  Returns the token id, or -1 when
-// the total weight is zero (only possible for RESID).
-template <typename T, bool RESID>
-__device__ int sample_span(const T* trow, const T* drow, int64_t V, float mst, float msd, double rho, float u,
-                           double* sd, int* si, double* s_sc) {
-  constexpr int BD = kFinalBD;
-  constexpr int VEC = Elem<T>::VEC;
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const Geom g = row_geom(trow, V);  // units follow the target row; the drafter row is read by range
-  const int64_t nu = g.nvec + 2;
-  const int64_t ulo = (int64_t)t * nu / BD, uhi = (int64_t)(t + 1) * nu / BD;
-
-  // per-thread sequential sum of its units, in unit order
-  double s = 0.0;
-  for (int64_t u0 = ulo; u0 < uhi; u0 += kFinalG) {
-    double us[kFinalG];
-#pragma unroll
-    for (int k = 0; k < kFinalG; ++k)
-      us[k] = (u0 + k < uhi) ? unit_sum<T, RESID>(trow, drow, g, u0 + k, mst, msd, rho) : 0.0;
-#pragma unroll
-    for (int k = 0; k < kFinalG; ++k)
-      if (u0 + k < uhi) s += us[k];
-  }
-  // exclusive scan over threads: wave scan by shuffles, then wave totals in order
-  double incl = s;
+// Block exclusive scan of one double per thread (wave scan by shuffles, wave totals
+// added in order): deterministic.
+template <int BD>
+__device__ __forceinline__ double block_excl_scan(double v, double* sd) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  double incl = v;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
     const double up = __shfl_up(incl, o);
     if (lane >= o) incl += up;
   }
-  double excl_w = __shfl_up(incl, 1);
-  if (lane == 0) excl_w = 0.0;
+  double ex = __shfl_up(incl, 1);
+  if (lane == 0) ex = 0.0;
   __syncthreads();
   if (lane == 63) sd[w] = incl;
   __syncthreads();
-  double wpre = 0.0;
-  for (int i = 0; i < w; ++i) wpre += sd[i];
-  const double excl = wpre + excl_w;
-  const double end = excl + s;
-  // R = end of the last thread holding weight; x = u R
-  const int tlast = block_all_i<BD>(s > 0.0 ? t : -1, OpMaxI(), si);
-  if (tlast < 0) return -1;
-  if (t == tlast) s_sc[0] = end;
-  __syncthreads();
-  const double R = s_sc[0];
-  const double x = (double)u * R;
-  const int tstar = block_all_i<BD>((s > 0.0 && end > x) ? t : INT32_MAX, OpMinI(), si);
-  if (t == tstar) s_sc[1] = excl;
+  double pre = 0.0;
+  for (int i = 0; i < w; ++i) pre += sd[i];
+  return pre + ex;
+}
+
+// Smallest element y in units [ulo, uhi) with q_y > 0 and base + C(y) > x, C the
+// cumulative weight from ulo in a fixed order (per-thread contiguous spans, a block
+// scan, sequential sums inside a span; the locate repeats exactly those sums).  If
+// none qualifies, the last element with q_y > 0.  Returns -1 if all weights are 0.
+template <typename T, bool RESID>
+__device__ int locate_units(const T* trow, const T* drow, const Geom& g, int64_t ulo_all, int64_t uhi_all,
+                            float mst, float msd, double rho, double base, double x, double* sd, int* si,
+                            double* s_sc) {
+  constexpr int BD = kSampleBD, VEC = Elem<T>::VEC;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int64_t nu = uhi_all - ulo_all;
+  const int64_t ulo = ulo_all + (int64_t)t * nu / BD, uhi = ulo_all + (int64_t)(t + 1) * nu / BD;
+  double s = 0.0;
+  for (int64_t u = ulo; u < uhi; ++u) s += unit_sum<T, RESID>(trow, drow, g, u, mst, msd, rho);
+  const double excl = block_excl_scan<BD>(s, sd);
+  const double end = base + (excl + s);
+  int pick = block_all_i<BD>((s > 0.0 && end > x) ? t : INT32_MAX, OpMinI(), si);
+  bool last = false;
+  if (pick == INT32_MAX) {
+    pick = block_all_i<BD>(s > 0.0 ? t : -1, OpMaxI(), si);
+    if (pick < 0) return -1;
+    last = true;
+  }
+  if (t == pick) s_sc[0] = excl;
   __syncthreads();
   int y = -1;
   if (w == 0) {
-    // locate inside thread tstar's span with the same summation order
-    const double base = s_sc[1];
-    const int64_t lo = (int64_t)tstar * nu / BD, hi = (int64_t)(tstar + 1) * nu / BD;
+    const double ex = s_sc[0];
+    const int64_t lo = ulo_all + (int64_t)pick * nu / BD, hi = ulo_all + (int64_t)(pick + 1) * nu / BD;
     double P = 0.0;
     int64_t uj = -1;
-    for (int64_t ub = lo; ub < hi && uj < 0; ub += 64) {
+    double Puj = 0.0;
+    for (int64_t ub = lo; ub < hi && (uj < 0 || last); ub += 64) {
       const double v = (ub + lane < hi) ? unit_sum<T, RESID>(trow, drow, g, ub + lane, mst, msd, rho) : 0.0;
       for (int l = 0; l < 64 && ub + l < hi; ++l) {
         const double vl = rl_d(v, l);
         const double Pn = P + vl;
-        if (vl > 0.0 && base + Pn > x) {
+        if (vl > 0.0 && (last || base + (ex + Pn) > x)) {
           uj = ub + l;
-          break;
+          Puj = P;
+          if (!last) break;
         }
         P = Pn;
       }
@@ -784,9 +917,9 @@ __device__ int sample_span(const T* trow, const T* drow, int64_t V, float mst, f
       for (int e = 0; e < n; ++e) {
         const double q = q_weight<RESID>(ft[e], RESID ? fd[e] : 0.f, mst, msd, rho);
         Q += q;
-        if (q > 0.0 && base + (P + Q) > x) {
+        if (q > 0.0 && (last || base + (ex + (Puj + Q)) > x)) {
           y = int(first + e);
-          break;
+          if (!last) break;
         }
       }
     }
@@ -799,41 +932,18 @@ __device__ int sample_span(const T* trow, const T* drow, int64_t V, float mst, f
 }
 
 template <typename T>
-__global__ __launch_bounds__(kFinalBD) void k_final(VerifyArgs a) {
-  using E = Elem<T>;
-  constexpr int BD = kFinalBD;
+__global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S, const SlicePart* __restrict__ ws) {
+  constexpr int BD = kSampleBD;
   __shared__ double sd[BD / 64];
   __shared__ int si[BD / 64];
   __shared__ double s_sc[2];
-  __shared__ int s_nacc;
-  const int t = threadIdx.x, lane = t & 63;
+  __shared__ int s_n;
+  const int t = threadIdx.x;
   const int b = blockIdx.x;
   if (b >= a.B) return;
-  const int64_t off = a.off[b], off1 = a.off[b + 1];
-  const int kb = a.klen[b];
-  const bool ok = kb >= 0 && kb <= a.k_max && off >= 0 && off1 == off + kb + 1 && off1 <= a.target_rows;
-  if (!ok) {
-    if (t == 0) {
-      a.n_acc[b] = -1;
-      a.next_tok[b] = -1;
-    }
-    return;
-  }
-  // first rejected position by ballots over the accept flags (wave 0)
-  if (t < 64) {
-    int nacc = kb;
-    bool bad = a.tstats[off + kb].accept != -1;
-    for (int base = 0; base < kb; base += 64) {
-      const int i = base + lane;
-      const int acc = i < kb ? a.tstats[off + i].accept : 1;
-      const unsigned long long rej = __ballot(acc == 0);
-      if (__ballot(acc != 0 && acc != 1) != 0ull) bad = true;
-      if (rej != 0ull && nacc == kb) nacc = base + __builtin_ctzll(rej);
-    }
-    if (lane == 0) s_nacc = bad ? -1 : nacc;
-  }
-  __syncthreads();
-  const int nacc = s_nacc;
+  int64_t off;
+  int kb;
+  const int nacc = seq_prefix(a, b, off, kb, &s_n);
   if (nacc < 0) {
     if (t == 0) {
       a.n_acc[b] = -1;
@@ -841,53 +951,83 @@ __global__ __launch_bounds__(kFinalBD) void k_final(VerifyArgs a) {
     }
     return;
   }
-  const float u = a.unif[off + kb];
-  const T* tbase = reinterpret_cast<const T*>(a.target);
-  const T* dbase = reinterpret_cast<const T*>(a.draft);
+  bool resid = nacc < kb;
+  const int64_t tr = off + (resid ? nacc : kb);
+  const int64_t dr = (int64_t)b * a.k_max + (resid ? nacc : 0);
+  const T* trow = reinterpret_cast<const T*>(a.target) + tr * a.tstride;
+  const T* drow = reinterpret_cast<const T*>(a.draft) + dr * a.dstride;
+  const float mst = a.tstats[tr].max_logit * kLog2e;
+  const float msd = resid ? a.dstats[dr].max_logit * kLog2e : 0.f;
+  const float rho0 = resid ? (float)((double)a.tstats[tr].sum_exp / (double)a.dstats[dr].sum_exp) : 0.f;
+  const SlicePart* P = ws + (int64_t)b * S;
+  // fresh normalisers and the exact ratio
+  double et = 0.0, ed = 0.0;
+  for (int s = t; s < S; s += BD) {
+    et += P[s].et;
+    ed += P[s].ed;
+  }
+  const double At = block_all_d<BD>(et, OpSumD(), sd);
+  const double Ad = block_all_d<BD>(ed, OpSumD(), sd);
+  const double rho = resid ? At / Ad : 0.0;
+  // slice masses (first-order correction of the rho0 sums), scanned in slice order;
+  // a zero residual falls back to the target row itself
+  auto mass = [&](int s, bool rs) -> double {
+    if (!rs) return P[s].et;
+    const double m = P[s].q - (rho - (double)rho0) * P[s].qd;
+    return m > 0.0 ? m : 0.0;
+  };
   int y = -1;
-  if (nacc < kb) {
-    const int64_t tr = off + nacc, dr = (int64_t)b * a.k_max + nacc;
-    const T* trow = tbase + tr * a.tstride;
-    const T* drow = dbase + dr * a.dstride;
-    const float mst = a.tstats[tr].max_logit * kLog2e;
-    const float msd = a.dstats[dr].max_logit * kLog2e;
-    // fresh, mutually consistent normalisers of both rows: rho = A_t / A_d
-    const Geom gt = row_geom(trow, a.V);
-    const int64_t nu = gt.nvec + 2;
-    const int64_t ulo = (int64_t)t * nu / BD, uhi = (int64_t)(t + 1) * nu / BD;
-    double st = 0.0, sdd = 0.0;
-    for (int64_t u0 = ulo; u0 < uhi; u0 += kFinalG) {
-      float at[kFinalG], ad[kFinalG];
-#pragma unroll
-      for (int k = 0; k < kFinalG; ++k) {
-        at[k] = 0.f;
-        ad[k] = 0.f;
-        if (u0 + k < uhi) {
-          float ft[E::VEC], fd[E::VEC];
-          const int n = unit_load(trow, gt, u0 + k, ft);
-          range_load(drow, unit_first<T>(gt, u0 + k), n, fd);
-          for (int e = 0; e < n; ++e) {
-            at[k] += fexp2(fmaf(ft[e], kLog2e, -mst));
-            ad[k] += fexp2(fmaf(fd[e], kLog2e, -msd));
-          }
-        }
-      }
-#pragma unroll
-      for (int k = 0; k < kFinalG; ++k) {
-        st += (double)at[k];
-        sdd += (double)ad[k];
-      }
+  const float u = a.unif[off + kb];
+  for (int pass = 0; pass < 2 && y < 0; ++pass) {
+    // per-thread contiguous run of slices
+    const int slo = (int)((int64_t)t * S / BD), shi = (int)((int64_t)(t + 1) * S / BD);
+    double sm = 0.0;
+    for (int s = slo; s < shi; ++s) sm += mass(s, resid);
+    const double excl = block_excl_scan<BD>(sm, sd);
+    const double end = excl + sm;
+    const int tlast = block_all_i<BD>(sm > 0.0 ? t : -1, OpMaxI(), si);
+    if (tlast < 0) {
+      resid = false;  // no residual mass: sample from the target row
+      continue;
     }
-    const double At = block_all_d<BD>(st, OpSumD(), sd);
-    const double Ad = block_all_d<BD>(sdd, OpSumD(), sd);
-    const double rho = At / Ad;
-    y = sample_span<T, true>(trow, drow, a.V, mst, msd, rho, u, sd, si, s_sc);
-    if (y == -1) y = sample_span<T, false>(trow, trow, a.V, mst, mst, 0.0, u, sd, si, s_sc);
-  } else {
-    const int64_t tr = off + kb;
-    const T* trow = tbase + tr * a.tstride;
-    const float mst = a.tstats[tr].max_logit * kLog2e;
-    y = sample_span<T, false>(trow, trow, a.V, mst, mst, 0.0, u, sd, si, s_sc);
+    if (t == tlast) s_sc[1] = end;
+    __syncthreads();
+    const double R = s_sc[1];
+    const double x = (double)u * R;
+    const int tp = block_all_i<BD>((sm > 0.0 && end > x) ? t : INT32_MAX, OpMinI(), si);
+    const int tq = tp == INT32_MAX ? tlast : tp;
+    // slice inside thread tq's run (every thread repeats the same sequential sums)
+    __syncthreads();
+    if (t == tq) s_sc[0] = excl;
+    __syncthreads();
+    const double ex = s_sc[0];
+    const int qlo = (int)((int64_t)tq * S / BD), qhi = (int)((int64_t)(tq + 1) * S / BD);
+    double Pacc = 0.0;
+    int sstar = -1;
+    double sbase = 0.0;
+    for (int s = qlo; s < qhi; ++s) {
+      const double m = mass(s, resid);
+      const double Pn = Pacc + m;
+      if (m > 0.0) {
+        sstar = s;
+        sbase = ex + Pacc;
+        if (tp != INT32_MAX && ex + Pn > x) break;
+      }
+      Pacc = Pn;
+    }
+    const Geom g = row_geom(trow, a.V);
+    const int64_t nu = g.nvec + 2;
+    const int64_t ulo = (int64_t)sstar * kSliceUnits;
+    const int64_t uhi = ulo + kSliceUnits < nu ? ulo + kSliceUnits : nu;
+    if (resid)
+      y = locate_units<T, true>(trow, drow, g, ulo, uhi, mst, msd, rho, sbase, x, sd, si, s_sc);
+    else
+      y = locate_units<T, false>(trow, trow, g, ulo, uhi, mst, mst, 0.0, sbase, x, sd, si, s_sc);
+    if (y < 0 && resid) {
+      resid = false;
+      continue;
+    }
+    break;
   }
   if (t == 0) {
     a.n_acc[b] = nacc;
@@ -904,6 +1044,13 @@ cmsd_status launched() { return hipGetLastError() == hipSuccess ? CMSD_OK : CMSD
 constexpr int kConfBD = 256;
 constexpr int kRowBD = 256;
 
+// Number of vocabulary slices of the final-token pass: units are 16-byte vectors
+// plus a head and a tail unit; the bf16 geometry (8 per vector) has the most units.
+int verify_slices(int64_t vocab) {
+  const int64_t units = vocab / 4 + 2;  // upper bound for either dtype (fp32: 4 per vector)
+  return (int)((units + kSliceUnits - 1) / kSliceUnits);
+}
+
 }  // namespace
 
 // ----------------------------------------------------------------------------- C ABI
@@ -919,7 +1066,12 @@ const char* cmsd_status_string(cmsd_status s) {
   return "unknown status";
 }
 
-int32_t cmsd_version(void) { return (1 << 16) | 0; }
+int32_t cmsd_version(void) { return (1 << 16) | 1; }
+
+size_t cmsd_verify_workspace_bytes(int32_t batch, int64_t vocab) {
+  if (batch <= 0 || vocab < 2 || vocab > INT32_MAX) return 0;
+  return (size_t)batch * (size_t)verify_slices(vocab) * sizeof(SlicePart);
+}
 
 cmsd_status cmsd_confidence(const void* logits, int32_t dtype, int64_t n_rows, int64_t vocab, int64_t row_stride,
                             const cmsd_conf_params* params, cmsd_row_stats* stats, void* stream) {
@@ -964,7 +1116,7 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
                         const int32_t* target_offsets, const int32_t* draft_len, const int32_t* drafted,
                         const float* uniforms, int32_t dtype, int32_t batch, int32_t k_max, int64_t vocab,
                         const cmsd_verify_params* params, cmsd_target_stats* target_stats, int32_t* n_accepted,
-                        int32_t* next_token, void* stream) {
+                        int32_t* next_token, void* workspace, size_t workspace_bytes, void* stream) {
   if (dtype != CMSD_F32 && dtype != CMSD_BF16) return CMSD_ERR_DTYPE;
   if (!params) return CMSD_ERR_ARG;
   if (batch < 0 || k_max < 1 || k_max > 4096 || vocab < 2 || vocab > INT32_MAX) return CMSD_ERR_ARG;
@@ -976,8 +1128,10 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   if ((int64_t)batch * k_max > INT32_MAX) return CMSD_ERR_ARG;
   const size_t es = dtype == CMSD_F32 ? 4 : 2;
   if (!draft_logits || !draft_stats || !target_logits || !target_offsets || !draft_len || !drafted || !uniforms ||
-      !target_stats || !n_accepted || !next_token)
+      !target_stats || !n_accepted || !next_token || !workspace)
     return CMSD_ERR_ARG;
+  if (workspace_bytes < cmsd_verify_workspace_bytes(batch, vocab) || !aligned(workspace, 8)) return CMSD_ERR_ARG;
+  if ((int64_t)batch * verify_slices(vocab) > INT32_MAX) return CMSD_ERR_ARG;
   if (!aligned(draft_logits, es) || !aligned(target_logits, es) || !aligned(draft_stats, 4) ||
       !aligned(target_offsets, 4) || !aligned(draft_len, 4) || !aligned(drafted, 4) || !aligned(uniforms, 4) ||
       !aligned(target_stats, 4) || !aligned(n_accepted, 4) || !aligned(next_token, 4))
@@ -1004,14 +1158,17 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   a.n_acc = n_accepted;
   a.next_tok = next_token;
   const hipStream_t st = as_stream(stream);
+  const int S = verify_slices(vocab);
+  SlicePart* ws = static_cast<SlicePart*>(workspace);
+  const unsigned gp = (unsigned)((int64_t)batch * S);
   if (dtype == CMSD_F32) {
     hipLaunchKernelGGL((k_target_rows<float, kRowBD>), dim3((unsigned)target_rows), dim3(kRowBD), 0, st, a);
-    if (launched() != CMSD_OK) return CMSD_ERR_LAUNCH;
-    hipLaunchKernelGGL((k_final<float>), dim3((unsigned)batch), dim3(kFinalBD), 0, st, a);
+    hipLaunchKernelGGL((k_final_parts<float>), dim3(gp), dim3(kPartBD), 0, st, a, S, ws);
+    hipLaunchKernelGGL((k_final_sample<float>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   } else {
     hipLaunchKernelGGL((k_target_rows<Bf16, kRowBD>), dim3((unsigned)target_rows), dim3(kRowBD), 0, st, a);
-    if (launched() != CMSD_OK) return CMSD_ERR_LAUNCH;
-    hipLaunchKernelGGL((k_final<Bf16>), dim3((unsigned)batch), dim3(kFinalBD), 0, st, a);
+    hipLaunchKernelGGL((k_final_parts<Bf16>), dim3(gp), dim3(kPartBD), 0, st, a, S, ws);
+    hipLaunchKernelGGL((k_final_sample<Bf16>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   }
   return launched();
 }

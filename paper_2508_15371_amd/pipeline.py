@@ -50,6 +50,7 @@ class LogitPass:
         self.tstats = torch.empty((self.target_rows, 4), dtype=torch.float32, device=dev)
         self.n_acc = torch.empty(B, dtype=torch.int32, device=dev)
         self.next_tok = torch.empty(B, dtype=torch.int32, device=dev)
+        self.ws = cmsd.verify_workspace(B, V, dev)
 
     def confidence(self, draft: torch.Tensor, stream=None) -> None:
         cmsd.cmsd_confidence(draft, self.stats, lambdas=self.p.lambdas, beta_margin=self.p.beta_margin,
@@ -65,7 +66,7 @@ class LogitPass:
         cmsd.cmsd_verify(draft, self.stats, target, off, k, drafted, uniforms, batch=self.B, k_max=self.k_max,
                          mode=self.p.mode, top_beta=self.p.top_beta, tau_base=self.p.tau_base,
                          gamma=self.p.gamma, target_stats=self.tstats, n_accepted=self.n_acc,
-                         next_token=self.next_tok, stream=stream)
+                         next_token=self.next_tok, workspace=self.ws, stream=stream)
 
     def run(self, draft, target, drafted, uniforms, stream=None) -> None:
         """confidence + draft_len + verify, enqueued on ``stream``."""

@@ -12,7 +12,8 @@ P = 0x10000          # fake, aligned device addresses: never dereferenced on the
 
 def test_exports_every_declared_symbol():
     syms = cm.header_symbols()
-    assert set(syms) >= {"cmsd_confidence", "cmsd_draft_len", "cmsd_verify", "cmsd_status_string", "cmsd_version"}
+    assert set(syms) >= {"cmsd_confidence", "cmsd_draft_len", "cmsd_verify", "cmsd_verify_workspace_bytes",
+                         "cmsd_status_string", "cmsd_version"}
     lib = cm.lib()
     for s in syms:
         assert hasattr(lib, s), s
@@ -63,12 +64,12 @@ def test_draft_len_argument_errors(k_min, k_max, alpha, batch, want):
 
 def _verify(**kw):
     a = dict(dl=P, ds=1024, dst=P, tl=P, ts=1024, trows=90, off=P, k=P, dr=P, u=P, dtype=cm.CMSD_BF16,
-             B=10, K=8, V=1024, p=cm.VerifyParams(1, 3, 0.1, 1.0), tst=P, na=P, nt=P)
+             B=10, K=8, V=1024, p=cm.VerifyParams(1, 3, 0.1, 1.0), tst=P, na=P, nt=P, ws=P, wsb=1 << 20)
     a.update(kw)
     return cm.lib().cmsd_verify(a["dl"], a["ds"], a["dst"], a["tl"], a["ts"], a["trows"], a["off"], a["k"],
                                 a["dr"], a["u"], a["dtype"], a["B"], a["K"], a["V"],
                                 C.byref(a["p"]) if a["p"] is not None else None, a["tst"], a["na"], a["nt"],
-                                None)
+                                a["ws"], a["wsb"], None)
 
 
 @pytest.mark.parametrize("kw,want", [
@@ -89,7 +90,19 @@ def _verify(**kw):
     (dict(na=None), cm.CMSD_ERR_ARG),
     (dict(tl=P + 1), cm.CMSD_ERR_ARG),
     (dict(dr=P + 2), cm.CMSD_ERR_ARG),
-    (dict(B=0, dl=None, tl=None), cm.CMSD_OK),
+    (dict(ws=None), cm.CMSD_ERR_ARG),
+    (dict(wsb=16), cm.CMSD_ERR_ARG),                              # workspace too small
+    (dict(ws=P + 4), cm.CMSD_ERR_ARG),                            # misaligned workspace
+    (dict(B=0, dl=None, tl=None, ws=None, wsb=0), cm.CMSD_OK),
 ])
+
 def test_verify_argument_errors(kw, want):
     assert _verify(**kw) == want
+
+
+def test_workspace_size():
+    f = cm.lib().cmsd_verify_workspace_bytes
+    assert f(0, 1000) == 0 and f(4, 1) == 0
+    # per sequence: one 32-byte record per slice of 1024 16-byte units (+ head and tail)
+    assert f(256, 128256) == 256 * 32 * (((128256 // 4 + 2) + 1023) // 1024)
+    assert f(1, 2) == 32
