@@ -39,7 +39,18 @@ template <typename T> struct Elem;
 template <> struct Elem<float> {
   static constexpr int VEC = 4;   // elements per 16-byte vector
   static constexpr int U = 8;     // vectors per thread per chunk (32 elements)
+  static constexpr uint32_t NINF = 0xff800000u;  // -inf, as one element's bits
   __device__ static float load(const float* p) { return *p; }
+  // n < VEC elements at p as one raw 16-byte vector, padded with -inf
+  __device__ static uint4 raw_partial(const float* p, int n) {
+    uint4 r;
+    r.x = n > 0 ? __float_as_uint(p[0]) : NINF;
+    r.y = n > 1 ? __float_as_uint(p[1]) : NINF;
+    r.z = n > 2 ? __float_as_uint(p[2]) : NINF;
+    r.w = n > 3 ? __float_as_uint(p[3]) : NINF;
+    return r;
+  }
+  __device__ static uint4 raw_ninf() { return make_uint4(NINF, NINF, NINF, NINF); }
   __device__ static void unpack(const uint4& v, float* f) {
     f[0] = __uint_as_float(v.x); f[1] = __uint_as_float(v.y);
     f[2] = __uint_as_float(v.z); f[3] = __uint_as_float(v.w);
@@ -48,7 +59,18 @@ template <> struct Elem<float> {
 template <> struct Elem<Bf16> {
   static constexpr int VEC = 8;
   static constexpr int U = 4;     // 32 elements per chunk
+  static constexpr uint32_t NINF = 0xff80u;
   __device__ static float load(const Bf16* p) { return __uint_as_float(uint32_t(p->bits) << 16); }
+  __device__ static uint4 raw_partial(const Bf16* p, int n) {
+    uint32_t h[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h[e] = e < n ? uint32_t(p[e].bits) : NINF;
+    return make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16));
+  }
+  __device__ static uint4 raw_ninf() {
+    const uint32_t w = NINF | (NINF << 16);
+    return make_uint4(w, w, w, w);
+  }
   __device__ static void unpack(const uint4& v, float* f) {
     f[0] = __uint_as_float(v.x << 16); f[1] = __uint_as_float(v.x & 0xffff0000u);
     f[2] = __uint_as_float(v.y << 16); f[3] = __uint_as_float(v.y & 0xffff0000u);
@@ -80,6 +102,14 @@ __device__ __forceinline__ Geom row_geom(const T* row, int64_t V) {
 }
 
 __device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Streaming 16-byte load with the nontemporal hint: logit rows are read once per
+// pass, and the hint keeps them from displacing reused lines in the caches.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld_stream(const uint4* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 // ----------------------------------------------------------------------------- wave / block reductions
 // Wave64 all-reduce: DPP quad permutes and row mirrors inside each 16-lane row,
@@ -177,6 +207,28 @@ __device__ __forceinline__ int block_all_i(int v, Op op, int* slot) {
 #pragma unroll
   for (int i = 1; i < NW; ++i) r = op(r, slot[i]);
   return r;
+}
+
+// Block sums of N doubles in one LDS round: every thread receives all N totals
+// (waves combined in order).  `lds` must hold N * BD/64 doubles.
+template <int BD, int N>
+__device__ __forceinline__ void block_sum_n(double (&v)[N], double* lds) {
+  constexpr int NW = BD / 64;
+  double w[N];
+#pragma unroll
+  for (int j = 0; j < N; ++j) w[j] = wave_all_d(v[j], OpSumD());
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+    for (int j = 0; j < N; ++j) lds[j * NW + (threadIdx.x >> 6)] = w[j];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    double r = lds[j * NW];
+    for (int i = 1; i < NW; ++i) r += lds[j * NW + i];
+    v[j] = r;
+  }
 }
 
 // ----------------------------------------------------------------------------- streaming row state
@@ -280,6 +332,7 @@ __device__ void rescan_chunk(const T* row, const Geom& g, int64_t nr, int cid, f
 // ----------------------------------------------------------------------------- K1 confidence
 struct ConfArgs {
   float l_ent, l_margin, l_soft, beta_m;
+  double lnV;  // ln(vocab)
 };
 
 template <typename T, int BD>
@@ -289,8 +342,9 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
   constexpr int VEC = E::VEC, U = E::U, N = VEC * U;
   __shared__ double sd[BD / 64];
   __shared__ float sf[BD / 64];
-  __shared__ int si[BD / 64];
-  __shared__ float s_other;
+  __shared__ double ep_d[2][BD / 64];
+  __shared__ float ep_f[2][BD / 64];
+  __shared__ int ep_i[2][BD / 64];
   const int t = threadIdx.x;
 
   for (int64_t r = blockIdx.x; r < n_rows; r += gridDim.x) {
@@ -307,7 +361,7 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
     uint4 nxt[U];
     if (nr > 0) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) nxt[u] = vp[u * BD + t];
+      for (int u = 0; u < U; ++u) nxt[u] = ld_stream(vp + u * BD + t);
     }
     for (int64_t k = 0; k < nr; ++k) {
       uint4 cur[U];
@@ -316,7 +370,7 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
       if (k + 1 < nr) {
         const uint4* q = vp + (k + 1) * per_round;
 #pragma unroll
-        for (int u = 0; u < U; ++u) nxt[u] = q[u * BD + t];
+        for (int u = 0; u < U; ++u) nxt[u] = ld_stream(q + u * BD + t);
       }
       float f[N];
 #pragma unroll
@@ -332,7 +386,7 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
       for (int u = 0; u < U; ++u) {
         const int64_t j = rb + (int64_t)u * BD + t;
         if (j < g.nvec) {
-          E::unpack(vp[j], f + u * VEC);
+          E::unpack(ld_stream(vp + j), f + u * VEC);
           valid |= ((1u << VEC) - 1u) << (u * VEC);
         } else {
 #pragma unroll
@@ -358,12 +412,48 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
     const float contrib = is_max ? s.t2 : s.t1;
     const int idx32 = idx == INT64_MAX ? INT32_MAX : int(idx);
 
-    const double A = block_all_d<BD>(Ad, OpSumD(), sd);
-    double Tsum = block_all_d<BD>(Td, OpSumD(), sd);
-    const float cmx = block_all_f<BD>(contrib, OpMax(), sf);
-    const int nmax = block_all_i<BD>(is_max ? 1 : 0, OpSumI(), si);
-    const int top1 = block_all_i<BD>(idx32, OpMinI(), si);
-    if (idx32 == top1 && is_max) s_other = other;
+    // one LDS round for: sum A, sum T, max of the other chunk maxima, number of
+    // threads holding the max, and the lowest max index with its chunk's other value
+    double A, Tsum;
+    float cmx, s_oth;
+    int nmax, top1;
+    {
+      const double wA = wave_all_d(Ad, OpSumD());
+      const double wT = wave_all_d(Td, OpSumD());
+      const float wc = wave_all_f(contrib, OpMax());
+      const int wn = wave_all_i(is_max ? 1 : 0, OpSumI());
+      const int wi = wave_all_i(idx32, OpMinI());
+      const unsigned long long own = __ballot(idx32 == wi && is_max);
+      const float wo = own ? rl_f(other, __builtin_ctzll(own)) : -INFINITY;
+      __syncthreads();
+      if ((t & 63) == 0) {
+        const int w = t >> 6;
+        ep_d[0][w] = wA;
+        ep_d[1][w] = wT;
+        ep_f[0][w] = wc;
+        ep_f[1][w] = wo;
+        ep_i[0][w] = wn;
+        ep_i[1][w] = wi;
+      }
+      __syncthreads();
+      A = ep_d[0][0];
+      Tsum = ep_d[1][0];
+      cmx = ep_f[0][0];
+      s_oth = ep_f[1][0];
+      nmax = ep_i[0][0];
+      top1 = ep_i[1][0];
+#pragma unroll
+      for (int w = 1; w < BD / 64; ++w) {
+        A += ep_d[0][w];
+        Tsum += ep_d[1][w];
+        cmx = fmaxf(cmx, ep_f[0][w]);
+        nmax += ep_i[0][w];
+        if (ep_i[1][w] < top1) {
+          top1 = ep_i[1][w];
+          s_oth = ep_f[1][w];
+        }
+      }
+    }
     uint32_t flags = 0;
     if (Tsum != Tsum) {
       // the row holds -inf logits: recompute T skipping them
@@ -387,17 +477,17 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
     }
     __syncthreads();
     if (t == 0) {
-      const float z2 = nmax >= 2 ? m : fmaxf(cmx, s_other);
+      const float z2 = nmax >= 2 ? m : fmaxf(cmx, s_oth);
       const double Vd = (double)V;
       const double Tn = Tsum * kLn2;
-      double H = log(A) - Tn / A;
+      double H = (double)log1pf((float)(A - 1.0)) - Tn / A;  // ln A = log1p(A - 1), A - 1 exact in fp64
       H = H < 0.0 ? 0.0 : H;
       const double dm = (double)m, dz2 = (double)z2;
       const double margin = z2 == -INFINITY ? INFINITY : dm - dz2;
-      const double msoft = z2 == -INFINITY ? 1.0 / A : -expm1(dz2 - dm) / A;
-      const double c_ent = 1.0 - H / log(Vd);
+      const double msoft = z2 == -INFINITY ? 1.0 / A : (double)(-expm1f((float)(dz2 - dm))) / A;
+      const double c_ent = 1.0 - H / a.lnV;
       const double tm = (double)a.beta_m * margin;
-      const double c_m = tm == INFINITY ? 1.0 : 1.0 / (1.0 + exp(-tm));
+      const double c_m = tm == INFINITY ? 1.0 : 1.0 / (1.0 + (double)expf((float)-tm));
       const double c_s = fmin(1.0, msoft / (1.0 - 1.0 / Vd));
       const double C = (double)a.l_ent * c_ent + (double)a.l_margin * c_m + (double)a.l_soft * c_s;
       cmsd_row_stats o;
@@ -521,7 +611,7 @@ __device__ __forceinline__ void target_stream(const T* row, const Geom& g, float
   uint4 nxt[U];
   if (nr > 0) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) nxt[u] = vp[u * BD + t];
+    for (int u = 0; u < U; ++u) nxt[u] = ld_stream(vp + u * BD + t);
   }
   for (int64_t k = 0; k < nr; ++k) {
     uint4 cur[U];
@@ -530,7 +620,7 @@ __device__ __forceinline__ void target_stream(const T* row, const Geom& g, float
     if (k + 1 < nr) {
       const uint4* q = vp + (k + 1) * per_round;
 #pragma unroll
-      for (int u = 0; u < U; ++u) nxt[u] = q[u * BD + t];
+      for (int u = 0; u < U; ++u) nxt[u] = ld_stream(q + u * BD + t);
     }
     float f[N];
 #pragma unroll
@@ -545,7 +635,7 @@ __device__ __forceinline__ void target_stream(const T* row, const Geom& g, float
     for (int u = 0; u < U; ++u) {
       const int64_t j = rb + (int64_t)u * BD + t;
       if (j < g.nvec) {
-        E::unpack(vp[j], f + u * VEC);
+        E::unpack(ld_stream(vp + j), f + u * VEC);
         valid |= ((1u << VEC) - 1u) << (u * VEC);
       } else {
 #pragma unroll
@@ -617,8 +707,24 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
   const float m = block_all_f<BD>(s.t1, OpMax(), sf);
   const float ms_row = m * kLog2e;
   const float sc = fexp2(s.n.ms - ms_row);
-  const double A = block_all_d<BD>((double)(s.n.A * sc), OpSumD(), sd);
-  const int ngt = block_all_i<BD>((t & 63) == 0 ? wcnt : 0, OpSumI(), si);
+  double A;
+  int ngt;
+  {
+    const double wA = wave_all_d((double)(s.n.A * sc), OpSumD());
+    __syncthreads();
+    if ((t & 63) == 0) {
+      sd[t >> 6] = wA;
+      si[t >> 6] = wcnt;
+    }
+    __syncthreads();
+    A = sd[0];
+    ngt = si[0];
+#pragma unroll
+    for (int w = 1; w < BD / 64; ++w) {
+      A += sd[w];
+      ngt += si[w];
+    }
+  }
   if (t == 0) {
     cmsd_target_stats res;
     res.max_logit = m;
@@ -651,17 +757,19 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
 // The final token of sequence b is an inverse-CDF sample over one target row (the
 // bonus row k_b when every draft passed) or over the residual max(0, p_t - p_d) of
 // the target and drafter rows at the first rejection c.  Two kernels:
-//   k_final_parts   B x S workgroups: each streams one slice of the row (pair) and
-//                   writes fp64 partials {sum e_t, sum e_d, sum q0, sum_{q0>0} e_d},
-//                   e = 2^(z log2e - m log2e), q0 = max(0, e_t - rho0 e_d) with
-//                   rho0 = A_t / A_d from the row passes.
+//   k_final_parts   B x ceil(S/4) workgroups, each covering 4 slices of the row
+//                   (pair): fp64 partials {sum e_t, sum e_d, sum q0, sum_{q0>0} e_d}
+//                   per slice, e = 2^(z log2e - m log2e), q0 = max(0, e_t - rho0 e_d)
+//                   with rho0 = A_t / A_d from the row passes.
 //   k_final_sample  one workgroup per sequence: rho = sum e_t / sum e_d from the
 //                   fresh sums, slice masses corrected to first order in rho - rho0,
 //                   a scan over slices, then an exact scan/locate inside one slice.
 // A unit is the head (unit 0), one 16-byte vector (1..nvec) or the tail (nvec+1) of
-// the target row; slices are runs of kSliceUnits units.
+// the target row, always handled as one raw 16-byte vector padded with -inf (whose
+// weights are exactly 0); slices are runs of kSliceUnits units.
 constexpr int kPartBD = 256;
 constexpr int kSliceUnits = 1024;
+constexpr int kSubPerWG = 4;
 constexpr int kSampleBD = 256;
 
 struct SlicePart {
@@ -669,36 +777,35 @@ struct SlicePart {
 };
 
 template <typename T>
-__device__ __forceinline__ int unit_load(const T* row, const Geom& g, int64_t u, float* f) {
-  using E = Elem<T>;
-  constexpr int VEC = E::VEC;
-  if (u >= 1 && u <= g.nvec) {
-    E::unpack(reinterpret_cast<const uint4*>(row + g.head)[u - 1], f);
-    return VEC;
-  }
-  if (u == 0) {
-    for (int e = 0; e < VEC; ++e) f[e] = e < g.head ? E::load(row + e) : -INFINITY;
-    return g.head;
-  }
-  const int64_t base = g.head + g.nvec * VEC;
-  for (int e = 0; e < VEC; ++e) f[e] = e < g.tail ? E::load(row + base + e) : -INFINITY;
-  return g.tail;
-}
-template <typename T>
 __device__ __forceinline__ int64_t unit_first(const Geom& g, int64_t u) {
   return u == 0 ? 0 : (u <= g.nvec ? g.head + (u - 1) * Elem<T>::VEC : g.head + g.nvec * Elem<T>::VEC);
 }
-// Elements [first, first+n) of a second row whose 16-byte phase may differ from the
-// row that defines the units: one vector load when aligned, element loads otherwise.
 template <typename T>
-__device__ __forceinline__ void range_load(const T* row, int64_t first, int n, float* f) {
+__device__ __forceinline__ int unit_count(const Geom& g, int64_t u) {
+  return u == 0 ? g.head : (u <= g.nvec ? Elem<T>::VEC : (u == g.nvec + 1 ? g.tail : 0));
+}
+// Unit u of the row that defines the units.
+template <typename T, bool NT>
+__device__ __forceinline__ uint4 unit_raw(const T* row, const Geom& g, int64_t u) {
   using E = Elem<T>;
-  const T* p = row + first;
-  if (n == E::VEC && (reinterpret_cast<uintptr_t>(p) & 15u) == 0) {
-    E::unpack(*reinterpret_cast<const uint4*>(p), f);
-    return;
+  if (u >= 1 && u <= g.nvec) {
+    const uint4* p = reinterpret_cast<const uint4*>(row + g.head) + (u - 1);
+    return NT ? ld_stream(p) : *p;
   }
-  for (int e = 0; e < E::VEC; ++e) f[e] = e < n ? E::load(p + e) : -INFINITY;
+  const int n = unit_count<T>(g, u);
+  return n > 0 ? E::raw_partial(row + unit_first<T>(g, u), n) : E::raw_ninf();
+}
+// The same elements of a second row whose 16-byte phase may differ (`same_phase`
+// tells whether it matches): one vector load when aligned, element loads otherwise.
+template <typename T, bool NT>
+__device__ __forceinline__ uint4 unit_raw2(const T* row, const Geom& g, int64_t u, bool same_phase) {
+  using E = Elem<T>;
+  if (same_phase && u >= 1 && u <= g.nvec) {
+    const uint4* p = reinterpret_cast<const uint4*>(row + g.head) + (u - 1);
+    return NT ? ld_stream(p) : *p;
+  }
+  const int n = unit_count<T>(g, u);
+  return n > 0 ? E::raw_partial(row + unit_first<T>(g, u), n) : E::raw_ninf();
 }
 
 // Sequence bookkeeping shared by both kernels: layout check and the first rejected
@@ -732,11 +839,17 @@ __device__ int seq_prefix(const VerifyArgs& a, int b, int64_t& off, int& kb, int
   return r;
 }
 
-// Partial sums of one unit (n elements): e_t, e_d, q0 and e_d over q0 > 0.
-template <bool RESID, int VEC>
-__device__ __forceinline__ void part_unit(const float* ft, const float* fd, int n, float mst, float msd, float rho0,
+// Partial sums of one raw unit: e_t, e_d, q0 and e_d where q0 > 0.
+template <typename T, bool RESID>
+__device__ __forceinline__ void part_unit(const uint4& rt, const uint4& rd, float mst, float msd, float rho0,
                                           float& at, float& ad, float& aq, float& aqd) {
-  auto one = [&](int e) {
+  using E = Elem<T>;
+  constexpr int VEC = E::VEC;
+  float ft[VEC], fd[VEC];
+  E::unpack(rt, ft);
+  if (RESID) E::unpack(rd, fd);
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) {
     const float et = fexp2(fmaf(ft[e], kLog2e, -mst));
     at += et;
     if (RESID) {
@@ -746,37 +859,25 @@ __device__ __forceinline__ void part_unit(const float* ft, const float* fd, int 
       aq += q;
       aqd += q > 0.f ? ed : 0.f;
     }
-  };
-  if (n == VEC) {
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) one(e);
-  } else {
-    for (int e = 0; e < n; ++e) one(e);
   }
 }
 
 template <typename T, bool RESID>
-__device__ __forceinline__ void parts_slice(const T* trow, const T* drow, const Geom& g, int64_t u0, float mst,
-                                            float msd, float rho0, double (&sum)[4]) {
-  using E = Elem<T>;
-  constexpr int BD = kPartBD, VEC = E::VEC, UPT = kSliceUnits / BD;
+__device__ __forceinline__ void parts_slice(const T* trow, const T* drow, const Geom& g, bool same_phase,
+                                            int64_t u0, float mst, float msd, float rho0, double (&sum)[4]) {
+  constexpr int BD = kPartBD, UPT = kSliceUnits / BD;
   const int t = threadIdx.x;
-  const int64_t nu = g.nvec + 2;
-  float ft[UPT][VEC], fd[UPT][VEC];
-  int n[UPT];
+  uint4 rt[UPT], rd[UPT];
 #pragma unroll
   for (int j = 0; j < UPT; ++j) {
     const int64_t u = u0 + (int64_t)j * BD + t;
-    n[j] = 0;
-    if (u < nu) {
-      n[j] = unit_load(trow, g, u, ft[j]);
-      if (RESID) range_load(drow, unit_first<T>(g, u), n[j], fd[j]);
-    }
+    rt[j] = unit_raw<T, true>(trow, g, u);
+    if (RESID) rd[j] = unit_raw2<T, true>(drow, g, u, same_phase);
   }
 #pragma unroll
   for (int j = 0; j < UPT; ++j) {
     float at = 0.f, ad = 0.f, aq = 0.f, aqd = 0.f;
-    part_unit<RESID, VEC>(ft[j], fd[j], n[j], mst, msd, rho0, at, ad, aq, aqd);
+    part_unit<T, RESID>(rt[j], rd[j], mst, msd, rho0, at, ad, aq, aqd);
     sum[0] += (double)at;
     sum[1] += (double)ad;
     sum[2] += (double)aq;
@@ -785,12 +886,12 @@ __device__ __forceinline__ void parts_slice(const T* trow, const T* drow, const 
 }
 
 template <typename T>
-__global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, SlicePart* __restrict__ ws) {
+__global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, int SW, SlicePart* __restrict__ ws) {
   constexpr int BD = kPartBD;
-  __shared__ double sd[BD / 64];
+  __shared__ double sd[4 * (BD / 64)];
   __shared__ int s_n;
   const int t = threadIdx.x;
-  const int b = blockIdx.x / S, sl = blockIdx.x % S;
+  const int b = blockIdx.x / SW, sl0 = (blockIdx.x % SW) * kSubPerWG;
   if (b >= a.B) return;
   int64_t off;
   int kb;
@@ -801,44 +902,59 @@ __global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, Sl
   const int64_t dr = (int64_t)b * a.k_max + (resid ? nacc : 0);
   const T* trow = reinterpret_cast<const T*>(a.target) + tr * a.tstride;
   const T* drow = reinterpret_cast<const T*>(a.draft) + dr * a.dstride;
+  const bool same_phase = ((reinterpret_cast<uintptr_t>(trow) ^ reinterpret_cast<uintptr_t>(drow)) & 15u) == 0;
   const float mst = a.tstats[tr].max_logit * kLog2e;
+  const float msd = resid ? a.dstats[dr].max_logit * kLog2e : 0.f;
+  const float rho0 = resid ? (float)((double)a.tstats[tr].sum_exp / (double)a.dstats[dr].sum_exp) : 0.f;
   const Geom g = row_geom(trow, a.V);
-  const int64_t u0 = (int64_t)sl * kSliceUnits;
-  double sum[4] = {0.0, 0.0, 0.0, 0.0};
-  if (resid) {
-    const float msd = a.dstats[dr].max_logit * kLog2e;
-    const float rho0 = (float)((double)a.tstats[tr].sum_exp / (double)a.dstats[dr].sum_exp);
-    parts_slice<T, true>(trow, drow, g, u0, mst, msd, rho0, sum);
-  } else {
-    parts_slice<T, false>(trow, trow, g, u0, mst, 0.f, 0.f, sum);
+  for (int k = 0; k < kSubPerWG; ++k) {
+    const int sl = sl0 + k;
+    if (sl >= S) break;
+    double sum[4] = {0.0, 0.0, 0.0, 0.0};
+    const int64_t u0 = (int64_t)sl * kSliceUnits;
+    if (resid)
+      parts_slice<T, true>(trow, drow, g, same_phase, u0, mst, msd, rho0, sum);
+    else
+      parts_slice<T, false>(trow, trow, g, true, u0, mst, 0.f, 0.f, sum);
+    block_sum_n<BD, 4>(sum, sd);
+    if (t == 0) ws[(int64_t)b * S + sl] = SlicePart{sum[0], sum[1], sum[2], sum[3]};
   }
-  SlicePart p;
-  p.et = block_all_d<BD>(sum[0], OpSumD(), sd);
-  p.ed = block_all_d<BD>(sum[1], OpSumD(), sd);
-  p.q = block_all_d<BD>(sum[2], OpSumD(), sd);
-  p.qd = block_all_d<BD>(sum[3], OpSumD(), sd);
-  if (t == 0) ws[(int64_t)b * S + sl] = p;
 }
 
-// Sampling weight of one element: RESID max(0, e_t - rho e_d), else e_t (fp64).
-template <bool RESID>
-__device__ __forceinline__ double q_weight(float zt, float zd, float mst, float msd, double rho) {
-  const double et = (double)fexp2(fmaf(zt, kLog2e, -mst));
-  if (!RESID) return et;
-  const double ed = (double)fexp2(fmaf(zd, kLog2e, -msd));
-  const double q = fma(-rho, ed, et);
-  return q > 0.0 ? q : 0.0;
+// Sampling weights of one raw unit: RESID max(0, e_t - rho e_d), else e_t (fp64);
+// padding elements weigh exactly 0.
+template <typename T, bool RESID>
+__device__ __forceinline__ void unit_weights(const uint4& rt, const uint4& rd, float mst, float msd, double rho,
+                                             double* q) {
+  using E = Elem<T>;
+  constexpr int VEC = E::VEC;
+  float ft[VEC], fd[VEC];
+  E::unpack(rt, ft);
+  if (RESID) E::unpack(rd, fd);
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) {
+    const double et = (double)fexp2(fmaf(ft[e], kLog2e, -mst));
+    if (RESID) {
+      const double ed = (double)fexp2(fmaf(fd[e], kLog2e, -msd));
+      const double d = fma(-rho, ed, et);
+      q[e] = d > 0.0 ? d : 0.0;
+    } else {
+      q[e] = et;
+    }
+  }
 }
 
 template <typename T, bool RESID>
-__device__ __forceinline__ double unit_sum(const T* trow, const T* drow, const Geom& g, int64_t u, float mst,
-                                           float msd, double rho) {
+__device__ __forceinline__ double unit_sum(const T* trow, const T* drow, const Geom& g, bool same_phase, int64_t u,
+                                           float mst, float msd, double rho) {
   constexpr int VEC = Elem<T>::VEC;
-  float ft[VEC], fd[VEC];
-  const int n = unit_load(trow, g, u, ft);
-  if (RESID) range_load(drow, unit_first<T>(g, u), n, fd);
+  const uint4 rt = unit_raw<T, false>(trow, g, u);
+  const uint4 rd = RESID ? unit_raw2<T, false>(drow, g, u, same_phase) : rt;
+  double q[VEC];
+  unit_weights<T, RESID>(rt, rd, mst, msd, rho, q);
   double s = 0.0;
-  for (int e = 0; e < n; ++e) s += q_weight<RESID>(ft[e], RESID ? fd[e] : 0.f, mst, msd, rho);
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) s += q[e];
   return s;
 }
 
@@ -863,20 +979,21 @@ __device__ __forceinline__ double block_excl_scan(double v, double* sd) {
   return pre + ex;
 }
 
-// Smallest element y in units [ulo, uhi) with q_y > 0 and base + C(y) > x, C the
-// cumulative weight from ulo in a fixed order (per-thread contiguous spans, a block
-// scan, sequential sums inside a span; the locate repeats exactly those sums).  If
-// none qualifies, the last element with q_y > 0.  Returns -1 if all weights are 0.
+// Smallest element y in units [ulo_all, uhi_all) with q_y > 0 and base + C(y) > x,
+// C the cumulative weight from ulo_all in a fixed order (per-thread contiguous
+// spans, a block scan, sequential sums inside a span; the locate repeats exactly
+// those sums).  If none qualifies, the last element with q_y > 0.  Returns -1 if
+// every weight is 0.
 template <typename T, bool RESID>
-__device__ int locate_units(const T* trow, const T* drow, const Geom& g, int64_t ulo_all, int64_t uhi_all,
-                            float mst, float msd, double rho, double base, double x, double* sd, int* si,
-                            double* s_sc) {
+__device__ int locate_units(const T* trow, const T* drow, const Geom& g, bool same_phase, int64_t ulo_all,
+                            int64_t uhi_all, float mst, float msd, double rho, double base, double x, double* sd,
+                            int* si, double* s_sc) {
   constexpr int BD = kSampleBD, VEC = Elem<T>::VEC;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int64_t nu = uhi_all - ulo_all;
   const int64_t ulo = ulo_all + (int64_t)t * nu / BD, uhi = ulo_all + (int64_t)(t + 1) * nu / BD;
   double s = 0.0;
-  for (int64_t u = ulo; u < uhi; ++u) s += unit_sum<T, RESID>(trow, drow, g, u, mst, msd, rho);
+  for (int64_t u = ulo; u < uhi; ++u) s += unit_sum<T, RESID>(trow, drow, g, same_phase, u, mst, msd, rho);
   const double excl = block_excl_scan<BD>(s, sd);
   const double end = base + (excl + s);
   int pick = block_all_i<BD>((s > 0.0 && end > x) ? t : INT32_MAX, OpMinI(), si);
@@ -896,7 +1013,8 @@ __device__ int locate_units(const T* trow, const T* drow, const Geom& g, int64_t
     int64_t uj = -1;
     double Puj = 0.0;
     for (int64_t ub = lo; ub < hi && (uj < 0 || last); ub += 64) {
-      const double v = (ub + lane < hi) ? unit_sum<T, RESID>(trow, drow, g, ub + lane, mst, msd, rho) : 0.0;
+      const double v =
+          (ub + lane < hi) ? unit_sum<T, RESID>(trow, drow, g, same_phase, ub + lane, mst, msd, rho) : 0.0;
       for (int l = 0; l < 64 && ub + l < hi; ++l) {
         const double vl = rl_d(v, l);
         const double Pn = P + vl;
@@ -909,15 +1027,15 @@ __device__ int locate_units(const T* trow, const T* drow, const Geom& g, int64_t
       }
     }
     if (uj >= 0) {
-      float ft[VEC], fd[VEC];
-      const int n = unit_load(trow, g, uj, ft);
+      const uint4 rt = unit_raw<T, false>(trow, g, uj);
+      const uint4 rd = RESID ? unit_raw2<T, false>(drow, g, uj, same_phase) : rt;
+      double q[VEC];
+      unit_weights<T, RESID>(rt, rd, mst, msd, rho, q);
       const int64_t first = unit_first<T>(g, uj);
-      if (RESID) range_load(drow, first, n, fd);
       double Q = 0.0;
-      for (int e = 0; e < n; ++e) {
-        const double q = q_weight<RESID>(ft[e], RESID ? fd[e] : 0.f, mst, msd, rho);
-        Q += q;
-        if (q > 0.0 && (last || base + (ex + (Puj + Q)) > x)) {
+      for (int e = 0; e < VEC; ++e) {
+        Q += q[e];
+        if (q[e] > 0.0 && (last || base + (ex + (Puj + Q)) > x)) {
           y = int(first + e);
           if (!last) break;
         }
@@ -934,7 +1052,7 @@ __device__ int locate_units(const T* trow, const T* drow, const Geom& g, int64_t
 template <typename T>
 __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S, const SlicePart* __restrict__ ws) {
   constexpr int BD = kSampleBD;
-  __shared__ double sd[BD / 64];
+  __shared__ double sd[2 * (BD / 64)];
   __shared__ int si[BD / 64];
   __shared__ double s_sc[2];
   __shared__ int s_n;
@@ -956,19 +1074,19 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
   const int64_t dr = (int64_t)b * a.k_max + (resid ? nacc : 0);
   const T* trow = reinterpret_cast<const T*>(a.target) + tr * a.tstride;
   const T* drow = reinterpret_cast<const T*>(a.draft) + dr * a.dstride;
+  const bool same_phase = ((reinterpret_cast<uintptr_t>(trow) ^ reinterpret_cast<uintptr_t>(drow)) & 15u) == 0;
   const float mst = a.tstats[tr].max_logit * kLog2e;
   const float msd = resid ? a.dstats[dr].max_logit * kLog2e : 0.f;
   const float rho0 = resid ? (float)((double)a.tstats[tr].sum_exp / (double)a.dstats[dr].sum_exp) : 0.f;
   const SlicePart* P = ws + (int64_t)b * S;
   // fresh normalisers and the exact ratio
-  double et = 0.0, ed = 0.0;
+  double tot[2] = {0.0, 0.0};
   for (int s = t; s < S; s += BD) {
-    et += P[s].et;
-    ed += P[s].ed;
+    tot[0] += P[s].et;
+    tot[1] += P[s].ed;
   }
-  const double At = block_all_d<BD>(et, OpSumD(), sd);
-  const double Ad = block_all_d<BD>(ed, OpSumD(), sd);
-  const double rho = resid ? At / Ad : 0.0;
+  block_sum_n<BD, 2>(tot, sd);
+  const double rho = resid ? tot[0] / tot[1] : 0.0;
   // slice masses (first-order correction of the rho0 sums), scanned in slice order;
   // a zero residual falls back to the target row itself
   auto mass = [&](int s, bool rs) -> double {
@@ -978,6 +1096,8 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
   };
   int y = -1;
   const float u = a.unif[off + kb];
+  const Geom g = row_geom(trow, a.V);
+  const int64_t nu = g.nvec + 2;
   for (int pass = 0; pass < 2 && y < 0; ++pass) {
     // per-thread contiguous run of slices
     const int slo = (int)((int64_t)t * S / BD), shi = (int)((int64_t)(t + 1) * S / BD);
@@ -996,10 +1116,9 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
     const double x = (double)u * R;
     const int tp = block_all_i<BD>((sm > 0.0 && end > x) ? t : INT32_MAX, OpMinI(), si);
     const int tq = tp == INT32_MAX ? tlast : tp;
-    // slice inside thread tq's run (every thread repeats the same sequential sums)
-    __syncthreads();
     if (t == tq) s_sc[0] = excl;
     __syncthreads();
+    // the slice inside thread tq's run, repeating its sequential sums exactly
     const double ex = s_sc[0];
     const int qlo = (int)((int64_t)tq * S / BD), qhi = (int)((int64_t)(tq + 1) * S / BD);
     double Pacc = 0.0;
@@ -1015,14 +1134,12 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
       }
       Pacc = Pn;
     }
-    const Geom g = row_geom(trow, a.V);
-    const int64_t nu = g.nvec + 2;
     const int64_t ulo = (int64_t)sstar * kSliceUnits;
     const int64_t uhi = ulo + kSliceUnits < nu ? ulo + kSliceUnits : nu;
     if (resid)
-      y = locate_units<T, true>(trow, drow, g, ulo, uhi, mst, msd, rho, sbase, x, sd, si, s_sc);
+      y = locate_units<T, true>(trow, drow, g, same_phase, ulo, uhi, mst, msd, rho, sbase, x, sd, si, s_sc);
     else
-      y = locate_units<T, false>(trow, trow, g, ulo, uhi, mst, mst, 0.0, sbase, x, sd, si, s_sc);
+      y = locate_units<T, false>(trow, trow, g, true, ulo, uhi, mst, mst, 0.0, sbase, x, sd, si, s_sc);
     if (y < 0 && resid) {
       resid = false;
       continue;
@@ -1086,7 +1203,7 @@ cmsd_status cmsd_confidence(const void* logits, int32_t dtype, int64_t n_rows, i
   if (n_rows == 0) return CMSD_OK;
   if (!logits || !stats || !aligned(logits, es) || !aligned(stats, 4)) return CMSD_ERR_ARG;
   if (row_stride > INT64_MAX / n_rows) return CMSD_ERR_ARG;
-  const ConfArgs a{l1, l2, l3, params->beta_margin};
+  const ConfArgs a{l1, l2, l3, params->beta_margin, log((double)vocab)};
   const dim3 grid((unsigned)n_rows), block(kConfBD);
   if (dtype == CMSD_F32)
     hipLaunchKernelGGL((k_confidence<float, kConfBD>), grid, block, 0, as_stream(stream),
@@ -1159,15 +1276,16 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   a.next_tok = next_token;
   const hipStream_t st = as_stream(stream);
   const int S = verify_slices(vocab);
+  const int SW = (S + kSubPerWG - 1) / kSubPerWG;
   SlicePart* ws = static_cast<SlicePart*>(workspace);
-  const unsigned gp = (unsigned)((int64_t)batch * S);
+  const unsigned gp = (unsigned)((int64_t)batch * SW);
   if (dtype == CMSD_F32) {
     hipLaunchKernelGGL((k_target_rows<float, kRowBD>), dim3((unsigned)target_rows), dim3(kRowBD), 0, st, a);
-    hipLaunchKernelGGL((k_final_parts<float>), dim3(gp), dim3(kPartBD), 0, st, a, S, ws);
+    hipLaunchKernelGGL((k_final_parts<float>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
     hipLaunchKernelGGL((k_final_sample<float>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   } else {
     hipLaunchKernelGGL((k_target_rows<Bf16, kRowBD>), dim3((unsigned)target_rows), dim3(kRowBD), 0, st, a);
-    hipLaunchKernelGGL((k_final_parts<Bf16>), dim3(gp), dim3(kPartBD), 0, st, a, S, ws);
+    hipLaunchKernelGGL((k_final_parts<Bf16>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
     hipLaunchKernelGGL((k_final_sample<Bf16>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   }
   return launched();
