@@ -521,7 +521,14 @@ __global__ __launch_bounds__(kDraftBD) void k_draft_len(const cmsd_row_stats* __
     if (b < B) {
       const cmsd_row_stats* p = stats + (int64_t)b * k_max;
       double s = 0.0;
-      for (int i = 0; i < k_max; ++i) s += (double)p[i].conf;
+      for (int i0 = 0; i0 < k_max; i0 += 8) {
+        float c[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) c[j] = i0 + j < k_max ? p[i0 + j].conf : 0.f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (i0 + j < k_max) s += (double)c[j];
+      }
       const double x = (double)alpha * (s / (double)k_max) * (double)k_max;
       const double fl = floor(x);
       int kf = fl < (double)k_min ? k_min : (fl > (double)k_max ? k_max : (int)fl);
@@ -888,7 +895,7 @@ __device__ __forceinline__ void parts_slice(const T* trow, const T* drow, const 
 template <typename T>
 __global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, int SW, SlicePart* __restrict__ ws) {
   constexpr int BD = kPartBD;
-  __shared__ double sd[4 * (BD / 64)];
+  __shared__ double sd[kSubPerWG * 4 * (BD / 64)];
   __shared__ int s_n;
   const int t = threadIdx.x;
   const int b = blockIdx.x / SW, sl0 = (blockIdx.x % SW) * kSubPerWG;
@@ -907,17 +914,35 @@ __global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, in
   const float msd = resid ? a.dstats[dr].max_logit * kLog2e : 0.f;
   const float rho0 = resid ? (float)((double)a.tstats[tr].sum_exp / (double)a.dstats[dr].sum_exp) : 0.f;
   const Geom g = row_geom(trow, a.V);
+  const int64_t nu = g.nvec + 2;
+  // wave-level sums per slice (uniform values), one LDS round at the end
+  double ws_w[kSubPerWG][4];
+#pragma unroll
   for (int k = 0; k < kSubPerWG; ++k) {
-    const int sl = sl0 + k;
-    if (sl >= S) break;
+    const int64_t u0 = (int64_t)(sl0 + k) * kSliceUnits;
     double sum[4] = {0.0, 0.0, 0.0, 0.0};
-    const int64_t u0 = (int64_t)sl * kSliceUnits;
-    if (resid)
-      parts_slice<T, true>(trow, drow, g, same_phase, u0, mst, msd, rho0, sum);
-    else
-      parts_slice<T, false>(trow, trow, g, true, u0, mst, 0.f, 0.f, sum);
-    block_sum_n<BD, 4>(sum, sd);
-    if (t == 0) ws[(int64_t)b * S + sl] = SlicePart{sum[0], sum[1], sum[2], sum[3]};
+    if (sl0 + k < S && u0 < nu) {
+      if (resid)
+        parts_slice<T, true>(trow, drow, g, same_phase, u0, mst, msd, rho0, sum);
+      else
+        parts_slice<T, false>(trow, trow, g, true, u0, mst, 0.f, 0.f, sum);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) ws_w[k][j] = wave_all_d(sum[j], OpSumD());
+  }
+  constexpr int NW = BD / 64;
+  if ((t & 63) == 0) {
+#pragma unroll
+    for (int k = 0; k < kSubPerWG; ++k)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sd[(k * 4 + j) * NW + (t >> 6)] = ws_w[k][j];
+  }
+  __syncthreads();
+  if (t < kSubPerWG * 4) {
+    const int k = t >> 2;
+    double r = sd[t * NW];
+    for (int i = 1; i < NW; ++i) r += sd[t * NW + i];
+    if (sl0 + k < S) reinterpret_cast<double*>(ws + (int64_t)b * S + sl0 + k)[t & 3] = r;
   }
 }
 
@@ -1162,9 +1187,10 @@ constexpr int kConfBD = 256;
 constexpr int kRowBD = 256;
 
 // Number of vocabulary slices of the final-token pass: units are 16-byte vectors
-// plus a head and a tail unit; the bf16 geometry (8 per vector) has the most units.
-int verify_slices(int64_t vocab) {
-  const int64_t units = vocab / 4 + 2;  // upper bound for either dtype (fp32: 4 per vector)
+// plus a head and a tail unit (the head shortens the vector run, so nvec + 2 is at
+// most vocab / VEC + 2).  The workspace is sized for fp32, the dtype with most units.
+int verify_slices(int64_t vocab, int elem_bytes) {
+  const int64_t units = vocab / (16 / elem_bytes) + 2;
   return (int)((units + kSliceUnits - 1) / kSliceUnits);
 }
 
@@ -1187,7 +1213,7 @@ int32_t cmsd_version(void) { return (1 << 16) | 1; }
 
 size_t cmsd_verify_workspace_bytes(int32_t batch, int64_t vocab) {
   if (batch <= 0 || vocab < 2 || vocab > INT32_MAX) return 0;
-  return (size_t)batch * (size_t)verify_slices(vocab) * sizeof(SlicePart);
+  return (size_t)batch * (size_t)verify_slices(vocab, 4) * sizeof(SlicePart);
 }
 
 cmsd_status cmsd_confidence(const void* logits, int32_t dtype, int64_t n_rows, int64_t vocab, int64_t row_stride,
@@ -1248,7 +1274,7 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
       !target_stats || !n_accepted || !next_token || !workspace)
     return CMSD_ERR_ARG;
   if (workspace_bytes < cmsd_verify_workspace_bytes(batch, vocab) || !aligned(workspace, 8)) return CMSD_ERR_ARG;
-  if ((int64_t)batch * verify_slices(vocab) > INT32_MAX) return CMSD_ERR_ARG;
+  if ((int64_t)batch * verify_slices(vocab, 4) > INT32_MAX) return CMSD_ERR_ARG;
   if (!aligned(draft_logits, es) || !aligned(target_logits, es) || !aligned(draft_stats, 4) ||
       !aligned(target_offsets, 4) || !aligned(draft_len, 4) || !aligned(drafted, 4) || !aligned(uniforms, 4) ||
       !aligned(target_stats, 4) || !aligned(n_accepted, 4) || !aligned(next_token, 4))
@@ -1275,7 +1301,7 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   a.n_acc = n_accepted;
   a.next_tok = next_token;
   const hipStream_t st = as_stream(stream);
-  const int S = verify_slices(vocab);
+  const int S = verify_slices(vocab, (int)es);
   const int SW = (S + kSubPerWG - 1) / kSubPerWG;
   SlicePart* ws = static_cast<SlicePart*>(workspace);
   const unsigned gp = (unsigned)((int64_t)batch * SW);
