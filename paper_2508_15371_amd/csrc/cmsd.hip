@@ -231,6 +231,42 @@ __device__ __forceinline__ void block_sum_n(double (&v)[N], double* lds) {
   }
 }
 
+// Streams the nr full rounds of a row: round k is U vectors per thread at
+// vp[(k*U + u)*BD + t].  DEPTH rounds of loads are kept in flight in a ring of
+// registers (fully unrolled, so each slot is consumed and then refilled in place:
+// no register copies).  prep() runs once the first loads are issued (work that
+// must precede the first round overlaps their latency); consume(raw[U], k) is
+// called in round order.
+#ifndef CMSD_STREAM_DEPTH
+#define CMSD_STREAM_DEPTH 2
+#endif
+template <int U, int BD, int DEPTH, typename P, typename F>
+__device__ __forceinline__ void stream_rounds(const uint4* vp, int64_t nr, int t, P&& prep, F&& consume) {
+  uint4 buf[DEPTH][U];
+#pragma unroll
+  for (int d = 0; d < DEPTH; ++d) {
+    if (d < nr) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) buf[d][u] = ld_stream(vp + ((int64_t)d * U + u) * BD + t);
+    }
+  }
+  prep();
+  for (int64_t k0 = 0; k0 < nr; k0 += DEPTH) {
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) {
+      const int64_t k = k0 + d;
+      if (k < nr) {
+        consume(buf[d], k);
+        const int64_t kn = k + DEPTH;
+        if (kn < nr) {
+#pragma unroll
+          for (int u = 0; u < U; ++u) buf[d][u] = ld_stream(vp + (kn * U + u) * BD + t);
+        }
+      }
+    }
+  }
+}
+
 // ----------------------------------------------------------------------------- streaming row state
 // Online normaliser in base-2 units relative to a running scaled max ms = fl(max*log2e):
 //   A = sum 2^x,  T = sum 2^x * x,  x = z*log2e - ms.
@@ -358,25 +394,12 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
     if (t < g.head) conf_one(s, E::load(row + t), 0);
 
     // full rounds, next round's loads issued before the current one is consumed
-    uint4 nxt[U];
-    if (nr > 0) {
-#pragma unroll
-      for (int u = 0; u < U; ++u) nxt[u] = ld_stream(vp + u * BD + t);
-    }
-    for (int64_t k = 0; k < nr; ++k) {
-      uint4 cur[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) cur[u] = nxt[u];
-      if (k + 1 < nr) {
-        const uint4* q = vp + (k + 1) * per_round;
-#pragma unroll
-        for (int u = 0; u < U; ++u) nxt[u] = ld_stream(q + u * BD + t);
-      }
+    stream_rounds<U, BD, CMSD_STREAM_DEPTH>(vp, nr, t, [] {}, [&](const uint4 (&raw)[U], int64_t k) {
       float f[N];
 #pragma unroll
-      for (int u = 0; u < U; ++u) E::unpack(cur[u], f + u * VEC);
+      for (int u = 0; u < U; ++u) E::unpack(raw[u], f + u * VEC);
       conf_chunk<N, false>(s, f, 0xffffffffu, int(k + 1));
-    }
+    });
     // partial round
     const int64_t rb = nr * per_round;
     if (rb < g.nvec) {
@@ -586,54 +609,45 @@ struct TargetState {
   float t1 = -INFINITY;
 };
 
-template <int N, bool GUARD, bool COUNT>
-__device__ __forceinline__ void target_chunk(TargetState& s, const float* f, uint32_t valid, float gz, int beta,
-                                             int& wcnt) {
+template <int N, bool GUARD>
+__device__ __forceinline__ void target_chunk(TargetState& s, const float* f, uint32_t valid, bool count, float gz,
+                                             int beta, int& wcnt) {
   const float cmax = chunk_max<N>(f);
   s.t1 = fmaxf(s.t1, cmax);
   norm_chunk<N, GUARD, false>(s.n, f, valid, cmax);
-  if (COUNT) {
-    // wave-uniform: skip chunks where no lane holds a logit above the drafted one,
-    // and stop once this wave alone has seen top_beta of them
-    if (wcnt < beta && __ballot(cmax > gz) != 0ull) {
+  // wave-uniform: count only when the gate needs it, skip chunks where no lane holds
+  // a logit above the drafted one, and stop once this wave alone has seen top_beta
+  if (count && wcnt < beta && __ballot(cmax > gz) != 0ull) {
 #pragma unroll
-      for (int j = 0; j < N; ++j) wcnt += __popcll(__ballot(f[j] > gz));
-    }
+    for (int j = 0; j < N; ++j) wcnt += __popcll(__ballot(f[j] > gz));
   }
 }
 
-template <typename T, int BD, bool COUNT>
-__device__ __forceinline__ void target_stream(const T* row, const Geom& g, float gz, int beta, TargetState& s,
-                                              int& wcnt) {
+// The target row pass.  prep() resolves the drafted token (and with it `count` and
+// `gz`) while the first rounds of the row are already in flight.
+template <typename T, int BD, typename P>
+__device__ __forceinline__ void target_stream(const T* row, const Geom& g, const bool& count, const float& gz,
+                                              int beta, TargetState& s, int& wcnt, P&& prep) {
   using E = Elem<T>;
   constexpr int VEC = E::VEC, U = E::U, N = VEC * U;
   const int t = threadIdx.x;
   const uint4* vp = reinterpret_cast<const uint4*>(row + g.head);
   const int64_t per_round = (int64_t)U * BD;
   const int64_t nr = g.nvec / per_round;
-  {
-    float f[1] = {t < g.head ? E::load(row + t) : -INFINITY};
-    target_chunk<1, true, COUNT>(s, f, t < g.head ? 1u : 0u, gz, beta, wcnt);
-  }
-  uint4 nxt[U];
-  if (nr > 0) {
+  const float head = t < g.head ? E::load(row + t) : -INFINITY;
+  stream_rounds<U, BD, CMSD_STREAM_DEPTH>(
+      vp, nr, t,
+      [&] {
+        prep();
+        float f[1] = {head};
+        target_chunk<1, true>(s, f, t < g.head ? 1u : 0u, count, gz, beta, wcnt);
+      },
+      [&](const uint4 (&raw)[U], int64_t) {
+        float f[N];
 #pragma unroll
-    for (int u = 0; u < U; ++u) nxt[u] = ld_stream(vp + u * BD + t);
-  }
-  for (int64_t k = 0; k < nr; ++k) {
-    uint4 cur[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) cur[u] = nxt[u];
-    if (k + 1 < nr) {
-      const uint4* q = vp + (k + 1) * per_round;
-#pragma unroll
-      for (int u = 0; u < U; ++u) nxt[u] = ld_stream(q + u * BD + t);
-    }
-    float f[N];
-#pragma unroll
-    for (int u = 0; u < U; ++u) E::unpack(cur[u], f + u * VEC);
-    target_chunk<N, false, COUNT>(s, f, 0xffffffffu, gz, beta, wcnt);
-  }
+        for (int u = 0; u < U; ++u) E::unpack(raw[u], f + u * VEC);
+        target_chunk<N, false>(s, f, 0xffffffffu, count, gz, beta, wcnt);
+      });
   const int64_t rb = nr * per_round;
   if (rb < g.nvec) {
     float f[N];
@@ -649,12 +663,12 @@ __device__ __forceinline__ void target_stream(const T* row, const Geom& g, float
         for (int e = 0; e < VEC; ++e) f[u * VEC + e] = -INFINITY;
       }
     }
-    target_chunk<N, true, COUNT>(s, f, valid, gz, beta, wcnt);
+    target_chunk<N, true>(s, f, valid, count, gz, beta, wcnt);
   }
   {
     const int64_t tail0 = g.head + g.nvec * VEC;
     float f[1] = {t < g.tail ? E::load(row + tail0 + t) : -INFINITY};
-    target_chunk<1, true, COUNT>(s, f, t < g.tail ? 1u : 0u, gz, beta, wcnt);
+    target_chunk<1, true>(s, f, t < g.tail ? 1u : 0u, count, gz, beta, wcnt);
   }
 }
 
@@ -668,48 +682,44 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
   const int64_t r = blockIdx.x;
   const int total = a.off[a.B];
   if (r >= total || r >= a.target_rows) return;
-
-  // sequence owning row r: number of offsets[1..B] that are <= r
-  int cnt = 0;
-  for (int j = 1 + t; j <= a.B; j += BD) cnt += a.off[j] <= r ? 1 : 0;
-  int b = block_all_i<BD>(cnt, OpSumI(), si);
-  b = b < a.B ? b : a.B - 1;
-  const int64_t off_b = a.off[b], off_b1 = a.off[b + 1];
-  const int kb = a.klen[b];
-  cmsd_target_stats* o = a.tstats + r;
-  const bool layout_ok = kb >= 0 && kb <= a.k_max && off_b >= 0 && off_b <= r && r < off_b1 &&
-                         off_b1 == off_b + kb + 1 && off_b1 <= a.target_rows;
-  if (!layout_ok) {
-    if (t == 0) *o = cmsd_target_stats{NAN, NAN, -1, -2};
-    return;
-  }
-  const int i = int(r - off_b);
-  const bool has_draft = i < kb;
   const T* trow = reinterpret_cast<const T*>(a.target) + r * a.tstride;
-  int y = 0;
-  float gz = -INFINITY, zd = -INFINITY, cm = 0.f, dm = 0.f, dA = 1.f;
-  if (has_draft) {
-    const int64_t drow = (int64_t)b * a.k_max + i;
-    y = a.drafted[drow];
-    if (y < 0 || (int64_t)y >= a.V) {
-      if (t == 0) *o = cmsd_target_stats{NAN, NAN, -1, -2};
-      return;
-    }
-    gz = E::load(trow + y);
-    zd = E::load(reinterpret_cast<const T*>(a.draft) + drow * a.dstride + y);
-    const cmsd_row_stats ds = a.dstats[drow];
-    cm = ds.conf;
-    dm = ds.max_logit;
-    dA = ds.sum_exp;
-  }
   const Geom g = row_geom(trow, a.V);
+
+  // resolved by prep(), while the first rounds of the row load
+  bool valid = false, has_draft = false, count = false;
+  float gz = -INFINITY, zd = -INFINITY, cm = 0.f, dm = 0.f, dA = 1.f;
+  auto prep = [&] {
+    // sequence owning row r: number of offsets[1..B] that are <= r
+    int cnt = 0;
+    for (int j = 1 + t; j <= a.B; j += BD) cnt += a.off[j] <= r ? 1 : 0;
+    int b = block_all_i<BD>(cnt, OpSumI(), si);
+    b = b < a.B ? b : a.B - 1;
+    const int64_t off_b = a.off[b], off_b1 = a.off[b + 1];
+    const int kb = a.klen[b];
+    valid = kb >= 0 && kb <= a.k_max && off_b >= 0 && off_b <= r && r < off_b1 && off_b1 == off_b + kb + 1 &&
+            off_b1 <= a.target_rows;
+    const int i = int(r - off_b);
+    has_draft = valid && i < kb;
+    if (has_draft) {
+      const int64_t drow = (int64_t)b * a.k_max + i;
+      const int y = a.drafted[drow];
+      if (y < 0 || (int64_t)y >= a.V) {
+        valid = false;
+        has_draft = false;
+      } else {
+        gz = E::load(trow + y);
+        zd = E::load(reinterpret_cast<const T*>(a.draft) + drow * a.dstride + y);
+        const cmsd_row_stats ds = a.dstats[drow];
+        cm = ds.conf;
+        dm = ds.max_logit;
+        dA = ds.sum_exp;
+      }
+    }
+    count = has_draft && a.mode == CMSD_MODE_CM && a.beta > 0;
+  };
   TargetState s;
   int wcnt = 0;
-  const bool count = has_draft && a.mode == CMSD_MODE_CM && a.beta > 0;
-  if (count)
-    target_stream<T, BD, true>(trow, g, gz, a.beta, s, wcnt);
-  else
-    target_stream<T, BD, false>(trow, g, gz, a.beta, s, wcnt);
+  target_stream<T, BD>(trow, g, count, gz, a.beta, s, wcnt, prep);
 
   const float m = block_all_f<BD>(s.t1, OpMax(), sf);
   const float ms_row = m * kLog2e;
@@ -736,7 +746,9 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
     cmsd_target_stats res;
     res.max_logit = m;
     res.sum_exp = (float)A;
-    if (!has_draft) {
+    if (!valid) {
+      res = cmsd_target_stats{NAN, NAN, -1, -2};
+    } else if (!has_draft) {
       res.n_greater = -1;
       res.accept = -1;
     } else {
@@ -756,7 +768,7 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
       res.n_greater = ng;
       res.accept = (stoch || (a.mode == CMSD_MODE_CM && gate)) ? 1 : 0;
     }
-    *o = res;
+    a.tstats[r] = res;
   }
 }
 
