@@ -94,8 +94,8 @@ def _traffic(workload: str):
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="c4", choices=["c2", "c3", "c4"])
     ap.add_argument("--mode", default="cm", choices=["cm", "standard"])
     ap.add_argument("--seed", type=int, default=0)
