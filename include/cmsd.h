@@ -180,11 +180,9 @@ cmsd_status cmsd_draft_len(const cmsd_row_stats* stats, int32_t batch, const cms
  *                   out of range, drafted id outside [0, vocab)).
  *   next_token      device, batch int32 (output): the final token; -1 when invalid.
  *   workspace       device scratch of at least cmsd_verify_workspace_bytes(batch,
- *                   vocab) bytes, 8-byte aligned, owned by the caller: per-sequence
- *                   counters and hand-off records, per-vocabulary-slice partial sums.
- *                   Its contents need no initialisation (the call resets what it
- *                   uses) and are meaningless after the call.  Calls that share a
- *                   workspace must be ordered (same stream); overlapping calls race.
+ *                   vocab) bytes, 8-byte aligned, owned by the caller; its contents
+ *                   need no initialisation and are meaningless after the call.  Calls
+ *                   that share a workspace must be ordered (same stream).
  *   workspace_bytes its size.
  * Errors: CMSD_ERR_ARG, CMSD_ERR_DTYPE, CMSD_ERR_LAUNCH.
  */
@@ -196,9 +194,9 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
                         int32_t* n_accepted, int32_t* next_token, void* workspace, size_t workspace_bytes,
                         void* stream);
 
-/* Workspace cmsd_verify needs for `batch` sequences over `vocab`: per sequence, one
- * 32-byte record per vocabulary slice (1024 16-byte vectors), a 48-byte hand-off
- * record and three counters; 0 for batch <= 0 or an invalid vocab. */
+/* Workspace cmsd_verify needs for `batch` sequences over `vocab` (per-sequence,
+ * per-vocabulary-slice partial sums of the final-token sample); 0 for batch <= 0
+ * or an invalid vocab. */
 size_t cmsd_verify_workspace_bytes(int32_t batch, int64_t vocab);
 
 /* Human-readable name of a status code (static string). */

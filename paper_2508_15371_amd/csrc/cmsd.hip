@@ -11,12 +11,10 @@
 //   k_target_rows  one workgroup per packed target row: max / sum-exp of the row,
 //                  scalar (ballot + s_bcnt1) count of logits above the drafted
 //                  token's, and the acceptance decision of that position.
-//   k_final_parts  B x ceil(S/4) workgroups: vocabulary-slice partial sums of the
-//                  final-token row (pair); the last workgroup of each sequence takes
-//                  the inverse-CDF sample (slice scan, then an exact per-thread-span
-//                  scan and a wave-level locate that repeats the scan's sums).
-//   The first rejected position comes from atomicMin over the rows' accept flags;
-//   the last row of each sequence to finish publishes the final-token descriptor.
+//   k_final        one workgroup per sequence: ballot-based first-reject scan, then
+//                  an inverse-CDF sample from the residual (or bonus) row using a
+//                  per-thread contiguous span, a workgroup scan and a wave-level
+//                  locate that reproduces the scan's sums bit for bit.
 //
 // Numerics: exponentials are evaluated as 2^(z*log2e - m*log2e) with one FMA and
 // v_exp_f32; per-thread partial sums are fp32 over 32-element chunks, the
@@ -604,24 +602,6 @@ struct VerifyArgs {
   cmsd_target_stats* tstats;
   int32_t* n_acc;
   int32_t* next_tok;
-  // workspace views (see ws_layout)
-  struct SeqDesc* desc;
-  int32_t* cnt_rows;   // per sequence: target rows finished
-  int32_t* cnt_parts;  // per sequence: slice-partial workgroups finished
-  int32_t* first_rej;  // per sequence: first rejected position (-1: invalid input)
-};
-
-// Per-sequence hand-off from the target-row pass to the final-token pass.
-struct SeqDesc {
-  int64_t tr;   // packed target row of the final sample
-  int64_t dr;   // drafter row of the residual (when nacc < kb)
-  int32_t nacc; // accepted prefix length, -1 for an invalid sequence
-  int32_t kb;   // draft length
-  float mst;    // target row max * log2e
-  float msd;    // drafter row max * log2e
-  float rho0;   // A_t / A_d from the row passes
-  float u;      // the final-sample uniform
-  int32_t pad[2];
 };
 
 struct TargetState {
@@ -708,20 +688,17 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
   // resolved by prep(), while the first rounds of the row load
   bool valid = false, has_draft = false, count = false;
   float gz = -INFINITY, zd = -INFINITY, cm = 0.f, dm = 0.f, dA = 1.f;
-  int b = 0, kb = 0, i = 0;
-  int64_t off_b = 0;
   auto prep = [&] {
     // sequence owning row r: number of offsets[1..B] that are <= r
     int cnt = 0;
     for (int j = 1 + t; j <= a.B; j += BD) cnt += a.off[j] <= r ? 1 : 0;
-    b = block_all_i<BD>(cnt, OpSumI(), si);
+    int b = block_all_i<BD>(cnt, OpSumI(), si);
     b = b < a.B ? b : a.B - 1;
-    off_b = a.off[b];
-    const int64_t off_b1 = a.off[b + 1];
-    kb = a.klen[b];
+    const int64_t off_b = a.off[b], off_b1 = a.off[b + 1];
+    const int kb = a.klen[b];
     valid = kb >= 0 && kb <= a.k_max && off_b >= 0 && off_b <= r && r < off_b1 && off_b1 == off_b + kb + 1 &&
             off_b1 <= a.target_rows;
-    i = int(r - off_b);
+    const int i = int(r - off_b);
     has_draft = valid && i < kb;
     if (has_draft) {
       const int64_t drow = (int64_t)b * a.k_max + i;
@@ -792,66 +769,27 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
       res.accept = (stoch || (a.mode == CMSD_MODE_CM && gate)) ? 1 : 0;
     }
     a.tstats[r] = res;
-    // completion: rejections lower the sequence's first rejected position; the last
-    // of its k_b + 1 rows publishes the descriptor of the final-token pass
-    if (res.accept == 0) atomicMin(a.first_rej + b, i);
-    if (res.accept == -2) atomicMin(a.first_rej + b, -1);
-    __threadfence();
-    if (atomicAdd(a.cnt_rows + b, 1) == kb && valid) {
-      __threadfence();
-      const int fr = __hip_atomic_load(a.first_rej + b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      SeqDesc d{};
-      d.kb = kb;
-      d.nacc = fr < 0 ? -1 : (fr < kb ? fr : kb);
-      if (d.nacc >= 0) {
-        const bool resid = d.nacc < kb;
-        d.tr = off_b + (resid ? d.nacc : kb);
-        d.dr = (int64_t)b * a.k_max + (resid ? d.nacc : 0);
-        const cmsd_target_stats tt = a.tstats[d.tr];
-        d.mst = tt.max_logit * kLog2e;
-        d.u = a.unif[off_b + kb];
-        if (resid) {
-          const cmsd_row_stats ds = a.dstats[d.dr];
-          d.msd = ds.max_logit * kLog2e;
-          d.rho0 = (float)((double)tt.sum_exp / (double)ds.sum_exp);
-        }
-      }
-      a.desc[b] = d;
-    }
-  }
-}
-
-// Resets the per-sequence counters and descriptors before the target-row pass.
-__global__ __launch_bounds__(256) void k_verify_init(VerifyArgs a) {
-  const int b = blockIdx.x * 256 + threadIdx.x;
-  if (b < a.B) {
-    a.cnt_rows[b] = 0;
-    a.cnt_parts[b] = 0;
-    a.first_rej[b] = INT32_MAX;
-    SeqDesc d{};
-    d.nacc = -1;
-    a.desc[b] = d;
   }
 }
 
 // ----------------------------------------------------------------------------- K4 final token
 // The final token of sequence b is an inverse-CDF sample over one target row (the
 // bonus row k_b when every draft passed) or over the residual max(0, p_t - p_d) of
-// the target and drafter rows at the first rejection c.  The last target row of a
-// sequence to finish publishes a descriptor (c, the rows, their maxima, rho0 =
-// A_t / A_d from the row passes); then k_final_parts runs B x ceil(S/4) workgroups,
-// each streaming 4 slices of the row (pair) into fp64 partials
-// {sum e_t, sum e_d, sum q0, sum_{q0>0} e_d}, e = 2^(z log2e - m log2e),
-// q0 = max(0, e_t - rho0 e_d).  The last workgroup of each sequence takes the
-// sample: rho = sum e_t / sum e_d from the fresh sums, slice masses corrected to
-// first order in rho - rho0, a scan over slices, then an exact scan/locate inside
-// one slice.
+// the target and drafter rows at the first rejection c.  Two kernels:
+//   k_final_parts   B x ceil(S/4) workgroups, each covering 4 slices of the row
+//                   (pair): fp64 partials {sum e_t, sum e_d, sum q0, sum_{q0>0} e_d}
+//                   per slice, e = 2^(z log2e - m log2e), q0 = max(0, e_t - rho0 e_d)
+//                   with rho0 = A_t / A_d from the row passes.
+//   k_final_sample  one workgroup per sequence: rho = sum e_t / sum e_d from the
+//                   fresh sums, slice masses corrected to first order in rho - rho0,
+//                   a scan over slices, then an exact scan/locate inside one slice.
 // A unit is the head (unit 0), one 16-byte vector (1..nvec) or the tail (nvec+1) of
 // the target row, always handled as one raw 16-byte vector padded with -inf (whose
 // weights are exactly 0); slices are runs of kSliceUnits units.
 constexpr int kPartBD = 256;
 constexpr int kSliceUnits = 1024;
 constexpr int kSubPerWG = 4;
+constexpr int kSampleBD = 256;
 
 struct SlicePart {
   double et, ed, q, qd;
@@ -887,6 +825,37 @@ __device__ __forceinline__ uint4 unit_raw2(const T* row, const Geom& g, int64_t 
   }
   const int n = unit_count<T>(g, u);
   return n > 0 ? E::raw_partial(row + unit_first<T>(g, u), n) : E::raw_ninf();
+}
+
+// Sequence bookkeeping shared by both kernels: layout check and the first rejected
+// position, by ballots over the accept flags (wave 0 computes, LDS broadcasts).
+// Returns -1 for an invalid sequence.
+__device__ int seq_prefix(const VerifyArgs& a, int b, int64_t& off, int& kb, int* s_out) {
+  const int t = threadIdx.x, lane = t & 63;
+  off = a.off[b];
+  const int64_t off1 = a.off[b + 1];
+  kb = a.klen[b];
+  const bool ok = kb >= 0 && kb <= a.k_max && off >= 0 && off1 == off + kb + 1 && off1 <= a.target_rows;
+  if (t < 64) {
+    int nacc = -1;
+    if (ok) {
+      nacc = kb;
+      bool bad = a.tstats[off + kb].accept != -1;
+      for (int base = 0; base < kb; base += 64) {
+        const int i = base + lane;
+        const int acc = i < kb ? a.tstats[off + i].accept : 1;
+        const unsigned long long rej = __ballot(acc == 0);
+        if (__ballot(acc != 0 && acc != 1) != 0ull) bad = true;
+        if (rej != 0ull && nacc == kb) nacc = base + __builtin_ctzll(rej);
+      }
+      if (bad) nacc = -1;
+    }
+    if (lane == 0) *s_out = nacc;
+  }
+  __syncthreads();
+  const int r = *s_out;
+  __syncthreads();
+  return r;
 }
 
 // Partial sums of one raw unit: e_t, e_d, q0 and e_d where q0 > 0.
@@ -936,27 +905,26 @@ __device__ __forceinline__ void parts_slice(const T* trow, const T* drow, const 
 }
 
 template <typename T>
-__device__ int final_sample_seq(const VerifyArgs& a, const SeqDesc& D, int S, const SlicePart* __restrict__ P,
-                                double* sd, int* si, double* s_sc);
-
-template <typename T>
 __global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, int SW, SlicePart* __restrict__ ws) {
   constexpr int BD = kPartBD;
   __shared__ double sd[kSubPerWG * 4 * (BD / 64)];
-  __shared__ int si[BD / 64];
-  __shared__ double s_sc[2];
-  __shared__ int s_last;
+  __shared__ int s_n;
   const int t = threadIdx.x;
   const int b = blockIdx.x / SW, sl0 = (blockIdx.x % SW) * kSubPerWG;
   if (b >= a.B) return;
-  const SeqDesc D = a.desc[b];
-  const bool resid = D.nacc >= 0 && D.nacc < D.kb;
-  const bool ok = D.nacc >= 0 && D.tr >= 0 && D.tr < a.target_rows &&
-                  (!resid || (D.dr >= 0 && D.dr < (int64_t)a.B * a.k_max));
-  const T* trow = reinterpret_cast<const T*>(a.target) + (ok ? D.tr : 0) * a.tstride;
-  const T* drow = reinterpret_cast<const T*>(a.draft) + (ok && resid ? D.dr : 0) * a.dstride;
+  int64_t off;
+  int kb;
+  const int nacc = seq_prefix(a, b, off, kb, &s_n);
+  if (nacc < 0) return;
+  const bool resid = nacc < kb;
+  const int64_t tr = off + (resid ? nacc : kb);
+  const int64_t dr = (int64_t)b * a.k_max + (resid ? nacc : 0);
+  const T* trow = reinterpret_cast<const T*>(a.target) + tr * a.tstride;
+  const T* drow = reinterpret_cast<const T*>(a.draft) + dr * a.dstride;
   const bool same_phase = ((reinterpret_cast<uintptr_t>(trow) ^ reinterpret_cast<uintptr_t>(drow)) & 15u) == 0;
-  const float mst = D.mst, msd = D.msd, rho0 = D.rho0;
+  const float mst = a.tstats[tr].max_logit * kLog2e;
+  const float msd = resid ? a.dstats[dr].max_logit * kLog2e : 0.f;
+  const float rho0 = resid ? (float)((double)a.tstats[tr].sum_exp / (double)a.dstats[dr].sum_exp) : 0.f;
   const Geom g = row_geom(trow, a.V);
   const int64_t nu = g.nvec + 2;
   // wave-level sums per slice (uniform values), one LDS round at the end
@@ -965,7 +933,7 @@ __global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, in
   for (int k = 0; k < kSubPerWG; ++k) {
     const int64_t u0 = (int64_t)(sl0 + k) * kSliceUnits;
     double sum[4] = {0.0, 0.0, 0.0, 0.0};
-    if (ok && sl0 + k < S && u0 < nu) {
+    if (sl0 + k < S && u0 < nu) {
       if (resid)
         parts_slice<T, true>(trow, drow, g, same_phase, u0, mst, msd, rho0, sum);
       else
@@ -987,18 +955,6 @@ __global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, in
     double r = sd[t * NW];
     for (int i = 1; i < NW; ++i) r += sd[t * NW + i];
     if (sl0 + k < S) reinterpret_cast<double*>(ws + (int64_t)b * S + sl0 + k)[t & 3] = r;
-  }
-  // the last of the sequence's SW workgroups takes the sample
-  __threadfence();
-  __syncthreads();
-  if (t == 0) s_last = atomicAdd(a.cnt_parts + b, 1) == SW - 1;
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  const int y = ok ? final_sample_seq<T>(a, D, S, ws + (int64_t)b * S, sd, si, s_sc) : -1;
-  if (t == 0) {
-    a.n_acc[b] = ok ? D.nacc : -1;
-    a.next_tok[b] = y;
   }
 }
 
@@ -1069,7 +1025,7 @@ template <typename T, bool RESID>
 __device__ int locate_units(const T* trow, const T* drow, const Geom& g, bool same_phase, int64_t ulo_all,
                             int64_t uhi_all, float mst, float msd, double rho, double base, double x, double* sd,
                             int* si, double* s_sc) {
-  constexpr int BD = kPartBD, VEC = Elem<T>::VEC;
+  constexpr int BD = kSampleBD, VEC = Elem<T>::VEC;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int64_t nu = uhi_all - ulo_all;
   const int64_t ulo = ulo_all + (int64_t)t * nu / BD, uhi = ulo_all + (int64_t)(t + 1) * nu / BD;
@@ -1130,18 +1086,36 @@ __device__ int locate_units(const T* trow, const T* drow, const Geom& g, bool sa
   return y;
 }
 
-// Exact inverse-CDF sample of sequence D (run by one workgroup of kPartBD threads
-// once every slice partial of the sequence is written).
 template <typename T>
-__device__ int final_sample_seq(const VerifyArgs& a, const SeqDesc& D, int S, const SlicePart* __restrict__ P,
-                                double* sd, int* si, double* s_sc) {
-  constexpr int BD = kPartBD;
+__global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S, const SlicePart* __restrict__ ws) {
+  constexpr int BD = kSampleBD;
+  __shared__ double sd[2 * (BD / 64)];
+  __shared__ int si[BD / 64];
+  __shared__ double s_sc[2];
+  __shared__ int s_n;
   const int t = threadIdx.x;
-  bool resid = D.nacc < D.kb;
-  const T* trow = reinterpret_cast<const T*>(a.target) + D.tr * a.tstride;
-  const T* drow = reinterpret_cast<const T*>(a.draft) + (resid ? D.dr : 0) * a.dstride;
+  const int b = blockIdx.x;
+  if (b >= a.B) return;
+  int64_t off;
+  int kb;
+  const int nacc = seq_prefix(a, b, off, kb, &s_n);
+  if (nacc < 0) {
+    if (t == 0) {
+      a.n_acc[b] = -1;
+      a.next_tok[b] = -1;
+    }
+    return;
+  }
+  bool resid = nacc < kb;
+  const int64_t tr = off + (resid ? nacc : kb);
+  const int64_t dr = (int64_t)b * a.k_max + (resid ? nacc : 0);
+  const T* trow = reinterpret_cast<const T*>(a.target) + tr * a.tstride;
+  const T* drow = reinterpret_cast<const T*>(a.draft) + dr * a.dstride;
   const bool same_phase = ((reinterpret_cast<uintptr_t>(trow) ^ reinterpret_cast<uintptr_t>(drow)) & 15u) == 0;
-  const float mst = D.mst, msd = D.msd, rho0 = D.rho0;
+  const float mst = a.tstats[tr].max_logit * kLog2e;
+  const float msd = resid ? a.dstats[dr].max_logit * kLog2e : 0.f;
+  const float rho0 = resid ? (float)((double)a.tstats[tr].sum_exp / (double)a.dstats[dr].sum_exp) : 0.f;
+  const SlicePart* P = ws + (int64_t)b * S;
   // fresh normalisers and the exact ratio
   double tot[2] = {0.0, 0.0};
   for (int s = t; s < S; s += BD) {
@@ -1158,7 +1132,7 @@ __device__ int final_sample_seq(const VerifyArgs& a, const SeqDesc& D, int S, co
     return m > 0.0 ? m : 0.0;
   };
   int y = -1;
-  const float u = D.u;
+  const float u = a.unif[off + kb];
   const Geom g = row_geom(trow, a.V);
   const int64_t nu = g.nvec + 2;
   for (int pass = 0; pass < 2 && y < 0; ++pass) {
@@ -1209,7 +1183,10 @@ __device__ int final_sample_seq(const VerifyArgs& a, const SeqDesc& D, int S, co
     }
     break;
   }
-  return y;
+  if (t == 0) {
+    a.n_acc[b] = nacc;
+    a.next_tok[b] = y;
+  }
 }
 
 // ----------------------------------------------------------------------------- host helpers
@@ -1227,12 +1204,6 @@ constexpr int kRowBD = 256;
 int verify_slices(int64_t vocab, int elem_bytes) {
   const int64_t units = vocab / (16 / elem_bytes) + 2;
   return (int)((units + kSliceUnits - 1) / kSliceUnits);
-}
-
-// Workspace layout: slice partials [B * S_ws], descriptors [B], then three int32
-// counters per sequence (rows finished, partial workgroups finished, first rejection).
-size_t ws_bytes(int B, int S_ws) {
-  return (size_t)B * ((size_t)S_ws * sizeof(SlicePart) + sizeof(SeqDesc) + 3 * sizeof(int32_t));
 }
 
 }  // namespace
@@ -1254,7 +1225,7 @@ int32_t cmsd_version(void) { return (1 << 16) | 1; }
 
 size_t cmsd_verify_workspace_bytes(int32_t batch, int64_t vocab) {
   if (batch <= 0 || vocab < 2 || vocab > INT32_MAX) return 0;
-  return ws_bytes(batch, verify_slices(vocab, 4));
+  return (size_t)batch * (size_t)verify_slices(vocab, 4) * sizeof(SlicePart);
 }
 
 cmsd_status cmsd_confidence(const void* logits, int32_t dtype, int64_t n_rows, int64_t vocab, int64_t row_stride,
@@ -1315,7 +1286,7 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
       !target_stats || !n_accepted || !next_token || !workspace)
     return CMSD_ERR_ARG;
   if (workspace_bytes < cmsd_verify_workspace_bytes(batch, vocab) || !aligned(workspace, 8)) return CMSD_ERR_ARG;
-  if ((int64_t)batch * ((verify_slices(vocab, 4) + kSubPerWG - 1) / kSubPerWG) > INT32_MAX) return CMSD_ERR_ARG;
+  if ((int64_t)batch * verify_slices(vocab, 4) > INT32_MAX) return CMSD_ERR_ARG;
   if (!aligned(draft_logits, es) || !aligned(target_logits, es) || !aligned(draft_stats, 4) ||
       !aligned(target_offsets, 4) || !aligned(draft_len, 4) || !aligned(drafted, 4) || !aligned(uniforms, 4) ||
       !aligned(target_stats, 4) || !aligned(n_accepted, 4) || !aligned(next_token, 4))
@@ -1343,21 +1314,17 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   a.next_tok = next_token;
   const hipStream_t st = as_stream(stream);
   const int S = verify_slices(vocab, (int)es);
-  const int S_ws = verify_slices(vocab, 4);
   const int SW = (S + kSubPerWG - 1) / kSubPerWG;
   SlicePart* ws = static_cast<SlicePart*>(workspace);
-  a.desc = reinterpret_cast<SeqDesc*>(ws + (size_t)batch * S_ws);
-  a.cnt_rows = reinterpret_cast<int32_t*>(a.desc + batch);
-  a.cnt_parts = a.cnt_rows + batch;
-  a.first_rej = a.cnt_parts + batch;
   const unsigned gp = (unsigned)((int64_t)batch * SW);
-  hipLaunchKernelGGL(k_verify_init, dim3((unsigned)((batch + 255) / 256)), dim3(256), 0, st, a);
   if (dtype == CMSD_F32) {
     hipLaunchKernelGGL((k_target_rows<float, kRowBD>), dim3((unsigned)target_rows), dim3(kRowBD), 0, st, a);
     hipLaunchKernelGGL((k_final_parts<float>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
+    hipLaunchKernelGGL((k_final_sample<float>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   } else {
     hipLaunchKernelGGL((k_target_rows<Bf16, kRowBD>), dim3((unsigned)target_rows), dim3(kRowBD), 0, st, a);
     hipLaunchKernelGGL((k_final_parts<Bf16>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
+    hipLaunchKernelGGL((k_final_sample<Bf16>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   }
   return launched();
 }

@@ -103,7 +103,6 @@ def test_verify_argument_errors(kw, want):
 def test_workspace_size():
     f = cm.lib().cmsd_verify_workspace_bytes
     assert f(0, 1000) == 0 and f(4, 1) == 0
-    # per sequence: one 32-byte record per slice of 1024 16-byte units (+ head and
-    # tail), a 48-byte descriptor and three int32 counters
-    assert f(256, 128256) == 256 * (32 * (((128256 // 4 + 2) + 1023) // 1024) + 48 + 12)
-    assert f(1, 2) == 32 + 48 + 12
+    # per sequence: one 32-byte record per slice of 1024 16-byte units (+ head and tail)
+    assert f(256, 128256) == 256 * 32 * (((128256 // 4 + 2) + 1023) // 1024)
+    assert f(1, 2) == 32
