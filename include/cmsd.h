@@ -163,7 +163,10 @@ cmsd_status cmsd_draft_len(const cmsd_row_stats* stats, int32_t batch, const cms
  *                   target_offsets[b] = b*(k_max+1) and draft_len[b] = k_max.
  *   target_rows     number of rows allocated in target_logits, uniforms and
  *                   target_stats (>= target_offsets[batch]).
- *   target_offsets  device, batch+1 int32 (as written by cmsd_draft_len).
+ *   target_offsets  device, batch+1 int32 (as written by cmsd_draft_len),
+ *                   non-decreasing; a sequence whose own offsets disagree with its
+ *                   draft length or target_rows is reported invalid, while
+ *                   non-monotone offsets give unspecified (in-bounds) results.
  *   draft_len       device, batch int32, each in [0, k_max].
  *   drafted         device, batch*k_max int32 token ids (entries i >= k_b unused).
  *   uniforms        device, target_rows floats in [0,1), packed like the target rows:
@@ -180,9 +183,12 @@ cmsd_status cmsd_draft_len(const cmsd_row_stats* stats, int32_t batch, const cms
  *                   out of range, drafted id outside [0, vocab)).
  *   next_token      device, batch int32 (output): the final token; -1 when invalid.
  *   workspace       device scratch of at least cmsd_verify_workspace_bytes(batch,
- *                   vocab) bytes, 8-byte aligned, owned by the caller; its contents
- *                   need no initialisation and are meaningless after the call.  Calls
- *                   that share a workspace must be ordered (same stream).
+ *                   k_max, vocab) bytes, 8-byte aligned, owned by the caller: the
+ *                   target-row results by (sequence, position) and the per-slice
+ *                   partial sums of the final-token sample.  Its contents need no
+ *                   initialisation and are meaningless after the call.  Calls that
+ *                   share a workspace must be ordered (same stream); overlapping
+ *                   calls race.
  *   workspace_bytes its size.
  * Errors: CMSD_ERR_ARG, CMSD_ERR_DTYPE, CMSD_ERR_LAUNCH.
  */
@@ -194,10 +200,11 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
                         int32_t* n_accepted, int32_t* next_token, void* workspace, size_t workspace_bytes,
                         void* stream);
 
-/* Workspace cmsd_verify needs for `batch` sequences over `vocab` (per-sequence,
- * per-vocabulary-slice partial sums of the final-token sample); 0 for batch <= 0
- * or an invalid vocab. */
-size_t cmsd_verify_workspace_bytes(int32_t batch, int64_t vocab);
+/* Workspace cmsd_verify needs for `batch` sequences of up to `k_max` drafts over
+ * `vocab`: per sequence, one 32-byte record per vocabulary slice (1024 16-byte
+ * vectors of a row) and one 16-byte record per target row position (k_max + 1);
+ * 0 for batch <= 0 or an invalid k_max / vocab. */
+size_t cmsd_verify_workspace_bytes(int32_t batch, int32_t k_max, int64_t vocab);
 
 /* Human-readable name of a status code (static string). */
 const char* cmsd_status_string(cmsd_status s);

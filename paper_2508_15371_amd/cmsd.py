@@ -56,7 +56,7 @@ def _load() -> C.CDLL:
     lib.cmsd_draft_len.restype = C.c_int
     lib.cmsd_verify.argtypes = [vp, i64, vp, vp, i64, i64, vp, vp, vp, vp, i32, i32, i32, i64,
                                 C.POINTER(VerifyParams), vp, vp, vp, vp, C.c_size_t, vp]
-    lib.cmsd_verify_workspace_bytes.argtypes = [i32, i64]
+    lib.cmsd_verify_workspace_bytes.argtypes = [i32, i32, i64]
     lib.cmsd_verify_workspace_bytes.restype = C.c_size_t
     lib.cmsd_verify.restype = C.c_int
     lib.cmsd_status_string.argtypes = [C.c_int]
@@ -141,14 +141,14 @@ def cmsd_draft_len(stats: torch.Tensor, batch: int, *, k_min: int, k_max: int, a
     return draft_len, target_offsets
 
 
-def cmsd_verify_workspace_bytes(batch: int, vocab: int) -> int:
+def cmsd_verify_workspace_bytes(batch: int, k_max: int, vocab: int) -> int:
     """Bytes of device workspace cmsd_verify needs."""
-    return int(_lib.cmsd_verify_workspace_bytes(int(batch), int(vocab)))
+    return int(_lib.cmsd_verify_workspace_bytes(int(batch), int(k_max), int(vocab)))
 
 
-def verify_workspace(batch: int, vocab: int, device) -> torch.Tensor:
+def verify_workspace(batch: int, k_max: int, vocab: int, device) -> torch.Tensor:
     """A device workspace tensor for cmsd_verify (allocate once, reuse across calls)."""
-    n = max(8, cmsd_verify_workspace_bytes(batch, vocab))
+    n = max(8, cmsd_verify_workspace_bytes(batch, k_max, vocab))
     return torch.empty((n + 7) // 8, dtype=torch.float64, device=device)
 
 
@@ -173,7 +173,7 @@ def cmsd_verify(draft_logits: torch.Tensor, draft_stats: torch.Tensor, target_lo
     if next_token is None:
         next_token = torch.empty(batch, dtype=torch.int32, device=dev)
     if workspace is None:
-        workspace = verify_workspace(batch, V, dev)
+        workspace = verify_workspace(batch, k_max, V, dev)
     for name, t, dt in (("target_offsets", target_offsets, torch.int32), ("draft_len", draft_len, torch.int32),
                         ("drafted", drafted, torch.int32), ("uniforms", uniforms, torch.float32)):
         if t.dtype != dt or not t.is_contiguous():

@@ -602,6 +602,16 @@ struct VerifyArgs {
   cmsd_target_stats* tstats;
   int32_t* n_acc;
   int32_t* next_tok;
+  struct RowSlot* slots;  // workspace: [B][k_max+1], by sequence and position
+};
+
+// Target-row results by (sequence, position), so the final-token pass reads a whole
+// sequence's rows in one round trip.  `r` tags the packed row that wrote the slot.
+struct RowSlot {
+  float m;
+  float A;
+  int32_t acc;
+  int32_t r;
 };
 
 struct TargetState {
@@ -686,19 +696,21 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
   const Geom g = row_geom(trow, a.V);
 
   // resolved by prep(), while the first rounds of the row load
-  bool valid = false, has_draft = false, count = false;
+  bool valid = false, layout = false, has_draft = false, count = false;
+  int b = 0, i = 0;
   float gz = -INFINITY, zd = -INFINITY, cm = 0.f, dm = 0.f, dA = 1.f;
   auto prep = [&] {
     // sequence owning row r: number of offsets[1..B] that are <= r
     int cnt = 0;
     for (int j = 1 + t; j <= a.B; j += BD) cnt += a.off[j] <= r ? 1 : 0;
-    int b = block_all_i<BD>(cnt, OpSumI(), si);
+    b = block_all_i<BD>(cnt, OpSumI(), si);
     b = b < a.B ? b : a.B - 1;
     const int64_t off_b = a.off[b], off_b1 = a.off[b + 1];
     const int kb = a.klen[b];
-    valid = kb >= 0 && kb <= a.k_max && off_b >= 0 && off_b <= r && r < off_b1 && off_b1 == off_b + kb + 1 &&
-            off_b1 <= a.target_rows;
-    const int i = int(r - off_b);
+    layout = kb >= 0 && kb <= a.k_max && off_b >= 0 && off_b <= r && r < off_b1 && off_b1 == off_b + kb + 1 &&
+             off_b1 <= a.target_rows;
+    valid = layout;
+    i = int(r - off_b);
     has_draft = valid && i < kb;
     if (has_draft) {
       const int64_t drow = (int64_t)b * a.k_max + i;
@@ -769,6 +781,7 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
       res.accept = (stoch || (a.mode == CMSD_MODE_CM && gate)) ? 1 : 0;
     }
     a.tstats[r] = res;
+    if (layout) a.slots[(int64_t)b * (a.k_max + 1) + i] = RowSlot{m, (float)A, res.accept, (int32_t)r};
   }
 }
 
@@ -788,7 +801,10 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
 // weights are exactly 0); slices are runs of kSliceUnits units.
 constexpr int kPartBD = 256;
 constexpr int kSliceUnits = 1024;
-constexpr int kSubPerWG = 4;
+#ifndef CMSD_SUB_PER_WG
+#define CMSD_SUB_PER_WG 1
+#endif
+constexpr int kSubPerWG = CMSD_SUB_PER_WG;  // slices per workgroup, all loaded before any is summed
 constexpr int kSampleBD = 256;
 
 struct SlicePart {
@@ -827,33 +843,81 @@ __device__ __forceinline__ uint4 unit_raw2(const T* row, const Geom& g, int64_t 
   return n > 0 ? E::raw_partial(row + unit_first<T>(g, u), n) : E::raw_ninf();
 }
 
-// Sequence bookkeeping shared by both kernels: layout check and the first rejected
-// position, by ballots over the accept flags (wave 0 computes, LDS broadcasts).
-// Returns -1 for an invalid sequence.
-__device__ int seq_prefix(const VerifyArgs& a, int b, int64_t& off, int& kb, int* s_out) {
+// What the final-token pass needs of sequence b: the layout check, the accepted
+// prefix (first rejection, by ballots over the accept flags), the row(s) of the
+// final sample and their normalisers.  Wave 0 reads the sequence's row slots and
+// drafter stats in one round trip (k_max < 64; longer drafts loop), the result is
+// broadcast through LDS.  nacc = -1 marks an invalid sequence.
+struct SeqInfo {
+  int64_t off, tr, dr;
+  int nacc, kb;
+  float mst, msd, rho0;
+};
+
+__device__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo* lds) {
   const int t = threadIdx.x, lane = t & 63;
-  off = a.off[b];
-  const int64_t off1 = a.off[b + 1];
-  kb = a.klen[b];
-  const bool ok = kb >= 0 && kb <= a.k_max && off >= 0 && off1 == off + kb + 1 && off1 <= a.target_rows;
   if (t < 64) {
-    int nacc = -1;
-    if (ok) {
-      nacc = kb;
-      bool bad = a.tstats[off + kb].accept != -1;
-      for (int base = 0; base < kb; base += 64) {
-        const int i = base + lane;
-        const int acc = i < kb ? a.tstats[off + i].accept : 1;
-        const unsigned long long rej = __ballot(acc == 0);
-        if (__ballot(acc != 0 && acc != 1) != 0ull) bad = true;
-        if (rej != 0ull && nacc == kb) nacc = base + __builtin_ctzll(rej);
+    const int K = a.k_max;
+    const int64_t off = a.off[b], off1 = a.off[b + 1];
+    const int kb = a.klen[b];
+    const RowSlot* S = a.slots + (int64_t)b * (K + 1);
+    const cmsd_row_stats* D = a.dstats + (int64_t)b * K;
+    SeqInfo q{};
+    q.nacc = -1;
+    const bool ok = kb >= 0 && kb <= K && off >= 0 && off1 == off + kb + 1 && off1 <= a.target_rows;
+    // slot j must be this call's row off + j with a consistent flag: 0/1 for drafted
+    // positions, -1 for the final row
+    auto bad_at = [&](int j, const RowSlot& sl) {
+      return j <= kb && (sl.r != (int32_t)(off + j) || (j < kb && sl.acc != 0 && sl.acc != 1) ||
+                         (j == kb && sl.acc != -1));
+    };
+    if (K < 64) {
+      const RowSlot sl = lane <= K ? S[lane] : RowSlot{0.f, 1.f, 1, 0};
+      const float dmx = lane < K ? D[lane].max_logit : 0.f;
+      const float dA = lane < K ? D[lane].sum_exp : 1.f;
+      if (ok && __ballot(bad_at(lane, sl)) == 0ull) {
+        const unsigned long long rej = __ballot(lane < kb && sl.acc == 0);
+        const int j = rej ? __builtin_ctzll(rej) : kb;  // slot of the final row: c, or k_b
+        q.nacc = j;
+        q.kb = kb;
+        q.off = off;
+        q.tr = off + j;
+        q.dr = (int64_t)b * K + (j < kb ? j : 0);
+        q.mst = rl_f(sl.m, j) * kLog2e;
+        if (j < kb) {
+          q.msd = rl_f(dmx, j) * kLog2e;
+          q.rho0 = (float)((double)rl_f(sl.A, j) / (double)rl_f(dA, j));
+        }
       }
-      if (bad) nacc = -1;
+    } else if (ok) {
+      bool bad = false;
+      int j = kb;
+      for (int base = 0; base <= kb; base += 64) {
+        const int jj = base + lane;
+        const RowSlot sl = jj <= kb ? S[jj] : RowSlot{0.f, 1.f, 1, 0};
+        if (__ballot(bad_at(jj, sl)) != 0ull) bad = true;
+        const unsigned long long rej = __ballot(jj < kb && sl.acc == 0);
+        if (rej != 0ull && j == kb) j = base + __builtin_ctzll(rej);
+      }
+      if (!bad) {
+        const RowSlot sl = S[j];
+        q.nacc = j;
+        q.kb = kb;
+        q.off = off;
+        q.tr = off + j;
+        q.dr = (int64_t)b * K + (j < kb ? j : 0);
+        q.mst = sl.m * kLog2e;
+        if (j < kb) {
+          const cmsd_row_stats ds = D[j];
+          q.msd = ds.max_logit * kLog2e;
+          q.rho0 = (float)((double)sl.A / (double)ds.sum_exp);
+        }
+      }
     }
-    if (lane == 0) *s_out = nacc;
+    if (lane == 0) *lds = q;
   }
   __syncthreads();
-  const int r = *s_out;
+  const SeqInfo r = *lds;
   __syncthreads();
   return r;
 }
@@ -881,26 +945,33 @@ __device__ __forceinline__ void part_unit(const uint4& rt, const uint4& rd, floa
   }
 }
 
+// The kSubPerWG slices of one workgroup: every unit load of every slice is issued
+// before any is summed, so the group costs one memory latency.
 template <typename T, bool RESID>
-__device__ __forceinline__ void parts_slice(const T* trow, const T* drow, const Geom& g, bool same_phase,
-                                            int64_t u0, float mst, float msd, float rho0, double (&sum)[4]) {
-  constexpr int BD = kPartBD, UPT = kSliceUnits / BD;
+__device__ __forceinline__ void parts_group(const T* trow, const T* drow, const Geom& g, bool same_phase,
+                                            int64_t u_first, float mst, float msd, float rho0,
+                                            double (&sum)[kSubPerWG][4]) {
+  constexpr int BD = kPartBD, UPT = kSliceUnits / BD, NU = kSubPerWG * UPT;
   const int t = threadIdx.x;
-  uint4 rt[UPT], rd[UPT];
+  uint4 rt[NU], rd[NU];
 #pragma unroll
-  for (int j = 0; j < UPT; ++j) {
-    const int64_t u = u0 + (int64_t)j * BD + t;
+  for (int j = 0; j < NU; ++j) {
+    const int64_t u = u_first + (int64_t)j * BD + t;
     rt[j] = unit_raw<T, true>(trow, g, u);
     if (RESID) rd[j] = unit_raw2<T, true>(drow, g, u, same_phase);
   }
 #pragma unroll
-  for (int j = 0; j < UPT; ++j) {
-    float at = 0.f, ad = 0.f, aq = 0.f, aqd = 0.f;
-    part_unit<T, RESID>(rt[j], rd[j], mst, msd, rho0, at, ad, aq, aqd);
-    sum[0] += (double)at;
-    sum[1] += (double)ad;
-    sum[2] += (double)aq;
-    sum[3] += (double)aqd;
+  for (int k = 0; k < kSubPerWG; ++k) {
+#pragma unroll
+    for (int jj = 0; jj < UPT; ++jj) {
+      const int j = k * UPT + jj;
+      float at = 0.f, ad = 0.f, aq = 0.f, aqd = 0.f;
+      part_unit<T, RESID>(rt[j], rd[j], mst, msd, rho0, at, ad, aq, aqd);
+      sum[k][0] += (double)at;
+      sum[k][1] += (double)ad;
+      sum[k][2] += (double)aq;
+      sum[k][3] += (double)aqd;
+    }
   }
 }
 
@@ -908,40 +979,33 @@ template <typename T>
 __global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, int SW, SlicePart* __restrict__ ws) {
   constexpr int BD = kPartBD;
   __shared__ double sd[kSubPerWG * 4 * (BD / 64)];
-  __shared__ int s_n;
+  __shared__ SeqInfo s_q;
   const int t = threadIdx.x;
   const int b = blockIdx.x / SW, sl0 = (blockIdx.x % SW) * kSubPerWG;
   if (b >= a.B) return;
-  int64_t off;
-  int kb;
-  const int nacc = seq_prefix(a, b, off, kb, &s_n);
-  if (nacc < 0) return;
-  const bool resid = nacc < kb;
-  const int64_t tr = off + (resid ? nacc : kb);
-  const int64_t dr = (int64_t)b * a.k_max + (resid ? nacc : 0);
-  const T* trow = reinterpret_cast<const T*>(a.target) + tr * a.tstride;
-  const T* drow = reinterpret_cast<const T*>(a.draft) + dr * a.dstride;
+  const SeqInfo q = seq_info(a, b, &s_q);
+  if (q.nacc < 0) return;
+  const bool resid = q.nacc < q.kb;
+  const T* trow = reinterpret_cast<const T*>(a.target) + q.tr * a.tstride;
+  const T* drow = reinterpret_cast<const T*>(a.draft) + q.dr * a.dstride;
   const bool same_phase = ((reinterpret_cast<uintptr_t>(trow) ^ reinterpret_cast<uintptr_t>(drow)) & 15u) == 0;
-  const float mst = a.tstats[tr].max_logit * kLog2e;
-  const float msd = resid ? a.dstats[dr].max_logit * kLog2e : 0.f;
-  const float rho0 = resid ? (float)((double)a.tstats[tr].sum_exp / (double)a.dstats[dr].sum_exp) : 0.f;
+  const float mst = q.mst, msd = q.msd, rho0 = q.rho0;
   const Geom g = row_geom(trow, a.V);
   const int64_t nu = g.nvec + 2;
   // wave-level sums per slice (uniform values), one LDS round at the end
+  double sum[kSubPerWG][4] = {};
+  const int64_t u_first = (int64_t)sl0 * kSliceUnits;
+  if (u_first < nu) {
+    if (resid)
+      parts_group<T, true>(trow, drow, g, same_phase, u_first, mst, msd, rho0, sum);
+    else
+      parts_group<T, false>(trow, trow, g, true, u_first, mst, 0.f, 0.f, sum);
+  }
   double ws_w[kSubPerWG][4];
 #pragma unroll
-  for (int k = 0; k < kSubPerWG; ++k) {
-    const int64_t u0 = (int64_t)(sl0 + k) * kSliceUnits;
-    double sum[4] = {0.0, 0.0, 0.0, 0.0};
-    if (sl0 + k < S && u0 < nu) {
-      if (resid)
-        parts_slice<T, true>(trow, drow, g, same_phase, u0, mst, msd, rho0, sum);
-      else
-        parts_slice<T, false>(trow, trow, g, true, u0, mst, 0.f, 0.f, sum);
-    }
+  for (int k = 0; k < kSubPerWG; ++k)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) ws_w[k][j] = wave_all_d(sum[j], OpSumD());
-  }
+    for (int j = 0; j < 4; ++j) ws_w[k][j] = wave_all_d(sum[k][j], OpSumD());
   constexpr int NW = BD / 64;
   if ((t & 63) == 0) {
 #pragma unroll
@@ -1092,29 +1156,25 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
   __shared__ double sd[2 * (BD / 64)];
   __shared__ int si[BD / 64];
   __shared__ double s_sc[2];
-  __shared__ int s_n;
+  __shared__ SeqInfo s_q;
   const int t = threadIdx.x;
   const int b = blockIdx.x;
   if (b >= a.B) return;
-  int64_t off;
-  int kb;
-  const int nacc = seq_prefix(a, b, off, kb, &s_n);
-  if (nacc < 0) {
+  const SeqInfo q = seq_info(a, b, &s_q);
+  if (q.nacc < 0) {
     if (t == 0) {
       a.n_acc[b] = -1;
       a.next_tok[b] = -1;
     }
     return;
   }
-  bool resid = nacc < kb;
-  const int64_t tr = off + (resid ? nacc : kb);
-  const int64_t dr = (int64_t)b * a.k_max + (resid ? nacc : 0);
-  const T* trow = reinterpret_cast<const T*>(a.target) + tr * a.tstride;
-  const T* drow = reinterpret_cast<const T*>(a.draft) + dr * a.dstride;
+  const int nacc = q.nacc;
+  bool resid = nacc < q.kb;
+  const T* trow = reinterpret_cast<const T*>(a.target) + q.tr * a.tstride;
+  const T* drow = reinterpret_cast<const T*>(a.draft) + q.dr * a.dstride;
   const bool same_phase = ((reinterpret_cast<uintptr_t>(trow) ^ reinterpret_cast<uintptr_t>(drow)) & 15u) == 0;
-  const float mst = a.tstats[tr].max_logit * kLog2e;
-  const float msd = resid ? a.dstats[dr].max_logit * kLog2e : 0.f;
-  const float rho0 = resid ? (float)((double)a.tstats[tr].sum_exp / (double)a.dstats[dr].sum_exp) : 0.f;
+  const float mst = q.mst, msd = q.msd, rho0 = q.rho0;
+  const float u = a.unif[q.off + q.kb];
   const SlicePart* P = ws + (int64_t)b * S;
   // fresh normalisers and the exact ratio
   double tot[2] = {0.0, 0.0};
@@ -1132,7 +1192,6 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
     return m > 0.0 ? m : 0.0;
   };
   int y = -1;
-  const float u = a.unif[off + kb];
   const Geom g = row_geom(trow, a.V);
   const int64_t nu = g.nvec + 2;
   for (int pass = 0; pass < 2 && y < 0; ++pass) {
@@ -1223,9 +1282,9 @@ const char* cmsd_status_string(cmsd_status s) {
 
 int32_t cmsd_version(void) { return (1 << 16) | 1; }
 
-size_t cmsd_verify_workspace_bytes(int32_t batch, int64_t vocab) {
-  if (batch <= 0 || vocab < 2 || vocab > INT32_MAX) return 0;
-  return (size_t)batch * (size_t)verify_slices(vocab, 4) * sizeof(SlicePart);
+size_t cmsd_verify_workspace_bytes(int32_t batch, int32_t k_max, int64_t vocab) {
+  if (batch <= 0 || k_max < 1 || k_max > 4096 || vocab < 2 || vocab > INT32_MAX) return 0;
+  return (size_t)batch * ((size_t)verify_slices(vocab, 4) * sizeof(SlicePart) + (size_t)(k_max + 1) * sizeof(RowSlot));
 }
 
 cmsd_status cmsd_confidence(const void* logits, int32_t dtype, int64_t n_rows, int64_t vocab, int64_t row_stride,
@@ -1285,7 +1344,7 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   if (!draft_logits || !draft_stats || !target_logits || !target_offsets || !draft_len || !drafted || !uniforms ||
       !target_stats || !n_accepted || !next_token || !workspace)
     return CMSD_ERR_ARG;
-  if (workspace_bytes < cmsd_verify_workspace_bytes(batch, vocab) || !aligned(workspace, 8)) return CMSD_ERR_ARG;
+  if (workspace_bytes < cmsd_verify_workspace_bytes(batch, k_max, vocab) || !aligned(workspace, 8)) return CMSD_ERR_ARG;
   if ((int64_t)batch * verify_slices(vocab, 4) > INT32_MAX) return CMSD_ERR_ARG;
   if (!aligned(draft_logits, es) || !aligned(target_logits, es) || !aligned(draft_stats, 4) ||
       !aligned(target_offsets, 4) || !aligned(draft_len, 4) || !aligned(drafted, 4) || !aligned(uniforms, 4) ||
@@ -1316,6 +1375,7 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   const int S = verify_slices(vocab, (int)es);
   const int SW = (S + kSubPerWG - 1) / kSubPerWG;
   SlicePart* ws = static_cast<SlicePart*>(workspace);
+  a.slots = reinterpret_cast<RowSlot*>(ws + (size_t)batch * verify_slices(vocab, 4));
   const unsigned gp = (unsigned)((int64_t)batch * SW);
   if (dtype == CMSD_F32) {
     hipLaunchKernelGGL((k_target_rows<float, kRowBD>), dim3((unsigned)target_rows), dim3(kRowBD), 0, st, a);

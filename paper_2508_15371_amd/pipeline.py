@@ -50,7 +50,7 @@ class LogitPass:
         self.tstats = torch.empty((self.target_rows, 4), dtype=torch.float32, device=dev)
         self.n_acc = torch.empty(B, dtype=torch.int32, device=dev)
         self.next_tok = torch.empty(B, dtype=torch.int32, device=dev)
-        self.ws = cmsd.verify_workspace(B, V, dev)
+        self.ws = cmsd.verify_workspace(B, k_max, V, dev)
 
     def confidence(self, draft: torch.Tensor, stream=None) -> None:
         cmsd.cmsd_confidence(draft, self.stats, lambdas=self.p.lambdas, beta_margin=self.p.beta_margin,

@@ -102,7 +102,8 @@ def test_verify_argument_errors(kw, want):
 
 def test_workspace_size():
     f = cm.lib().cmsd_verify_workspace_bytes
-    assert f(0, 1000) == 0 and f(4, 1) == 0
-    # per sequence: one 32-byte record per slice of 1024 16-byte units (+ head and tail)
-    assert f(256, 128256) == 256 * 32 * (((128256 // 4 + 2) + 1023) // 1024)
-    assert f(1, 2) == 32
+    assert f(0, 8, 1000) == 0 and f(4, 8, 1) == 0 and f(4, 0, 1000) == 0 and f(4, 5000, 1000) == 0
+    # per sequence: one 32-byte record per slice of 1024 16-byte units (+ head and
+    # tail) and one 16-byte record per target row position
+    assert f(256, 16, 128256) == 256 * (32 * (((128256 // 4 + 2) + 1023) // 1024) + 17 * 16)
+    assert f(1, 1, 2) == 32 + 2 * 16
