@@ -53,8 +53,10 @@ typedef enum {
 typedef enum { CMSD_F32 = 0, CMSD_BF16 = 1 } cmsd_dtype;
 
 typedef enum {
-  CMSD_MODE_STANDARD = 0, /* standard speculative sampling only            */
-  CMSD_MODE_CM = 1        /* plus the confidence-modulated gate (OR-ed)     */
+  CMSD_MODE_STANDARD = 0, /* standard speculative sampling only                    */
+  CMSD_MODE_CM = 1,       /* plus the confidence-modulated gate (OR-ed)            */
+  CMSD_MODE_GREEDY = 2    /* the paper's deterministic rule: the gate alone, and the
+                             target's top token after the accepted prefix          */
 } cmsd_mode;
 
 /* Weights of the unified confidence, Sec. III.B(1): C = lambda_ent*(1 - H/ln V)
@@ -98,13 +100,15 @@ typedef struct {
   uint32_t flags;     /* bit 0: the row contains -inf entries                     */
 } cmsd_row_stats;
 
-/* One record per packed target row (16 bytes), written by cmsd_verify. */
+/* One record per packed target row (32 bytes), written by cmsd_verify. */
 typedef struct {
   float max_logit;    /* max of the target row                                    */
   float sum_exp;      /* sum_v exp(z_v - max)                                     */
-  int32_t n_greater;  /* CM mode: min(#{v : z_v > z_drafted}, top_beta); 0 in STANDARD
-                         mode or with top_beta = 0; -1 on the final row             */
+  int32_t n_greater;  /* CM/GREEDY: min(#{v : z_v > z_drafted}, top_beta); 0 in
+                         STANDARD mode or with top_beta = 0; -1 on the final row   */
   int32_t accept;     /* 1 accepted, 0 rejected, -1 final row, -2 invalid input   */
+  int32_t top1;       /* GREEDY mode: lowest index of the row max; else -1        */
+  int32_t reserved[3];
 } cmsd_target_stats;
 
 /*
@@ -151,7 +155,10 @@ cmsd_status cmsd_draft_len(const cmsd_row_stats* stats, int32_t batch, const cms
  *
  * A position is accepted when u < p_t(y)/p_d(y) (standard speculative sampling)
  * or, in CMSD_MODE_CM, when the gate passes: #{v: z_t,v > z_t,y} < top_beta and
- * z_t^(1) - z_t,y <= tau_base + gamma*(1 - C).
+ * z_t^(1) - z_t,y <= tau_base + gamma*(1 - C).  In CMSD_MODE_GREEDY a position is
+ * accepted iff the gate passes and the final token is the target's top token
+ * (lowest index) at the first rejected position, or at position k_b; with
+ * top_beta = 1 and tau_base = gamma = 0 this is exact-match verification.
  *
  *   draft_logits    device, batch*k_max drafter rows (row b*k_max+i), stride
  *                   draft_stride >= vocab elements (the rows cmsd_confidence saw).
@@ -171,7 +178,7 @@ cmsd_status cmsd_draft_len(const cmsd_row_stats* stats, int32_t batch, const cms
  *   drafted         device, batch*k_max int32 token ids (entries i >= k_b unused).
  *   uniforms        device, target_rows floats in [0,1), packed like the target rows:
  *                   slot i < k_b is the accept test of position i, slot k_b the
- *                   final sample.
+ *                   final sample.  Unused (may be NULL) in CMSD_MODE_GREEDY.
  *   dtype           logit dtype of both logit arrays.
  *   batch >= 0, k_max in [1, 4096], vocab in [2, 2^31).
  *   params          host; see cmsd_verify_params.
@@ -202,7 +209,7 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
 
 /* Workspace cmsd_verify needs for `batch` sequences of up to `k_max` drafts over
  * `vocab`: per sequence, one 32-byte record per vocabulary slice (1024 16-byte
- * vectors of a row) and one 16-byte record per target row position (k_max + 1);
+ * vectors of a row) and one 32-byte record per target row position (k_max + 1);
  * 0 for batch <= 0 or an invalid k_max / vocab. */
 size_t cmsd_verify_workspace_bytes(int32_t batch, int32_t k_max, int64_t vocab);
 

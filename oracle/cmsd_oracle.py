@@ -35,12 +35,13 @@ import numpy as np
 
 MODE_STANDARD = 0
 MODE_CM = 1
+MODE_GREEDY = 2
 
 __all__ = [
-    "MODE_STANDARD", "MODE_CM", "RowStats", "decode_logits", "row_stats",
+    "MODE_STANDARD", "MODE_CM", "MODE_GREEDY", "RowStats", "decode_logits", "row_stats",
     "normalised_signals", "confidence", "draft_len", "log_softmax_at",
     "stochastic_accept", "top_beta_inclusion", "gap_gate", "accept_position",
-    "prefix_length", "residual_pmf", "inverse_cdf", "final_sample", "verify_sequence",
+    "prefix_length", "residual_pmf", "inverse_cdf", "final_sample", "greedy_next", "verify_sequence",
 ]
 
 
@@ -225,6 +226,9 @@ def accept_position(z_t: np.ndarray, rs_t: RowStats, z_d: np.ndarray, rs_d: RowS
       a position is accepted when the stochastic test passes OR the gate passes;
       in STANDARD mode only the stochastic test applies (standard speculative
       sampling).
+    * GREEDY mode is the paper's deterministic rule as printed: accepted iff the
+      gate passes (no uniform is consumed).  With beta = 1 and tau_t = 0 this is
+      exact-match verification against the target's top token, Sec. III.A.
 
     Returns a dict with acc, stoch, gate, n_greater_clamped (= min(#{v: z_v > z_y},
     beta)), and the slacks of the two inexact sub-decisions.
@@ -236,12 +240,16 @@ def accept_position(z_t: np.ndarray, rs_t: RowStats, z_d: np.ndarray, rs_d: RowS
     rank_ok = top_beta_inclusion(z_t, y, beta)
     gap_ok, gap, s_gap = gap_gate(z_t, y, rs_t, tau)
     gate = rank_ok and gap_ok
-    acc = stoch or (mode == MODE_CM and gate)
+    if mode == MODE_GREEDY:
+        acc = gate
+    else:
+        acc = stoch or (mode == MODE_CM and gate)
     n_greater = int(np.count_nonzero(z_t > z_t[y]))
     return {
         "acc": acc, "stoch": stoch, "gate": gate, "rank_ok": rank_ok, "gap_ok": gap_ok,
         "gap": gap, "tau": tau, "lp_t": lp_t, "lp_d": lp_d,
-        "slack_stoch": s_stoch, "slack_gap": s_gap if mode == MODE_CM and rank_ok else math.inf,
+        "slack_stoch": s_stoch if mode != MODE_GREEDY else math.inf,
+        "slack_gap": s_gap if mode in (MODE_CM, MODE_GREEDY) and rank_ok else math.inf,
         "n_greater_clamped": min(n_greater, max(beta, 0)),
     }
 
@@ -302,6 +310,14 @@ def final_sample(z_t_rows: list, rs_t_rows: list, z_d_rows: list, rs_d_rows: lis
     return inverse_cdf(q, u_final)
 
 
+def greedy_next(z_t_rows: list, k_b: int, n_acc: int) -> int:
+    """GREEDY mode's final token: the target's top token (lowest index among equal
+    maxima) at the first rejected position, or at position k_b when every draft
+    passed -- the verifier's own autoregressive choice ("reprocessed via AR
+    decoding", Sec. III.B(c); Sec. III.A step 2)."""
+    return int(np.argmax(z_t_rows[min(n_acc, k_b)]))
+
+
 def verify_sequence(z_t_rows: list, z_d_rows: list, drafted, uniforms, C, k_b: int, mode: int,
                     beta: int, tau_base: float, gamma: float, n_acc_override: int | None = None) -> dict:
     """Verify one sequence: positions 0..k_b-1 against target rows 0..k_b-1, then
@@ -321,6 +337,9 @@ def verify_sequence(z_t_rows: list, z_d_rows: list, drafted, uniforms, C, k_b: i
     flags = [p["acc"] for p in pos]
     n_acc = prefix_length(flags)
     c = n_acc if n_acc_override is None else n_acc_override
-    nxt, s_nxt = final_sample(z_t_rows, rs_t, z_d_rows, rs_d, k_b, c, float(uniforms[k_b]))
+    if mode == MODE_GREEDY:
+        nxt, s_nxt = greedy_next(z_t_rows, k_b, c), math.inf
+    else:
+        nxt, s_nxt = final_sample(z_t_rows, rs_t, z_d_rows, rs_d, k_b, c, float(uniforms[k_b]))
     return {"positions": pos, "flags": flags, "n_acc": n_acc, "next": nxt, "slack_next": s_nxt,
             "rs_t": rs_t, "rs_d": rs_d}

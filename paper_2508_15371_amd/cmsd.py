@@ -20,10 +20,10 @@ HEADER = os.path.join(os.path.dirname(_HERE), "include", "cmsd.h")
 
 CMSD_OK, CMSD_ERR_ARG, CMSD_ERR_DTYPE, CMSD_ERR_LAUNCH = 0, 1, 2, 3
 CMSD_F32, CMSD_BF16 = 0, 1
-CMSD_MODE_STANDARD, CMSD_MODE_CM = 0, 1
+CMSD_MODE_STANDARD, CMSD_MODE_CM, CMSD_MODE_GREEDY = 0, 1, 2
 
 STATS_FIELDS = ("max_logit", "sum_exp", "entropy", "margin_soft", "margin_logit", "conf", "top1", "flags")
-TSTATS_FIELDS = ("max_logit", "sum_exp", "n_greater", "accept")
+TSTATS_FIELDS = ("max_logit", "sum_exp", "n_greater", "accept", "top1", "reserved0", "reserved1", "reserved2")
 
 
 class ConfParams(C.Structure):
@@ -159,15 +159,15 @@ def cmsd_verify(draft_logits: torch.Tensor, draft_stats: torch.Tensor, target_lo
                 n_accepted: torch.Tensor | None = None, next_token: torch.Tensor | None = None,
                 workspace: torch.Tensor | None = None, stream=None) -> tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
     """Verification of every drafted position; returns (n_accepted [batch] int32,
-    next_token [batch] int32, target_stats float32 [target_rows, 4] with int32 bits in
-    columns 2 and 3)."""
+    next_token [batch] int32, target_stats float32 [target_rows, 8] with int32 bits in
+    columns 2..7).  ``uniforms`` may be None in GREEDY mode."""
     _, V, dst = _rows(draft_logits, "draft_logits")
     trows, V2, tst = _rows(target_logits, "target_logits")
     if V2 != V or target_logits.dtype != draft_logits.dtype:
         raise ValueError("draft and target logits must share vocab size and dtype")
     dev = target_logits.device
     if target_stats is None:
-        target_stats = torch.empty((trows, 4), dtype=torch.float32, device=dev)
+        target_stats = torch.empty((trows, 8), dtype=torch.float32, device=dev)
     if n_accepted is None:
         n_accepted = torch.empty(batch, dtype=torch.int32, device=dev)
     if next_token is None:
@@ -176,6 +176,8 @@ def cmsd_verify(draft_logits: torch.Tensor, draft_stats: torch.Tensor, target_lo
         workspace = verify_workspace(batch, k_max, V, dev)
     for name, t, dt in (("target_offsets", target_offsets, torch.int32), ("draft_len", draft_len, torch.int32),
                         ("drafted", drafted, torch.int32), ("uniforms", uniforms, torch.float32)):
+        if t is None and name == "uniforms":
+            continue
         if t.dtype != dt or not t.is_contiguous():
             raise ValueError(f"{name} must be a contiguous {dt} tensor")
     p = VerifyParams(int(mode), int(top_beta), float(tau_base), float(gamma))

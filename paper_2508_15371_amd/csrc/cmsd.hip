@@ -612,17 +612,21 @@ struct RowSlot {
   float A;
   int32_t acc;
   int32_t r;
+  int32_t top1;  // lowest index of the row max (GREEDY mode), else -1
+  int32_t pad[3];
 };
 
 struct TargetState {
   NormState n;
   float t1 = -INFINITY;
+  int gid = -1;  // first chunk (this thread's index order) attaining t1
 };
 
 template <int N, bool GUARD>
-__device__ __forceinline__ void target_chunk(TargetState& s, const float* f, uint32_t valid, bool count, float gz,
-                                             int beta, int& wcnt) {
+__device__ __forceinline__ void target_chunk(TargetState& s, const float* f, uint32_t valid, int cid, bool count,
+                                             float gz, int beta, int& wcnt) {
   const float cmax = chunk_max<N>(f);
+  s.gid = cmax > s.t1 ? cid : s.gid;
   s.t1 = fmaxf(s.t1, cmax);
   norm_chunk<N, GUARD, false>(s.n, f, valid, cmax);
   // wave-uniform: count only when the gate needs it, skip chunks where no lane holds
@@ -650,13 +654,13 @@ __device__ __forceinline__ void target_stream(const T* row, const Geom& g, const
       [&] {
         prep();
         float f[1] = {head};
-        target_chunk<1, true>(s, f, t < g.head ? 1u : 0u, count, gz, beta, wcnt);
+        target_chunk<1, true>(s, f, t < g.head ? 1u : 0u, 0, count, gz, beta, wcnt);
       },
-      [&](const uint4 (&raw)[U], int64_t) {
+      [&](const uint4 (&raw)[U], int64_t k) {
         float f[N];
 #pragma unroll
         for (int u = 0; u < U; ++u) E::unpack(raw[u], f + u * VEC);
-        target_chunk<N, false>(s, f, 0xffffffffu, count, gz, beta, wcnt);
+        target_chunk<N, false>(s, f, 0xffffffffu, int(k + 1), count, gz, beta, wcnt);
       });
   const int64_t rb = nr * per_round;
   if (rb < g.nvec) {
@@ -673,12 +677,12 @@ __device__ __forceinline__ void target_stream(const T* row, const Geom& g, const
         for (int e = 0; e < VEC; ++e) f[u * VEC + e] = -INFINITY;
       }
     }
-    target_chunk<N, true>(s, f, valid, count, gz, beta, wcnt);
+    target_chunk<N, true>(s, f, valid, int(nr + 1), count, gz, beta, wcnt);
   }
   {
     const int64_t tail0 = g.head + g.nvec * VEC;
     float f[1] = {t < g.tail ? E::load(row + tail0 + t) : -INFINITY};
-    target_chunk<1, true>(s, f, t < g.tail ? 1u : 0u, count, gz, beta, wcnt);
+    target_chunk<1, true>(s, f, t < g.tail ? 1u : 0u, int(nr + 2), count, gz, beta, wcnt);
   }
 }
 
@@ -727,7 +731,7 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
         dA = ds.sum_exp;
       }
     }
-    count = has_draft && a.mode == CMSD_MODE_CM && a.beta > 0;
+    count = has_draft && a.mode != CMSD_MODE_STANDARD && a.beta > 0;
   };
   TargetState s;
   int wcnt = 0;
@@ -736,6 +740,17 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
   const float m = block_all_f<BD>(s.t1, OpMax(), sf);
   const float ms_row = m * kLog2e;
   const float sc = fexp2(s.n.ms - ms_row);
+  int top1 = -1;
+  if (a.mode == CMSD_MODE_GREEDY) {
+    // lowest index of the row max: each thread holding it rescans its first such chunk
+    int64_t idx = INT64_MAX;
+    float other;
+    if (s.t1 == m) {
+      constexpr int U = Elem<T>::U;
+      rescan_chunk<T, BD>(trow, g, g.nvec / ((int64_t)U * BD), s.gid, m, idx, other);
+    }
+    top1 = block_all_i<BD>(idx == INT64_MAX ? INT32_MAX : int(idx), OpMinI(), si);
+  }
   double A;
   int ngt;
   {
@@ -755,11 +770,12 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
     }
   }
   if (t == 0) {
-    cmsd_target_stats res;
+    cmsd_target_stats res{};
     res.max_logit = m;
     res.sum_exp = (float)A;
+    res.top1 = top1;
     if (!valid) {
-      res = cmsd_target_stats{NAN, NAN, -1, -2};
+      res = cmsd_target_stats{NAN, NAN, -1, -2, -1, {0, 0, 0}};
     } else if (!has_draft) {
       res.n_greater = -1;
       res.accept = -1;
@@ -767,7 +783,7 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
       // standard speculative sampling: u < p_t(y) / p_d(y), in logs and fp64
       const double lpt = gz == -INFINITY ? -INFINITY : ((double)gz - (double)m) - log(A);
       const double lpd = zd == -INFINITY ? -INFINITY : ((double)zd - (double)dm) - log((double)dA);
-      const float u = a.unif[r];
+      const float u = a.mode == CMSD_MODE_GREEDY ? 0.f : a.unif[r];
       bool stoch;
       if (lpt == -INFINITY) stoch = false;
       else if (u == 0.f || lpd == -INFINITY) stoch = true;
@@ -778,10 +794,13 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
       const double tau = (double)a.tau_base + (double)a.gamma * (1.0 - (double)cm);
       const bool gate = count && ngt < a.beta && gap <= tau;
       res.n_greater = ng;
-      res.accept = (stoch || (a.mode == CMSD_MODE_CM && gate)) ? 1 : 0;
+      if (a.mode == CMSD_MODE_GREEDY)
+        res.accept = gate ? 1 : 0;  // the paper's deterministic rule
+      else
+        res.accept = (stoch || (a.mode == CMSD_MODE_CM && gate)) ? 1 : 0;
     }
     a.tstats[r] = res;
-    if (layout) a.slots[(int64_t)b * (a.k_max + 1) + i] = RowSlot{m, (float)A, res.accept, (int32_t)r};
+    if (layout) a.slots[(int64_t)b * (a.k_max + 1) + i] = RowSlot{m, (float)A, res.accept, (int32_t)r, top1, {0, 0, 0}};
   }
 }
 
@@ -852,6 +871,7 @@ struct SeqInfo {
   int64_t off, tr, dr;
   int nacc, kb;
   float mst, msd, rho0;
+  int top1;  // argmax of the final row (GREEDY mode)
 };
 
 __device__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo* lds) {
@@ -872,7 +892,7 @@ __device__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo* lds) {
                          (j == kb && sl.acc != -1));
     };
     if (K < 64) {
-      const RowSlot sl = lane <= K ? S[lane] : RowSlot{0.f, 1.f, 1, 0};
+      const RowSlot sl = lane <= K ? S[lane] : RowSlot{0.f, 1.f, 1, 0, -1, {0, 0, 0}};
       const float dmx = lane < K ? D[lane].max_logit : 0.f;
       const float dA = lane < K ? D[lane].sum_exp : 1.f;
       if (ok && __ballot(bad_at(lane, sl)) == 0ull) {
@@ -884,6 +904,7 @@ __device__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo* lds) {
         q.tr = off + j;
         q.dr = (int64_t)b * K + (j < kb ? j : 0);
         q.mst = rl_f(sl.m, j) * kLog2e;
+        q.top1 = __builtin_amdgcn_readlane(sl.top1, j);
         if (j < kb) {
           q.msd = rl_f(dmx, j) * kLog2e;
           q.rho0 = (float)((double)rl_f(sl.A, j) / (double)rl_f(dA, j));
@@ -894,7 +915,7 @@ __device__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo* lds) {
       int j = kb;
       for (int base = 0; base <= kb; base += 64) {
         const int jj = base + lane;
-        const RowSlot sl = jj <= kb ? S[jj] : RowSlot{0.f, 1.f, 1, 0};
+        const RowSlot sl = jj <= kb ? S[jj] : RowSlot{0.f, 1.f, 1, 0, -1, {0, 0, 0}};
         if (__ballot(bad_at(jj, sl)) != 0ull) bad = true;
         const unsigned long long rej = __ballot(jj < kb && sl.acc == 0);
         if (rej != 0ull && j == kb) j = base + __builtin_ctzll(rej);
@@ -907,6 +928,7 @@ __device__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo* lds) {
         q.tr = off + j;
         q.dr = (int64_t)b * K + (j < kb ? j : 0);
         q.mst = sl.m * kLog2e;
+        q.top1 = sl.top1;
         if (j < kb) {
           const cmsd_row_stats ds = D[j];
           q.msd = ds.max_logit * kLog2e;
@@ -1169,6 +1191,13 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
     return;
   }
   const int nacc = q.nacc;
+  if (a.mode == CMSD_MODE_GREEDY) {
+    if (t == 0) {
+      a.n_acc[b] = nacc;
+      a.next_tok[b] = q.top1;
+    }
+    return;
+  }
   bool resid = nacc < q.kb;
   const T* trow = reinterpret_cast<const T*>(a.target) + q.tr * a.tstride;
   const T* drow = reinterpret_cast<const T*>(a.draft) + q.dr * a.dstride;
@@ -1285,6 +1314,7 @@ int32_t cmsd_version(void) { return (1 << 16) | 1; }
 size_t cmsd_verify_workspace_bytes(int32_t batch, int32_t k_max, int64_t vocab) {
   if (batch <= 0 || k_max < 1 || k_max > 4096 || vocab < 2 || vocab > INT32_MAX) return 0;
   return (size_t)batch * ((size_t)verify_slices(vocab, 4) * sizeof(SlicePart) + (size_t)(k_max + 1) * sizeof(RowSlot));
+  static_assert(sizeof(RowSlot) == 32 && sizeof(SlicePart) == 32, "workspace record sizes");
 }
 
 cmsd_status cmsd_confidence(const void* logits, int32_t dtype, int64_t n_rows, int64_t vocab, int64_t row_stride,
@@ -1334,14 +1364,16 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   if (dtype != CMSD_F32 && dtype != CMSD_BF16) return CMSD_ERR_DTYPE;
   if (!params) return CMSD_ERR_ARG;
   if (batch < 0 || k_max < 1 || k_max > 4096 || vocab < 2 || vocab > INT32_MAX) return CMSD_ERR_ARG;
-  if (params->mode != CMSD_MODE_STANDARD && params->mode != CMSD_MODE_CM) return CMSD_ERR_ARG;
+  if (params->mode != CMSD_MODE_STANDARD && params->mode != CMSD_MODE_CM && params->mode != CMSD_MODE_GREEDY)
+    return CMSD_ERR_ARG;
   if (params->top_beta < 0 || !finite_f(params->tau_base) || !finite_f(params->gamma)) return CMSD_ERR_ARG;
   if (batch == 0) return CMSD_OK;
   if (target_rows < 1 || target_rows > INT32_MAX) return CMSD_ERR_ARG;
   if (draft_stride < vocab || target_stride < vocab) return CMSD_ERR_ARG;
   if ((int64_t)batch * k_max > INT32_MAX) return CMSD_ERR_ARG;
   const size_t es = dtype == CMSD_F32 ? 4 : 2;
-  if (!draft_logits || !draft_stats || !target_logits || !target_offsets || !draft_len || !drafted || !uniforms ||
+  if (!draft_logits || !draft_stats || !target_logits || !target_offsets || !draft_len || !drafted ||
+      (!uniforms && params->mode != CMSD_MODE_GREEDY) ||
       !target_stats || !n_accepted || !next_token || !workspace)
     return CMSD_ERR_ARG;
   if (workspace_bytes < cmsd_verify_workspace_bytes(batch, k_max, vocab) || !aligned(workspace, 8)) return CMSD_ERR_ARG;
@@ -1379,11 +1411,13 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   const unsigned gp = (unsigned)((int64_t)batch * SW);
   if (dtype == CMSD_F32) {
     hipLaunchKernelGGL((k_target_rows<float, kRowBD>), dim3((unsigned)target_rows), dim3(kRowBD), 0, st, a);
-    hipLaunchKernelGGL((k_final_parts<float>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
+    if (a.mode != CMSD_MODE_GREEDY)
+      hipLaunchKernelGGL((k_final_parts<float>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
     hipLaunchKernelGGL((k_final_sample<float>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   } else {
     hipLaunchKernelGGL((k_target_rows<Bf16, kRowBD>), dim3((unsigned)target_rows), dim3(kRowBD), 0, st, a);
-    hipLaunchKernelGGL((k_final_parts<Bf16>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
+    if (a.mode != CMSD_MODE_GREEDY)
+      hipLaunchKernelGGL((k_final_parts<Bf16>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
     hipLaunchKernelGGL((k_final_sample<Bf16>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   }
   return launched();

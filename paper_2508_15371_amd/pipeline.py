@@ -47,7 +47,7 @@ class LogitPass:
         self.off = torch.empty(B + 1, dtype=torch.int32, device=dev)
         self.k_dense = torch.full((B,), k_max, dtype=torch.int32, device=dev)
         self.off_dense = (torch.arange(B + 1, dtype=torch.int32, device=dev) * (k_max + 1)).contiguous()
-        self.tstats = torch.empty((self.target_rows, 4), dtype=torch.float32, device=dev)
+        self.tstats = torch.empty((self.target_rows, 8), dtype=torch.float32, device=dev)
         self.n_acc = torch.empty(B, dtype=torch.int32, device=dev)
         self.next_tok = torch.empty(B, dtype=torch.int32, device=dev)
         self.ws = cmsd.verify_workspace(B, k_max, V, dev)

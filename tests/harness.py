@@ -46,7 +46,7 @@ def tstats_np(ts: torch.Tensor) -> dict:
     s = ts.detach().cpu()
     f = s.numpy()
     i = s.view(torch.int32).numpy()
-    return {"m": f[:, 0], "A": f[:, 1], "ngt": i[:, 2], "acc": i[:, 3]}
+    return {"m": f[:, 0], "A": f[:, 1], "ngt": i[:, 2], "acc": i[:, 3], "top1": i[:, 4]}
 
 
 def close_rel(gpu: float, ref: float, rel: float = REL, floor: float = 1e-2) -> bool:
@@ -100,6 +100,8 @@ def acc_allowed(p: dict, mode: int) -> set:
     """acc values reachable by flipping sub-decisions whose slack is below SLACK."""
     stochs = {p["stoch"]} | ({not p["stoch"]} if p["slack_stoch"] < SLACK else set())
     gaps = {p["gap_ok"]} | ({not p["gap_ok"]} if p["slack_gap"] < SLACK else set())
+    if mode == O.MODE_GREEDY:
+        return {p["rank_ok"] and gg for gg in gaps}
     return {s or (mode == O.MODE_CM and p["rank_ok"] and gg) for s in stochs for gg in gaps}
 
 
@@ -115,6 +117,10 @@ def check_sequence(t: Tally, b: int, zt_rows, zd_rows, drafted, unif, C, kb: int
         t.value(f"tm[{b},{i}]", ts["m"][toff + i] == np.float32(rs.m), (ts["m"][toff + i], rs.m))
         t.value(f"tA[{b},{i}]", close_rel(float(ts["A"][toff + i]), rs.A, 1e-5, 0.0), (ts["A"][toff + i], rs.A))
     t.value(f"final-row[{b}]", int(ts["acc"][toff + kb]) == -1, int(ts["acc"][toff + kb]))
+    if mode == O.MODE_GREEDY:
+        for i in range(kb + 1):
+            want = int(np.argmax(zt_rows[i]))
+            t.value(f"top1[{b},{i}]", int(ts["top1"][toff + i]) == want, (int(ts["top1"][toff + i]), want))
     for i in range(kb):
         p = res["positions"][i]
         a = int(ts["acc"][toff + i])
@@ -127,7 +133,7 @@ def check_sequence(t: Tally, b: int, zt_rows, zd_rows, drafted, unif, C, kb: int
                 t.exceptions += 1
             else:
                 t.failures.append((f"acc[{b},{i}]", a, p))
-        if mode == O.MODE_CM and prm["top_beta"] > 0:
+        if mode in (O.MODE_CM, O.MODE_GREEDY) and prm["top_beta"] > 0:
             t.value(f"ngt[{b},{i}]", int(ts["ngt"][toff + i]) == p["n_greater_clamped"],
                     (int(ts["ngt"][toff + i]), p["n_greater_clamped"]))
     want = O.prefix_length(flags_gpu)

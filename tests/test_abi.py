@@ -75,7 +75,7 @@ def _verify(**kw):
 @pytest.mark.parametrize("kw,want", [
     (dict(dtype=9), cm.CMSD_ERR_DTYPE),
     (dict(p=None), cm.CMSD_ERR_ARG),
-    (dict(p=cm.VerifyParams(2, 3, 0.1, 1.0)), cm.CMSD_ERR_ARG),
+    (dict(p=cm.VerifyParams(3, 3, 0.1, 1.0)), cm.CMSD_ERR_ARG),
     (dict(p=cm.VerifyParams(1, -1, 0.1, 1.0)), cm.CMSD_ERR_ARG),
     (dict(p=cm.VerifyParams(1, 3, float("inf"), 1.0)), cm.CMSD_ERR_ARG),
     (dict(p=cm.VerifyParams(1, 3, 0.1, float("nan"))), cm.CMSD_ERR_ARG),
@@ -104,6 +104,6 @@ def test_workspace_size():
     f = cm.lib().cmsd_verify_workspace_bytes
     assert f(0, 8, 1000) == 0 and f(4, 8, 1) == 0 and f(4, 0, 1000) == 0 and f(4, 5000, 1000) == 0
     # per sequence: one 32-byte record per slice of 1024 16-byte units (+ head and
-    # tail) and one 16-byte record per target row position
-    assert f(256, 16, 128256) == 256 * (32 * (((128256 // 4 + 2) + 1023) // 1024) + 17 * 16)
-    assert f(1, 1, 2) == 32 + 2 * 16
+    # tail) and one 32-byte record per target row position
+    assert f(256, 16, 128256) == 256 * (32 * (((128256 // 4 + 2) + 1023) // 1024) + 17 * 32)
+    assert f(1, 1, 2) == 32 + 2 * 32

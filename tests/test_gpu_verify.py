@@ -94,7 +94,7 @@ def _verify_check(mods, name, mode, nseq):
     return t
 
 
-@pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM])
+@pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY])
 @pytest.mark.parametrize("name,nseq", [("tiny", 1), ("c2", 8), ("c3", 64), ("c4", 6), ("c5", 24)])
 def test_verify_configs(mods, name, nseq, mode):
     print(f"[verify parity] start {name} mode={mode}", flush=True)
@@ -142,7 +142,7 @@ def _run_small(mods, zd, zt, drafted, unif, k, dtype, B, K, V, mode=O.MODE_CM, t
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("V", [2, 5, 64, 1000, 4097, 32003])
-@pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM])
+@pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY])
 def test_ragged_lengths_small_vocab(mods, dtype, V, mode):
     # packed target rows with every draft length 0..K (k_b = 0: bonus sample only)
     g = np.random.default_rng(V + 31 * mode)
@@ -224,3 +224,33 @@ def test_draft_len_edges(mods):
         k_o, off_o, _ = O.draft_len(C.astype(np.float64).reshape(B, K), kmin, K, Hn.f32(alpha))
         assert np.array_equal(k.cpu().numpy(), k_o)
         assert np.array_equal(off.cpu().numpy(), off_o)
+
+
+def test_greedy_exact_match_on_device(mods):
+    # top_beta = 1, tau_base = gamma = 0: exact-match verification; drafts hit the
+    # target's top token at a seeded subset of positions; no uniforms are passed
+    cmsd, _ = mods
+    g = np.random.default_rng(21)
+    B, K, V = 16, 8, 5000
+    zd, zt, drafted, _ = _small_case(g, B, K, V, "bf16")
+    ztd = np.stack([Hn.decode(zt[r], "bf16") for r in range(B * (K + 1))])
+    for b in range(B):
+        for i in range(K):
+            if g.random() < 0.8:
+                drafted[b, i] = int(np.argmax(ztd[b * (K + 1) + i]))
+    dev = torch.device("cuda:0")
+    dd, td = Hn.to_device(zd, "bf16", dev), Hn.to_device(zt, "bf16", dev)
+    st = cmsd.cmsd_confidence(dd)
+    k = torch.full((B,), K, dtype=torch.int32, device=dev)
+    off = (torch.arange(B + 1, dtype=torch.int32, device=dev) * (K + 1)).contiguous()
+    n_acc, nxt, ts = cmsd.cmsd_verify(dd, st, td, off, k, torch.from_numpy(drafted.reshape(-1)).to(dev), None,
+                                      batch=B, k_max=K, mode=cmsd.CMSD_MODE_GREEDY, top_beta=1, tau_base=0.0,
+                                      gamma=0.0)
+    torch.cuda.synchronize()
+    n_acc, nxt = n_acc.cpu().numpy(), nxt.cpu().numpy()
+    for b in range(B):
+        c = 0
+        while c < K and ztd[b * (K + 1) + c][drafted[b, c]] == ztd[b * (K + 1) + c].max():
+            c += 1
+        assert n_acc[b] == c
+        assert nxt[b] == int(np.argmax(ztd[b * (K + 1) + c]))

@@ -254,3 +254,42 @@ def test_final_sample_uses_rejection_row_or_bonus_row():
     # equal rows at position 1 and an accepted position 0: bonus token from target row k = 2
     res = O.verify_sequence(zt, zd, [0, 3], [0.0, 0.0, 0.3], [0.5, 0.5], k, O.MODE_STANDARD, 3, 0.1, 1.0)
     assert res["n_acc"] == 2 and res["next"] == 5
+
+
+# ----------------------------------------------------------------------------- GREEDY mode
+@pytest.mark.parametrize("seed", range(12))
+def test_greedy_exact_match_reduction(seed):
+    # beta = 1, tau_t = 0: the accepted prefix is the longest run of drafts equal to
+    # the target's top token, and the next token is the target's top token right after
+    # (Sec. III.A step 2), written here as a direct scan
+    g = np.random.default_rng(300 + seed)
+    V, k = int(g.integers(2, 7)), int(g.integers(1, 6))
+    zt = [g.integers(-2, 3, V).astype(np.float64) for _ in range(k + 1)]
+    zd = _rows(g, V, k, 0.0)
+    ys = [int(v) for v in g.integers(0, V, k)]
+    for i in range(k):                      # make some drafts hit the top token
+        if g.random() < 0.6:
+            ys[i] = int(np.argmax(zt[i]))
+    res = O.verify_sequence(zt, zd, ys, [0.5] * (k + 1), [0.3] * k, k, O.MODE_GREEDY, 1, 0.0, 0.0)
+    c = 0
+    while c < k and zt[c][ys[c]] == zt[c].max():
+        c += 1
+    top = max(range(V), key=lambda v: (zt[c][v], -v))
+    assert res["n_acc"] == c
+    assert res["next"] == top
+
+
+def test_greedy_gate_monotone_in_beta_and_tau():
+    g = np.random.default_rng(11)
+    V, k = 30, 5
+    for _ in range(30):
+        zd = _rows(g, V, k, 0.0)
+        zt = _rows(g, V, k + 1, 0.0)
+        ys = [int(v) for v in g.integers(0, V, k)]
+        C = g.random(k).tolist()
+        prev = -1
+        for beta, tau in ((1, 0.0), (2, 0.5), (5, 1.0), (V, 100.0)):
+            n = O.verify_sequence(zt, zd, ys, [0.0] * (k + 1), C, k, O.MODE_GREEDY, beta, tau, 0.0)["n_acc"]
+            assert n >= prev
+            prev = n
+        assert prev == k                     # everything passes a gate of top-|V| and a huge tau
