@@ -2,7 +2,8 @@
  * cmsd.h - confidence-modulated speculative decoding: the vocabulary-wide logit
  * pass (arXiv 2508.15371, Sec. III.B), as a C ABI over gfx950 HIP kernels.
  *
- * Three calls, in the order one decoding iteration uses them:
+ * Three calls, in the order one decoding iteration uses them (plus
+ * cmsd_draft_sample, which draws sampled drafts from the drafter rows):
  *
  *   cmsd_confidence  per drafter row: softmax normaliser, entropy, top-1/top-2
  *                    margins and the unified confidence C     (Sec. III.B(1))
@@ -212,6 +213,30 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
  * vectors of a row) and one 32-byte record per target row position (k_max + 1);
  * 0 for batch <= 0 or an invalid k_max / vocab. */
 size_t cmsd_verify_workspace_bytes(int32_t batch, int32_t k_max, int64_t vocab);
+
+/*
+ * cmsd_draft_sample - one sample per row from the row's softmax: the smallest
+ * token y whose cumulative probability (vocabulary order) exceeds u (the
+ * inverse-CDF convention of cmsd_verify's final token).  This draws the drafted
+ * tokens that standard speculative sampling assumes (x ~ p_d); the paper's own
+ * drafter takes the argmax (stats.top1), Sec. III.A step 1.
+ *
+ *   logits, dtype, n_rows, vocab, row_stride   as for cmsd_confidence.
+ *   stats       device, n_rows records from cmsd_confidence on the same logits
+ *               (max_logit is the exponent reference).
+ *   uniforms    device, n_rows floats in [0,1), one per row.
+ *   drafted     device, n_rows int32 (output).
+ *   workspace   device scratch of cmsd_draft_sample_workspace_bytes(n_rows, vocab)
+ *               bytes, 8-byte aligned, no initialisation needed.
+ * Errors: CMSD_ERR_ARG, CMSD_ERR_DTYPE, CMSD_ERR_LAUNCH.
+ */
+cmsd_status cmsd_draft_sample(const void* logits, int32_t dtype, int64_t n_rows, int64_t vocab, int64_t row_stride,
+                              const cmsd_row_stats* stats, const float* uniforms, int32_t* drafted, void* workspace,
+                              size_t workspace_bytes, void* stream);
+
+/* Workspace cmsd_draft_sample needs: one 32-byte record per vocabulary slice
+ * (1024 16-byte vectors) per row; 0 for n_rows <= 0 or an invalid vocab. */
+size_t cmsd_draft_sample_workspace_bytes(int64_t n_rows, int64_t vocab);
 
 /* Human-readable name of a status code (static string). */
 const char* cmsd_status_string(cmsd_status s);

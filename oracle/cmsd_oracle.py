@@ -41,7 +41,7 @@ __all__ = [
     "MODE_STANDARD", "MODE_CM", "MODE_GREEDY", "RowStats", "decode_logits", "row_stats",
     "normalised_signals", "confidence", "draft_len", "log_softmax_at",
     "stochastic_accept", "top_beta_inclusion", "gap_gate", "accept_position",
-    "prefix_length", "residual_pmf", "inverse_cdf", "final_sample", "greedy_next", "verify_sequence",
+    "prefix_length", "residual_pmf", "inverse_cdf", "final_sample", "greedy_next", "draft_sample", "verify_sequence",
 ]
 
 
@@ -316,6 +316,14 @@ def greedy_next(z_t_rows: list, k_b: int, n_acc: int) -> int:
     passed -- the verifier's own autoregressive choice ("reprocessed via AR
     decoding", Sec. III.B(c); Sec. III.A step 2)."""
     return int(np.argmax(z_t_rows[min(n_acc, k_b)]))
+
+
+def draft_sample(z: np.ndarray, u: float) -> tuple[int, float]:
+    """A sampled draft: x ~ p_d = softmax(z), by the inverse CDF with u (the
+    convention of ``inverse_cdf``).  Speculative sampling's exactness assumes drafts
+    drawn this way; the paper's drafter itself takes the argmax (Sec. III.A step 1)."""
+    rs = row_stats(z)
+    return inverse_cdf(np.exp(np.asarray(z, dtype=np.float64) - rs.m) / rs.A, u)
 
 
 def verify_sequence(z_t_rows: list, z_d_rows: list, drafted, uniforms, C, k_b: int, mode: int,

@@ -59,6 +59,10 @@ def _load() -> C.CDLL:
     lib.cmsd_verify_workspace_bytes.argtypes = [i32, i32, i64]
     lib.cmsd_verify_workspace_bytes.restype = C.c_size_t
     lib.cmsd_verify.restype = C.c_int
+    lib.cmsd_draft_sample.argtypes = [vp, i32, i64, i64, i64, vp, vp, vp, vp, C.c_size_t, vp]
+    lib.cmsd_draft_sample.restype = C.c_int
+    lib.cmsd_draft_sample_workspace_bytes.argtypes = [i64, i64]
+    lib.cmsd_draft_sample_workspace_bytes.restype = C.c_size_t
     lib.cmsd_status_string.argtypes = [C.c_int]
     lib.cmsd_status_string.restype = C.c_char_p
     lib.cmsd_version.argtypes = []
@@ -187,3 +191,27 @@ def cmsd_verify(draft_logits: torch.Tensor, draft_stats: torch.Tensor, target_lo
         int(batch), int(k_max), V, C.byref(p), _ptr(target_stats), _ptr(n_accepted), _ptr(next_token),
         _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
     return n_accepted, next_token, target_stats
+
+
+def cmsd_draft_sample_workspace_bytes(n_rows: int, vocab: int) -> int:
+    return int(_lib.cmsd_draft_sample_workspace_bytes(int(n_rows), int(vocab)))
+
+
+def cmsd_draft_sample(logits: torch.Tensor, stats: torch.Tensor, uniforms: torch.Tensor,
+                      drafted: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                      stream=None) -> torch.Tensor:
+    """One softmax sample per row of ``logits`` [rows, V] with ``uniforms`` [rows]
+    (stats from cmsd_confidence on the same logits) -> int32 [rows]."""
+    n, V, st = _rows(logits, "logits")
+    dev = logits.device
+    if drafted is None:
+        drafted = torch.empty(n, dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = torch.empty(max(1, (cmsd_draft_sample_workspace_bytes(n, V) + 7) // 8), dtype=torch.float64,
+                                device=dev)
+    if uniforms.dtype != torch.float32 or not uniforms.is_contiguous():
+        raise ValueError("uniforms must be a contiguous float32 tensor")
+    _check("cmsd_draft_sample", _lib.cmsd_draft_sample(
+        _ptr(logits), _dtype_code(logits), n, V, st, _ptr(stats), _ptr(uniforms), _ptr(drafted), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+    return drafted

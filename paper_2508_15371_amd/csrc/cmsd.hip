@@ -1172,39 +1172,18 @@ __device__ int locate_units(const T* trow, const T* drow, const Geom& g, bool sa
   return y;
 }
 
+// Inverse-CDF sample over one row (RESID off) or the residual of a row pair, from
+// the row's vocabulary-slice partials P[0..S): rho = sum e_t / sum e_d (fresh sums),
+// slice masses corrected to first order in rho - rho0 and scanned in slice order,
+// then an exact scan/locate inside the chosen slice.  A zero residual falls back to
+// the target row.  Run by one workgroup of kSampleBD threads.
 template <typename T>
-__global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S, const SlicePart* __restrict__ ws) {
+__device__ int sample_from_parts(const T* trow, const T* drow, int64_t V, bool resid, float mst, float msd,
+                                 float rho0, float u, const SlicePart* __restrict__ P, int S, double* sd, int* si,
+                                 double* s_sc) {
   constexpr int BD = kSampleBD;
-  __shared__ double sd[2 * (BD / 64)];
-  __shared__ int si[BD / 64];
-  __shared__ double s_sc[2];
-  __shared__ SeqInfo s_q;
   const int t = threadIdx.x;
-  const int b = blockIdx.x;
-  if (b >= a.B) return;
-  const SeqInfo q = seq_info(a, b, &s_q);
-  if (q.nacc < 0) {
-    if (t == 0) {
-      a.n_acc[b] = -1;
-      a.next_tok[b] = -1;
-    }
-    return;
-  }
-  const int nacc = q.nacc;
-  if (a.mode == CMSD_MODE_GREEDY) {
-    if (t == 0) {
-      a.n_acc[b] = nacc;
-      a.next_tok[b] = q.top1;
-    }
-    return;
-  }
-  bool resid = nacc < q.kb;
-  const T* trow = reinterpret_cast<const T*>(a.target) + q.tr * a.tstride;
-  const T* drow = reinterpret_cast<const T*>(a.draft) + q.dr * a.dstride;
   const bool same_phase = ((reinterpret_cast<uintptr_t>(trow) ^ reinterpret_cast<uintptr_t>(drow)) & 15u) == 0;
-  const float mst = q.mst, msd = q.msd, rho0 = q.rho0;
-  const float u = a.unif[q.off + q.kb];
-  const SlicePart* P = ws + (int64_t)b * S;
   // fresh normalisers and the exact ratio
   double tot[2] = {0.0, 0.0};
   for (int s = t; s < S; s += BD) {
@@ -1221,7 +1200,7 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
     return m > 0.0 ? m : 0.0;
   };
   int y = -1;
-  const Geom g = row_geom(trow, a.V);
+  const Geom g = row_geom(trow, V);
   const int64_t nu = g.nvec + 2;
   for (int pass = 0; pass < 2 && y < 0; ++pass) {
     // per-thread contiguous run of slices
@@ -1271,10 +1250,97 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
     }
     break;
   }
+  return y;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S, const SlicePart* __restrict__ ws) {
+  constexpr int BD = kSampleBD;
+  __shared__ double sd[2 * (BD / 64)];
+  __shared__ int si[BD / 64];
+  __shared__ double s_sc[2];
+  __shared__ SeqInfo s_q;
+  const int t = threadIdx.x;
+  const int b = blockIdx.x;
+  if (b >= a.B) return;
+  const SeqInfo q = seq_info(a, b, &s_q);
+  if (q.nacc < 0) {
+    if (t == 0) {
+      a.n_acc[b] = -1;
+      a.next_tok[b] = -1;
+    }
+    return;
+  }
+  const int nacc = q.nacc;
+  if (a.mode == CMSD_MODE_GREEDY) {
+    if (t == 0) {
+      a.n_acc[b] = nacc;
+      a.next_tok[b] = q.top1;
+    }
+    return;
+  }
+  const bool resid = nacc < q.kb;
+  const T* trow = reinterpret_cast<const T*>(a.target) + q.tr * a.tstride;
+  const T* drow = reinterpret_cast<const T*>(a.draft) + q.dr * a.dstride;
+  const float u = a.unif[q.off + q.kb];
+  const int y = sample_from_parts<T>(trow, drow, a.V, resid, q.mst, q.msd, q.rho0, u, ws + (int64_t)b * S, S, sd,
+                                     si, s_sc);
   if (t == 0) {
     a.n_acc[b] = nacc;
     a.next_tok[b] = y;
   }
+}
+
+// ----------------------------------------------------------------------------- K5 draft sampling
+// One exact softmax sample per drafter row (the draws a sampled draft needs):
+// vocabulary-slice partials of e = 2^(z log2e - m log2e), then the same slice scan
+// and exact in-slice locate as the final token, with u one uniform per row.
+template <typename T>
+__global__ __launch_bounds__(kPartBD) void k_draft_parts(const T* __restrict__ logits, int64_t stride, int64_t V,
+                                                         const cmsd_row_stats* __restrict__ stats, int S, int SW,
+                                                         SlicePart* __restrict__ ws) {
+  constexpr int BD = kPartBD;
+  __shared__ double sd[kSubPerWG * 4 * (BD / 64)];
+  const int t = threadIdx.x;
+  const int64_t r = blockIdx.x / SW;
+  const int sl0 = (blockIdx.x % SW) * kSubPerWG;
+  const T* row = logits + r * stride;
+  const Geom g = row_geom(row, V);
+  const int64_t nu = g.nvec + 2;
+  const float mst = stats[r].max_logit * kLog2e;
+  double sum[kSubPerWG][4] = {};
+  const int64_t u_first = (int64_t)sl0 * kSliceUnits;
+  if (u_first < nu) parts_group<T, false>(row, row, g, true, u_first, mst, 0.f, 0.f, sum);
+  double w_[kSubPerWG];
+#pragma unroll
+  for (int k = 0; k < kSubPerWG; ++k) w_[k] = wave_all_d(sum[k][0], OpSumD());
+  constexpr int NW = BD / 64;
+  if ((t & 63) == 0) {
+#pragma unroll
+    for (int k = 0; k < kSubPerWG; ++k) sd[k * NW + (t >> 6)] = w_[k];
+  }
+  __syncthreads();
+  if (t < kSubPerWG && sl0 + t < S) {
+    double e = sd[t * NW];
+    for (int i = 1; i < NW; ++i) e += sd[t * NW + i];
+    ws[r * S + sl0 + t] = SlicePart{e, 0.0, 0.0, 0.0};
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kSampleBD) void k_draft_pick(const T* __restrict__ logits, int64_t stride, int64_t V,
+                                                          const cmsd_row_stats* __restrict__ stats,
+                                                          const float* __restrict__ unif, int S,
+                                                          const SlicePart* __restrict__ ws, int32_t* __restrict__ out) {
+  constexpr int BD = kSampleBD;
+  __shared__ double sd[2 * (BD / 64)];
+  __shared__ int si[BD / 64];
+  __shared__ double s_sc[2];
+  const int64_t r = blockIdx.x;
+  const T* row = logits + r * stride;
+  const int y = sample_from_parts<T>(row, row, V, false, stats[r].max_logit * kLog2e, 0.f, 0.f, unif[r], ws + r * S,
+                                     S, sd, si, s_sc);
+  if (threadIdx.x == 0) out[r] = y;
 }
 
 // ----------------------------------------------------------------------------- host helpers
@@ -1310,6 +1376,44 @@ const char* cmsd_status_string(cmsd_status s) {
 }
 
 int32_t cmsd_version(void) { return (1 << 16) | 1; }
+
+size_t cmsd_draft_sample_workspace_bytes(int64_t n_rows, int64_t vocab) {
+  if (n_rows <= 0 || n_rows > INT32_MAX || vocab < 2 || vocab > INT32_MAX) return 0;
+  return (size_t)n_rows * (size_t)verify_slices(vocab, 4) * sizeof(SlicePart);
+}
+
+cmsd_status cmsd_draft_sample(const void* logits, int32_t dtype, int64_t n_rows, int64_t vocab, int64_t row_stride,
+                              const cmsd_row_stats* stats, const float* uniforms, int32_t* drafted, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  if (dtype != CMSD_F32 && dtype != CMSD_BF16) return CMSD_ERR_DTYPE;
+  if (n_rows < 0 || n_rows > INT32_MAX || vocab < 2 || vocab > INT32_MAX || row_stride < vocab) return CMSD_ERR_ARG;
+  if (n_rows == 0) return CMSD_OK;
+  const size_t es = dtype == CMSD_F32 ? 4 : 2;
+  if (!logits || !stats || !uniforms || !drafted || !workspace) return CMSD_ERR_ARG;
+  if (!aligned(logits, es) || !aligned(stats, 4) || !aligned(uniforms, 4) || !aligned(drafted, 4) ||
+      !aligned(workspace, 8))
+    return CMSD_ERR_ARG;
+  if (workspace_bytes < cmsd_draft_sample_workspace_bytes(n_rows, vocab)) return CMSD_ERR_ARG;
+  if (row_stride > INT64_MAX / n_rows) return CMSD_ERR_ARG;
+  const int S = verify_slices(vocab, (int)es);
+  const int SW = (S + kSubPerWG - 1) / kSubPerWG;
+  if (n_rows * SW > INT32_MAX) return CMSD_ERR_ARG;
+  SlicePart* ws = static_cast<SlicePart*>(workspace);
+  const hipStream_t st = as_stream(stream);
+  const dim3 gp((unsigned)(n_rows * SW)), gr((unsigned)n_rows);
+  if (dtype == CMSD_F32) {
+    hipLaunchKernelGGL((k_draft_parts<float>), gp, dim3(kPartBD), 0, st, static_cast<const float*>(logits), row_stride,
+                       vocab, stats, S, SW, ws);
+    hipLaunchKernelGGL((k_draft_pick<float>), gr, dim3(kSampleBD), 0, st, static_cast<const float*>(logits),
+                       row_stride, vocab, stats, uniforms, S, ws, drafted);
+  } else {
+    hipLaunchKernelGGL((k_draft_parts<Bf16>), gp, dim3(kPartBD), 0, st, static_cast<const Bf16*>(logits), row_stride,
+                       vocab, stats, S, SW, ws);
+    hipLaunchKernelGGL((k_draft_pick<Bf16>), gr, dim3(kSampleBD), 0, st, static_cast<const Bf16*>(logits),
+                       row_stride, vocab, stats, uniforms, S, ws, drafted);
+  }
+  return launched();
+}
 
 size_t cmsd_verify_workspace_bytes(int32_t batch, int32_t k_max, int64_t vocab) {
   if (batch <= 0 || k_max < 1 || k_max > 4096 || vocab < 2 || vocab > INT32_MAX) return 0;

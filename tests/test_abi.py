@@ -13,7 +13,8 @@ P = 0x10000          # fake, aligned device addresses: never dereferenced on the
 def test_exports_every_declared_symbol():
     syms = cm.header_symbols()
     assert set(syms) >= {"cmsd_confidence", "cmsd_draft_len", "cmsd_verify", "cmsd_verify_workspace_bytes",
-                         "cmsd_status_string", "cmsd_version"}
+                         "cmsd_draft_sample", "cmsd_draft_sample_workspace_bytes", "cmsd_status_string",
+                         "cmsd_version"}
     lib = cm.lib()
     for s in syms:
         assert hasattr(lib, s), s
@@ -107,3 +108,22 @@ def test_workspace_size():
     # tail) and one 32-byte record per target row position
     assert f(256, 16, 128256) == 256 * (32 * (((128256 // 4 + 2) + 1023) // 1024) + 17 * 32)
     assert f(1, 1, 2) == 32 + 2 * 32
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(dtype=4), cm.CMSD_ERR_DTYPE),
+    (dict(V=1), cm.CMSD_ERR_ARG),
+    (dict(stride=10), cm.CMSD_ERR_ARG),
+    (dict(u=None), cm.CMSD_ERR_ARG),
+    (dict(ws=None), cm.CMSD_ERR_ARG),
+    (dict(wsb=8), cm.CMSD_ERR_ARG),
+    (dict(logits=P + 1), cm.CMSD_ERR_ARG),
+    (dict(n=0, logits=None, ws=None, wsb=0), cm.CMSD_OK),
+])
+def test_draft_sample_argument_errors(kw, want):
+    a = dict(logits=P, dtype=cm.CMSD_BF16, n=8, V=1000, stride=1000, st=P, u=P, out=P, ws=P, wsb=1 << 20)
+    a.update(kw)
+    assert cm.lib().cmsd_draft_sample(a["logits"], a["dtype"], a["n"], a["V"], a["stride"], a["st"], a["u"],
+                                      a["out"], a["ws"], a["wsb"], None) == want
+    f = cm.lib().cmsd_draft_sample_workspace_bytes
+    assert f(0, 100) == 0 and f(3, 1) == 0 and f(3, 4096) == 3 * 32 * ((4096 // 4 + 2 + 1023) // 1024)

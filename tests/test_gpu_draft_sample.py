@@ -1,0 +1,64 @@
+"""GPU parity of cmsd_draft_sample (one softmax sample per drafter row) against the
+oracle's inverse-CDF draw, through the C ABI."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import cmsd_oracle as O
+from tests import harness as Hn
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def cm():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2508_15371_amd import cmsd
+    return cmsd
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("V", [2, 7, 1000, 32000, 50257, 128259])
+def test_draft_sample_rows(cm, dtype, V):
+    g = np.random.default_rng(V + (7 if dtype == "bf16" else 0))
+    n = 24
+    z = np.stack([g.normal(0, float(g.uniform(0.2, 6)), V) for _ in range(n)]).astype(np.float32)
+    for r in range(0, n, 5):
+        m = g.random(V) < 0.3
+        m[int(np.argmax(z[r]))] = False
+        z[r][m] = -np.inf
+    stored = z if dtype == "f32" else W.bf16_bits_from_f32(z)
+    u = (g.integers(0, 1 << 24, n) * 2.0 ** -24).astype(np.float32)
+    u[0], u[1] = 0.0, np.float32(1.0 - 2.0 ** -24)
+    dev = torch.device("cuda:0")
+    x = Hn.to_device(stored, dtype, dev)
+    st = cm.cmsd_confidence(x)
+    y = cm.cmsd_draft_sample(x, st, torch.from_numpy(u).to(dev))
+    torch.cuda.synchronize()
+    y = y.cpu().numpy()
+    t = Hn.Tally()
+    for r in range(n):
+        want, slack = O.draft_sample(Hn.decode(stored[r], dtype), float(u[r]))
+        t.decision(f"y[{r}]", int(y[r]), want, slack)
+    t.assert_ok()
+
+
+def test_draft_sample_workload_rows(cm):
+    d = Hn.workload("c3", 0)
+    g = np.random.default_rng(3)
+    n = d["draft"].shape[0]
+    u = (g.integers(0, 1 << 24, n) * 2.0 ** -24).astype(np.float32)
+    dev = torch.device("cuda:0")
+    st = cm.cmsd_confidence(d["draft_dev"])
+    y = cm.cmsd_draft_sample(d["draft_dev"], st, torch.from_numpy(u).to(dev))
+    torch.cuda.synchronize()
+    y = y.cpu().numpy()
+    t = Hn.Tally()
+    for r in g.choice(n, 48, replace=False):
+        want, slack = O.draft_sample(Hn.decode(d["draft"][r], "bf16"), float(u[r]))
+        t.decision(f"y[{r}]", int(y[r]), want, slack)
+    t.assert_ok()

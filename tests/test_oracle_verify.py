@@ -293,3 +293,15 @@ def test_greedy_gate_monotone_in_beta_and_tau():
             assert n >= prev
             prev = n
         assert prev == k                     # everything passes a gate of top-|V| and a huge tau
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_draft_sample_exact_measure(seed):
+    # over the 2^24-point uniform lattice, token y is drawn with probability p_d(y)
+    g = np.random.default_rng(500 + seed)
+    V = int(g.integers(2, 9))
+    z = _rows(g, V, 1, 0.25)[0]
+    p = softmax(z)
+    starts = [first_true(lambda j, y=y: O.draft_sample(z, u_at(j))[0] >= y) for y in range(V)] + [N]
+    for y in range(V):
+        assert (starts[y + 1] - starts[y]) / N == pytest.approx(p[y], abs=2.0 / N)
