@@ -24,6 +24,27 @@ class Params:
     tau_base: float = 0.1
     gamma: float = 1.0
 
+    # The ablation settings of the paper's Table III, as parameter presets
+    # (everything else as given): a fixed draft length, a fixed threshold, both
+    # fixed, or a single confidence signal.
+    def fixed_k(self, k_max: int) -> "Params":
+        return Params(**{**self.__dict__, "k_min": k_max})
+
+    def fixed_tau(self) -> "Params":
+        return Params(**{**self.__dict__, "gamma": 0.0})
+
+    def fixed_k_and_tau(self, k_max: int) -> "Params":
+        return Params(**{**self.__dict__, "k_min": k_max, "gamma": 0.0})
+
+    def entropy_only(self) -> "Params":
+        return Params(**{**self.__dict__, "lambdas": (1.0, 0.0, 0.0)})
+
+    def margin_only(self) -> "Params":
+        return Params(**{**self.__dict__, "lambdas": (0.0, 1.0, 0.0)})
+
+    def softmax_only(self) -> "Params":
+        return Params(**{**self.__dict__, "lambdas": (0.0, 0.0, 1.0)})
+
 
 class LogitPass:
     """Buffers and calls for B sequences of k_max drafted positions over vocab V.

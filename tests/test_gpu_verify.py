@@ -254,3 +254,36 @@ def test_greedy_exact_match_on_device(mods):
             c += 1
         assert n_acc[b] == c
         assert nxt[b] == int(np.argmax(ztd[b * (K + 1) + c]))
+
+
+@pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY])
+@pytest.mark.parametrize("K", [63, 64, 70, 130])
+def test_long_drafts(mods, mode, K):
+    # draft lengths around and beyond one wavefront of positions (the prefix scan and
+    # the final pass read a sequence's positions 64 at a time)
+    g = np.random.default_rng(K * 3 + mode)
+    B, V = 4, 300
+    zd, zt_pad, drafted, unif_pad = _small_case(g, B, K, V, "f32", scale=0.4)
+    # targets equal to the drafts except a few positions, so prefixes run long
+    for b in range(B):
+        for i in range(K):
+            zt_pad[b * (K + 1) + i] = zd[b * K + i]
+    for b, i in ((0, 5), (1, 63), (1, K - 1), (2, min(64, K - 1))):
+        zt_pad[b * (K + 1) + i] = g.normal(0, 3, V).astype(np.float32)
+    unif_pad[:, :K] = np.float32(0.9)
+    k = np.array([K, K, min(64, K), K - 1], dtype=np.int32)
+    zt = W.pack_ragged(k, K, zt_pad.reshape(B, K + 1, V))
+    unif = W.pack_ragged(k, K, unif_pad.reshape(B, K + 1, 1)).reshape(-1)
+    off = np.concatenate([[0], np.cumsum(k + 1)]).astype(np.int32)
+    prm = dict(Hn.PARAMS, top_beta=1, tau_base=0.0, gamma=0.0) if mode == O.MODE_GREEDY else Hn.PARAMS
+    gs, n_acc, nxt, ts = _run_small(mods, zd, zt, drafted, unif, k, "f32", B, K, V, mode=mode,
+                                    top_beta=prm["top_beta"], tau_base=prm["tau_base"], gamma=prm["gamma"])
+    t = Hn.Tally()
+    for b in range(B):
+        kb = int(k[b])
+        zdr = [Hn.decode(zd[b * K + i], "f32") for i in range(K)]
+        ztr = [Hn.decode(zt[off[b] + i], "f32") for i in range(kb + 1)]
+        C = [Hn.oracle_conf(z, V) for z in zdr]
+        Hn.check_sequence(t, b, ztr, zdr, drafted[b], unif[off[b]:off[b] + kb + 1], C, kb, mode, prm, ts,
+                          int(off[b]), int(n_acc[b]), int(nxt[b]))
+    t.assert_ok()
