@@ -48,9 +48,12 @@ def _cpu_baseline_worker(args):
     zt = [O.decode_logits(z, cfg.dtype) for z in zt_s]
     lam = (1 / 3, 1 / 3, 1 / 3)
     C = np.array([[O.confidence(O.row_stats(z), V, lam, 1.0) for z in zd]])
-    O.draft_len(C, 1, K, 1.0)
-    O.verify_sequence(zt, zd, drafted, unif, C[0], K, mode, 3, float(np.float32(0.1)), 1.0)
-    return 2 * K + 1, time.perf_counter() - t0
+    k_b = int(O.draft_len(C, 1, K, 1.0)[0][0]) if cfg.ragged else K
+    # ragged: the verifier scored positions 0..k_b-1 and the final slot
+    zt_b = zt[:k_b] + [zt[K]]
+    u_b = np.concatenate([unif[:k_b], unif[K:]])
+    O.verify_sequence(zt_b, zd, drafted, u_b, C[0], k_b, mode, 3, float(np.float32(0.1)), 1.0)
+    return K + k_b + 1, time.perf_counter() - t0
 
 
 def cpu_baseline(name: str, seed: int, mode: int, budget_s: float = 20.0) -> dict:
@@ -76,8 +79,9 @@ def cpu_baseline(name: str, seed: int, mode: int, budget_s: float = 20.0) -> dic
         if len(idx):
             rate += sum(res[i][0] for i in idx) / sum(res[i][1] for i in idx)
     return {"value": rate, "unit": "rows/s", "cores": workers, "kind": "oracle",
-            "sample": f"{nseq} of {cfg.B} sequences of {name} (each {cfg.k_max} drafter + {cfg.k_max + 1} "
-                      f"target rows, V={cfg.V}), numpy fp64, {workers} processes"}
+            "sample": f"{nseq} of {cfg.B} sequences of {name} (each {cfg.k_max} drafter + "
+                      f"{'k_b+1' if cfg.ragged else cfg.k_max + 1} target rows, V={cfg.V}), numpy fp64, "
+                      f"{workers} processes"}
 
 
 def _traffic(workload: str):
@@ -96,7 +100,7 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="c4", choices=["c2", "c3", "c4"])
+    ap.add_argument("--workload", default="c4", choices=["c2", "c3", "c4", "c5"])
     ap.add_argument("--mode", default="cm", choices=["cm", "standard"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -137,14 +141,23 @@ def main() -> int:
     drafted = torch.from_numpy(d["drafted"].reshape(-1)).to(dev)
     unif = torch.from_numpy(d["uniforms"].reshape(-1)).to(dev)
     del d
-    lp = pipeline.LogitPass(cfg.B, cfg.k_max, cfg.V, dev, pipeline.Params(mode=mode), dense=True)
+    lp = pipeline.LogitPass(cfg.B, cfg.k_max, cfg.V, dev, pipeline.Params(mode=mode), dense=not cfg.ragged)
     stream = torch.cuda.current_stream(dev)
+    R_d, R_t = cfg.draft_rows, cfg.dense_target_rows
+    if cfg.ragged:
+        # the verifier scores k_b + 1 positions per sequence, packed by the device
+        # offsets: pack the target rows and uniforms once (untimed); every timed step
+        # recomputes the same draft lengths from the same drafter rows
+        lp.confidence(draft, stream)
+        lp.draft_len(stream)
+        target = W.pack_device(target, lp.k, lp.off, cfg.k_max)
+        unif = W.pack_device(unif, lp.k, lp.off, cfg.k_max)
+        R_t = int(lp.off[cfg.B].item())
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
         lp.run(draft, target, drafted, unif, stream)
     torch.cuda.synchronize()
 
-    R_d, R_t = cfg.draft_rows, cfg.dense_target_rows
     # timed region: K steps.  HIP events on the launch stream bracket the roofline
     # kernel (k_confidence) in every step; each event marker costs a few us of GPU
     # time, so no other call is bracketed here.
@@ -176,10 +189,11 @@ def main() -> int:
     t_ver = float(np.mean([e[1].elapsed_time(e[2]) for e in ev2])) * 1e-3
 
     n_acc = lp.n_acc.cpu().numpy()
-    rej = int((n_acc < cfg.k_max).sum())
+    k_used = lp.k.cpu().numpy() if cfg.ragged else np.full(cfg.B, cfg.k_max)
+    rej = int((n_acc < k_used).sum())
     s = cfg.elem_bytes
     conf_bytes = R_d * cfg.V * s + R_d * 32
-    verify_bytes = R_t * cfg.V * s + rej * cfg.V * s + R_t * 16 + cfg.B * cfg.k_max * 8
+    verify_bytes = R_t * cfg.V * s + rej * cfg.V * s + R_t * 32 + cfg.B * cfg.k_max * 8
     step_bytes = conf_bytes + cfg.B * cfg.k_max * 32 + verify_bytes
 
     result = {
@@ -195,7 +209,8 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: B={cfg.B} k_max={cfg.k_max} V={cfg.V} {cfg.dtype} dense, "
+        "config": {"workload": f"{cfg.name}: B={cfg.B} k_max={cfg.k_max} V={cfg.V} {cfg.dtype} "
+                               f"{'ragged' if cfg.ragged else 'dense'}, "
                                f"mode={args.mode}", "batch": cfg.B, "k_max": cfg.k_max, "vocab": cfg.V,
                    "drafter_rows": R_d, "target_rows": R_t},
         "gbps_algorithmic": step_bytes / (ms_step * 1e-3) / 1e9,

@@ -23,6 +23,7 @@
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 
 #include "cmsd.h"
 
@@ -874,7 +875,7 @@ struct SeqInfo {
   int top1;  // argmax of the final row (GREEDY mode)
 };
 
-__device__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo* lds) {
+__device__ __forceinline__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo* lds) {
   const int t = threadIdx.x, lane = t & 63;
   if (t < 64) {
     const int K = a.k_max;
@@ -1102,21 +1103,43 @@ __device__ __forceinline__ double block_excl_scan(double v, double* sd) {
   return pre + ex;
 }
 
-// Smallest element y in units [ulo_all, uhi_all) with q_y > 0 and base + C(y) > x,
-// C the cumulative weight from ulo_all in a fixed order (per-thread contiguous
-// spans, a block scan, sequential sums inside a span; the locate repeats exactly
-// those sums).  If none qualifies, the last element with q_y > 0.  Returns -1 if
-// every weight is 0.
+// Units of one slice per thread of the sampling workgroup.
+constexpr int kLocUPT = kSliceUnits / kSampleBD;
+static_assert(kLocUPT * kSampleBD == kSliceUnits, "a slice splits evenly over the sampling workgroup");
+
+// Smallest element y in units [ulo, uhi) with q_y > 0 and base + C(y) > x, C the
+// cumulative weight from ulo in a fixed order: thread t owns the kLocUPT units from
+// ulo + t*kLocUPT (kept in registers) and sums them unit by unit, a block scan
+// orders the threads, and the thread whose span crosses x repeats its own sums
+// exactly.  If none qualifies, the last element with q_y > 0.  Returns -1 if every
+// weight is 0.  The result passes through *s_y.
 template <typename T, bool RESID>
-__device__ int locate_units(const T* trow, const T* drow, const Geom& g, bool same_phase, int64_t ulo_all,
-                            int64_t uhi_all, float mst, float msd, double rho, double base, double x, double* sd,
-                            int* si, double* s_sc) {
-  constexpr int BD = kSampleBD, VEC = Elem<T>::VEC;
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int64_t nu = uhi_all - ulo_all;
-  const int64_t ulo = ulo_all + (int64_t)t * nu / BD, uhi = ulo_all + (int64_t)(t + 1) * nu / BD;
+__device__ __forceinline__ int locate_units(const T* trow, const T* drow, const Geom& g, bool same_phase, int64_t ulo, int64_t uhi,
+                            float mst, float msd, double rho, double base, double x, double* sd, int* si,
+                            int* s_y) {
+  using E = Elem<T>;
+  constexpr int BD = kSampleBD, VEC = E::VEC, UPT = kLocUPT;
+  const int t = threadIdx.x;
+  const int64_t u0 = ulo + (int64_t)t * UPT;
+  uint4 rt[UPT], rd[UPT];
+#pragma unroll
+  for (int j = 0; j < UPT; ++j) {
+    const bool in = u0 + j < uhi;
+    rt[j] = in ? unit_raw<T, false>(trow, g, u0 + j) : E::raw_ninf();
+    rd[j] = RESID && in ? unit_raw2<T, false>(drow, g, u0 + j, same_phase) : rt[j];
+  }
+  double us[UPT];
   double s = 0.0;
-  for (int64_t u = ulo; u < uhi; ++u) s += unit_sum<T, RESID>(trow, drow, g, same_phase, u, mst, msd, rho);
+#pragma unroll
+  for (int j = 0; j < UPT; ++j) {
+    double q[VEC];
+    unit_weights<T, RESID>(rt[j], rd[j], mst, msd, rho, q);
+    double v = 0.0;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) v += q[e];
+    us[j] = v;
+    s += v;
+  }
   const double excl = block_excl_scan<BD>(s, sd);
   const double end = base + (excl + s);
   int pick = block_all_i<BD>((s > 0.0 && end > x) ? t : INT32_MAX, OpMinI(), si);
@@ -1126,85 +1149,75 @@ __device__ int locate_units(const T* trow, const T* drow, const Geom& g, bool sa
     if (pick < 0) return -1;
     last = true;
   }
-  if (t == pick) s_sc[0] = excl;
-  __syncthreads();
-  int y = -1;
-  if (w == 0) {
-    const double ex = s_sc[0];
-    const int64_t lo = ulo_all + (int64_t)pick * nu / BD, hi = ulo_all + (int64_t)(pick + 1) * nu / BD;
+  if (t == pick) {
+    int y = -1;
     double P = 0.0;
-    int64_t uj = -1;
-    double Puj = 0.0;
-    for (int64_t ub = lo; ub < hi && (uj < 0 || last); ub += 64) {
-      const double v =
-          (ub + lane < hi) ? unit_sum<T, RESID>(trow, drow, g, same_phase, ub + lane, mst, msd, rho) : 0.0;
-      for (int l = 0; l < 64 && ub + l < hi; ++l) {
-        const double vl = rl_d(v, l);
-        const double Pn = P + vl;
-        if (vl > 0.0 && (last || base + (ex + Pn) > x)) {
-          uj = ub + l;
-          Puj = P;
-          if (!last) break;
+    bool done = false;
+#pragma unroll
+    for (int j = 0; j < UPT; ++j) {
+      const double Pn = P + us[j];
+      if (!done && us[j] > 0.0 && (last || base + (excl + Pn) > x)) {
+        double q[VEC];
+        unit_weights<T, RESID>(rt[j], rd[j], mst, msd, rho, q);
+        const int64_t first = unit_first<T>(g, u0 + j);
+        double Q = 0.0;
+        bool found = false;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          Q += q[e];
+          if (!found && q[e] > 0.0 && (last || base + (excl + (P + Q)) > x)) {
+            y = int(first + e);
+            found = !last;
+          }
         }
-        P = Pn;
+        done = !last;
       }
+      P = Pn;
     }
-    if (uj >= 0) {
-      const uint4 rt = unit_raw<T, false>(trow, g, uj);
-      const uint4 rd = RESID ? unit_raw2<T, false>(drow, g, uj, same_phase) : rt;
-      double q[VEC];
-      unit_weights<T, RESID>(rt, rd, mst, msd, rho, q);
-      const int64_t first = unit_first<T>(g, uj);
-      double Q = 0.0;
-      for (int e = 0; e < VEC; ++e) {
-        Q += q[e];
-        if (q[e] > 0.0 && (last || base + (ex + (Puj + Q)) > x)) {
-          y = int(first + e);
-          if (!last) break;
-        }
-      }
-    }
-    if (lane == 0) si[0] = y;
+    *s_y = y;
   }
   __syncthreads();
-  y = si[0];
+  const int y = *s_y;
   __syncthreads();
   return y;
 }
 
 // Inverse-CDF sample over one row (RESID off) or the residual of a row pair, from
 // the row's vocabulary-slice partials P[0..S): rho = sum e_t / sum e_d (fresh sums),
-// slice masses corrected to first order in rho - rho0 and scanned in slice order,
+// slice masses corrected to first order in rho - rho0 and scanned in slice order
+// (each thread a contiguous run of slices, its first partial kept in registers),
 // then an exact scan/locate inside the chosen slice.  A zero residual falls back to
-// the target row.  Run by one workgroup of kSampleBD threads.
+// the target row.  Run by one workgroup of kSampleBD threads; s_sc holds 3 doubles.
 template <typename T>
-__device__ int sample_from_parts(const T* trow, const T* drow, int64_t V, bool resid, float mst, float msd,
+__device__ __forceinline__ int sample_from_parts(const T* trow, const T* drow, int64_t V, bool resid, float mst, float msd,
                                  float rho0, float u, const SlicePart* __restrict__ P, int S, double* sd, int* si,
-                                 double* s_sc) {
+                                 double* s_sc, int* s_y) {
   constexpr int BD = kSampleBD;
   const int t = threadIdx.x;
   const bool same_phase = ((reinterpret_cast<uintptr_t>(trow) ^ reinterpret_cast<uintptr_t>(drow)) & 15u) == 0;
+  const int slo = (int)((int64_t)t * S / BD), shi = (int)((int64_t)(t + 1) * S / BD);
+  const SlicePart p0 = slo < shi ? P[slo] : SlicePart{0.0, 0.0, 0.0, 0.0};
   // fresh normalisers and the exact ratio
   double tot[2] = {0.0, 0.0};
-  for (int s = t; s < S; s += BD) {
-    tot[0] += P[s].et;
-    tot[1] += P[s].ed;
+  for (int s = slo; s < shi; ++s) {
+    const SlicePart p = s == slo ? p0 : P[s];
+    tot[0] += p.et;
+    tot[1] += p.ed;
   }
   block_sum_n<BD, 2>(tot, sd);
   const double rho = resid ? tot[0] / tot[1] : 0.0;
-  // slice masses (first-order correction of the rho0 sums), scanned in slice order;
-  // a zero residual falls back to the target row itself
+  // slice masses (first-order correction of the rho0 sums); a zero residual falls
+  // back to the target row itself
   auto mass = [&](int s, bool rs) -> double {
-    if (!rs) return P[s].et;
-    const double m = P[s].q - (rho - (double)rho0) * P[s].qd;
+    const SlicePart p = s == slo ? p0 : P[s];
+    if (!rs) return p.et;
+    const double m = p.q - (rho - (double)rho0) * p.qd;
     return m > 0.0 ? m : 0.0;
   };
   int y = -1;
   const Geom g = row_geom(trow, V);
   const int64_t nu = g.nvec + 2;
   for (int pass = 0; pass < 2 && y < 0; ++pass) {
-    // per-thread contiguous run of slices
-    const int slo = (int)((int64_t)t * S / BD), shi = (int)((int64_t)(t + 1) * S / BD);
     double sm = 0.0;
     for (int s = slo; s < shi; ++s) sm += mass(s, resid);
     const double excl = block_excl_scan<BD>(sm, sd);
@@ -1216,34 +1229,34 @@ __device__ int sample_from_parts(const T* trow, const T* drow, int64_t V, bool r
     }
     if (t == tlast) s_sc[1] = end;
     __syncthreads();
-    const double R = s_sc[1];
-    const double x = (double)u * R;
+    const double x = (double)u * s_sc[1];
     const int tp = block_all_i<BD>((sm > 0.0 && end > x) ? t : INT32_MAX, OpMinI(), si);
     const int tq = tp == INT32_MAX ? tlast : tp;
-    if (t == tq) s_sc[0] = excl;
-    __syncthreads();
-    // the slice inside thread tq's run, repeating its sequential sums exactly
-    const double ex = s_sc[0];
-    const int qlo = (int)((int64_t)tq * S / BD), qhi = (int)((int64_t)(tq + 1) * S / BD);
-    double Pacc = 0.0;
-    int sstar = -1;
-    double sbase = 0.0;
-    for (int s = qlo; s < qhi; ++s) {
-      const double m = mass(s, resid);
-      const double Pn = Pacc + m;
-      if (m > 0.0) {
-        sstar = s;
-        sbase = ex + Pacc;
-        if (tp != INT32_MAX && ex + Pn > x) break;
+    if (t == tq) {
+      // the slice inside this thread's run, repeating its sequential sums exactly
+      double Pacc = 0.0, sbase = 0.0;
+      int sstar = -1;
+      for (int s = slo; s < shi; ++s) {
+        const double m = mass(s, resid);
+        const double Pn = Pacc + m;
+        if (m > 0.0) {
+          sstar = s;
+          sbase = excl + Pacc;
+          if (tp != INT32_MAX && excl + Pn > x) break;
+        }
+        Pacc = Pn;
       }
-      Pacc = Pn;
+      s_sc[0] = sbase;
+      s_sc[2] = (double)sstar;
     }
-    const int64_t ulo = (int64_t)sstar * kSliceUnits;
+    __syncthreads();
+    const double sbase = s_sc[0];
+    const int64_t ulo = (int64_t)s_sc[2] * kSliceUnits;
     const int64_t uhi = ulo + kSliceUnits < nu ? ulo + kSliceUnits : nu;
     if (resid)
-      y = locate_units<T, true>(trow, drow, g, same_phase, ulo, uhi, mst, msd, rho, sbase, x, sd, si, s_sc);
+      y = locate_units<T, true>(trow, drow, g, same_phase, ulo, uhi, mst, msd, rho, sbase, x, sd, si, s_y);
     else
-      y = locate_units<T, false>(trow, trow, g, true, ulo, uhi, mst, mst, 0.0, sbase, x, sd, si, s_sc);
+      y = locate_units<T, false>(trow, trow, g, true, ulo, uhi, mst, mst, 0.0, sbase, x, sd, si, s_y);
     if (y < 0 && resid) {
       resid = false;
       continue;
@@ -1258,7 +1271,8 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
   constexpr int BD = kSampleBD;
   __shared__ double sd[2 * (BD / 64)];
   __shared__ int si[BD / 64];
-  __shared__ double s_sc[2];
+  __shared__ double s_sc[3];
+  __shared__ int s_y;
   __shared__ SeqInfo s_q;
   const int t = threadIdx.x;
   const int b = blockIdx.x;
@@ -1284,7 +1298,7 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
   const T* drow = reinterpret_cast<const T*>(a.draft) + q.dr * a.dstride;
   const float u = a.unif[q.off + q.kb];
   const int y = sample_from_parts<T>(trow, drow, a.V, resid, q.mst, q.msd, q.rho0, u, ws + (int64_t)b * S, S, sd,
-                                     si, s_sc);
+                                     si, s_sc, &s_y);
   if (t == 0) {
     a.n_acc[b] = nacc;
     a.next_tok[b] = y;
@@ -1335,11 +1349,12 @@ __global__ __launch_bounds__(kSampleBD) void k_draft_pick(const T* __restrict__ 
   constexpr int BD = kSampleBD;
   __shared__ double sd[2 * (BD / 64)];
   __shared__ int si[BD / 64];
-  __shared__ double s_sc[2];
+  __shared__ double s_sc[3];
+  __shared__ int s_y;
   const int64_t r = blockIdx.x;
   const T* row = logits + r * stride;
   const int y = sample_from_parts<T>(row, row, V, false, stats[r].max_logit * kLog2e, 0.f, 0.f, unif[r], ws + r * S,
-                                     S, sd, si, s_sc);
+                                     S, sd, si, s_sc, &s_y);
   if (threadIdx.x == 0) out[r] = y;
 }
 
@@ -1349,8 +1364,57 @@ bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) %
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 cmsd_status launched() { return hipGetLastError() == hipSuccess ? CMSD_OK : CMSD_ERR_LAUNCH; }
 
-constexpr int kConfBD = 256;
-constexpr int kRowBD = 256;
+// Workgroup size of the row kernels (one workgroup per logit row).  A row pays a
+// fixed cost (pipeline fill, epilogue reductions, the argmax rescan) besides its
+// streaming time, so short rows go to narrower groups, each streaming its row for
+// longer, as long as the launch still fills every SIMD with 4 waves; long rows and
+// short launches use 256 threads.  CMSD_ROW_BLOCK (64, 128 or 256) in the
+// environment overrides the choice.
+int device_cus() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+  if (dev < 64 && cache[dev] > 0) return cache[dev];
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+  if (dev < 64) cache[dev] = n;
+  return n;
+}
+int row_block(int64_t n_rows, int64_t row_bytes) {
+  if (const char* e = getenv("CMSD_ROW_BLOCK")) {
+    const int v = atoi(e);
+    if (v == 64 || v == 128 || v == 256) return v;
+  }
+  const int64_t waves = 16 * (int64_t)device_cus();  // 4 waves on each of 4 SIMDs per CU
+  if (row_bytes <= (int64_t)128 << 10) {
+    if (n_rows >= waves) return 64;
+    if (n_rows >= waves / 2) return 128;
+  }
+  return 256;
+}
+
+template <typename T>
+void launch_confidence(int bd, const T* logits, int64_t n_rows, int64_t V, int64_t stride, const ConfArgs& a,
+                       cmsd_row_stats* out, hipStream_t st) {
+  const dim3 grid((unsigned)n_rows);
+  if (bd == 64)
+    hipLaunchKernelGGL((k_confidence<T, 64>), grid, dim3(64), 0, st, logits, n_rows, V, stride, a, out);
+  else if (bd == 128)
+    hipLaunchKernelGGL((k_confidence<T, 128>), grid, dim3(128), 0, st, logits, n_rows, V, stride, a, out);
+  else
+    hipLaunchKernelGGL((k_confidence<T, 256>), grid, dim3(256), 0, st, logits, n_rows, V, stride, a, out);
+}
+
+template <typename T>
+void launch_target_rows(int bd, const VerifyArgs& a, hipStream_t st) {
+  const dim3 grid((unsigned)a.target_rows);
+  if (bd == 64)
+    hipLaunchKernelGGL((k_target_rows<T, 64>), grid, dim3(64), 0, st, a);
+  else if (bd == 128)
+    hipLaunchKernelGGL((k_target_rows<T, 128>), grid, dim3(128), 0, st, a);
+  else
+    hipLaunchKernelGGL((k_target_rows<T, 256>), grid, dim3(256), 0, st, a);
+}
 
 // Number of vocabulary slices of the final-token pass: units are 16-byte vectors
 // plus a head and a tail unit (the head shortens the vector run, so nvec + 2 is at
@@ -1435,13 +1499,11 @@ cmsd_status cmsd_confidence(const void* logits, int32_t dtype, int64_t n_rows, i
   if (!logits || !stats || !aligned(logits, es) || !aligned(stats, 4)) return CMSD_ERR_ARG;
   if (row_stride > INT64_MAX / n_rows) return CMSD_ERR_ARG;
   const ConfArgs a{l1, l2, l3, params->beta_margin, log((double)vocab)};
-  const dim3 grid((unsigned)n_rows), block(kConfBD);
+  const int bd = row_block(n_rows, vocab * (int64_t)es);
   if (dtype == CMSD_F32)
-    hipLaunchKernelGGL((k_confidence<float, kConfBD>), grid, block, 0, as_stream(stream),
-                       static_cast<const float*>(logits), n_rows, vocab, row_stride, a, stats);
+    launch_confidence(bd, static_cast<const float*>(logits), n_rows, vocab, row_stride, a, stats, as_stream(stream));
   else
-    hipLaunchKernelGGL((k_confidence<Bf16, kConfBD>), grid, block, 0, as_stream(stream),
-                       static_cast<const Bf16*>(logits), n_rows, vocab, row_stride, a, stats);
+    launch_confidence(bd, static_cast<const Bf16*>(logits), n_rows, vocab, row_stride, a, stats, as_stream(stream));
   return launched();
 }
 
@@ -1513,13 +1575,14 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   SlicePart* ws = static_cast<SlicePart*>(workspace);
   a.slots = reinterpret_cast<RowSlot*>(ws + (size_t)batch * verify_slices(vocab, 4));
   const unsigned gp = (unsigned)((int64_t)batch * SW);
+  const int bd = row_block(target_rows, vocab * (int64_t)es);
   if (dtype == CMSD_F32) {
-    hipLaunchKernelGGL((k_target_rows<float, kRowBD>), dim3((unsigned)target_rows), dim3(kRowBD), 0, st, a);
+    launch_target_rows<float>(bd, a, st);
     if (a.mode != CMSD_MODE_GREEDY)
       hipLaunchKernelGGL((k_final_parts<float>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
     hipLaunchKernelGGL((k_final_sample<float>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   } else {
-    hipLaunchKernelGGL((k_target_rows<Bf16, kRowBD>), dim3((unsigned)target_rows), dim3(kRowBD), 0, st, a);
+    launch_target_rows<Bf16>(bd, a, st);
     if (a.mode != CMSD_MODE_GREEDY)
       hipLaunchKernelGGL((k_final_parts<Bf16>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
     hipLaunchKernelGGL((k_final_sample<Bf16>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);

@@ -63,6 +63,25 @@ def test_invariant_rows(cm, dtype, V, pad):
     t.assert_ok()
 
 
+@pytest.mark.parametrize("block", [64, 128, 256])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("V", [9, 1025, 50257])
+def test_each_row_block(cm, monkeypatch, block, dtype, V):
+    # every workgroup size the library may pick for a launch (forced by CMSD_ROW_BLOCK)
+    monkeypatch.setenv("CMSD_ROW_BLOCK", str(block))
+    g = np.random.default_rng(V + block)
+    stored = _store(_invariant_rows(V, g), dtype)
+    tdev = Hn.to_device(stored, dtype, torch.device("cuda:0"))
+    st = cm.cmsd_confidence(tdev, lambdas=(0.2, 0.5, 0.3), beta_margin=0.7)
+    torch.cuda.synchronize()
+    gs = Hn.stats_np(st)
+    t = Hn.Tally()
+    lam32 = tuple(Hn.f32(x) for x in (0.2, 0.5, 0.3))
+    for r in range(stored.shape[0]):
+        Hn.check_row_stats(t, gs, r, Hn.decode(stored[r], dtype), V, lam32, Hn.f32(0.7))
+    t.assert_ok()
+
+
 def _sample_rows(cfg, k):
     n = cfg.draft_rows
     if n <= k:

@@ -164,6 +164,31 @@ def test_ragged_lengths_small_vocab(mods, dtype, V, mode):
     t.assert_ok()
 
 
+@pytest.mark.parametrize("block", [64, 128, 256])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY])
+def test_each_row_block(mods, monkeypatch, block, dtype, mode):
+    # every workgroup size the library may pick for the target-row pass
+    monkeypatch.setenv("CMSD_ROW_BLOCK", str(block))
+    g = np.random.default_rng(block + 7 * mode)
+    B, K, V = 5, 4, 9001
+    zd, zt_pad, drafted, unif_pad = _small_case(g, B, K, V, dtype)
+    k = np.array([4, 0, 2, 3, 1], dtype=np.int32)
+    zt = W.pack_ragged(k, K, zt_pad.reshape(B, K + 1, V))
+    unif = W.pack_ragged(k, K, unif_pad.reshape(B, K + 1, 1)).reshape(-1)
+    off = np.concatenate([[0], np.cumsum(k + 1)]).astype(np.int32)
+    gs, n_acc, nxt, ts = _run_small(mods, zd, zt, drafted, unif, k, dtype, B, K, V, mode=mode)
+    t = Hn.Tally()
+    for b in range(B):
+        kb = int(k[b])
+        zdr = [Hn.decode(zd[b * K + i], dtype) for i in range(K)]
+        ztr = [Hn.decode(zt[off[b] + i], dtype) for i in range(kb + 1)]
+        C = [Hn.oracle_conf(z, V) for z in zdr]
+        Hn.check_sequence(t, b, ztr, zdr, drafted[b], unif[off[b]:off[b] + kb + 1], C, kb, mode, Hn.PARAMS,
+                          ts, int(off[b]), int(n_acc[b]), int(nxt[b]))
+    t.assert_ok()
+
+
 def test_equal_rows_accept_everything_and_masked_targets(mods):
     g = np.random.default_rng(5)
     B, K, V = 4, 6, 3000
@@ -215,7 +240,9 @@ def test_draft_len_edges(mods):
     cmsd, _ = mods
     dev = torch.device("cuda:0")
     g = np.random.default_rng(8)
-    for B, K, kmin, alpha in ((0, 4, 1, 1.0), (1, 1, 1, 1.0), (3000, 16, 2, 0.61), (700, 7, 7, 0.3)):
+    # (1500, 40) and (5, 4096): sequences straddle the 16384-value staging chunks
+    for B, K, kmin, alpha in ((0, 4, 1, 1.0), (1, 1, 1, 1.0), (3000, 16, 2, 0.61), (700, 7, 7, 0.3),
+                              (1500, 40, 3, 0.9), (5, 4096, 1, 1.0)):
         C = g.uniform(0, 1, B * K).astype(np.float32)
         st = torch.zeros((B * K, 8), dtype=torch.float32)
         st[:, 5] = torch.from_numpy(C)
