@@ -209,7 +209,7 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
                         void* stream);
 
 /* Workspace cmsd_verify needs for `batch` sequences of up to `k_max` drafts over
- * `vocab`: per sequence, one 32-byte record per vocabulary slice (1024 16-byte
+ * `vocab`: per sequence, one 32-byte record per vocabulary slice (256 16-byte
  * vectors of a row) and one 32-byte record per target row position (k_max + 1);
  * 0 for batch <= 0 or an invalid k_max / vocab. */
 size_t cmsd_verify_workspace_bytes(int32_t batch, int32_t k_max, int64_t vocab);
@@ -235,7 +235,7 @@ cmsd_status cmsd_draft_sample(const void* logits, int32_t dtype, int64_t n_rows,
                               size_t workspace_bytes, void* stream);
 
 /* Workspace cmsd_draft_sample needs: one 32-byte record per vocabulary slice
- * (1024 16-byte vectors) per row; 0 for n_rows <= 0 or an invalid vocab. */
+ * (256 16-byte vectors) per row; 0 for n_rows <= 0 or an invalid vocab. */
 size_t cmsd_draft_sample_workspace_bytes(int64_t n_rows, int64_t vocab);
 
 /* Human-readable name of a status code (static string). */

@@ -809,7 +809,7 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
 // The final token of sequence b is an inverse-CDF sample over one target row (the
 // bonus row k_b when every draft passed) or over the residual max(0, p_t - p_d) of
 // the target and drafter rows at the first rejection c.  Two kernels:
-//   k_final_parts   B x ceil(S/4) workgroups, each covering 4 slices of the row
+//   k_final_parts   B x S one-wave workgroups, each covering one slice of the row
 //                   (pair): fp64 partials {sum e_t, sum e_d, sum q0, sum_{q0>0} e_d}
 //                   per slice, e = 2^(z log2e - m log2e), q0 = max(0, e_t - rho0 e_d)
 //                   with rho0 = A_t / A_d from the row passes.
@@ -818,9 +818,16 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
 //                   a scan over slices, then an exact scan/locate inside one slice.
 // A unit is the head (unit 0), one 16-byte vector (1..nvec) or the tail (nvec+1) of
 // the target row, always handled as one raw 16-byte vector padded with -inf (whose
-// weights are exactly 0); slices are runs of kSliceUnits units.
-constexpr int kPartBD = 256;
-constexpr int kSliceUnits = 1024;
+// weights are exactly 0); slices are runs of kSliceUnits units.  Small slices and
+// one-wave partial groups keep every stage of this latency-bound pass short.
+#ifndef CMSD_PART_BD
+#define CMSD_PART_BD 64
+#endif
+#ifndef CMSD_SLICE_UNITS
+#define CMSD_SLICE_UNITS 256
+#endif
+constexpr int kPartBD = CMSD_PART_BD;
+constexpr int kSliceUnits = CMSD_SLICE_UNITS;
 #ifndef CMSD_SUB_PER_WG
 #define CMSD_SUB_PER_WG 1
 #endif
@@ -850,14 +857,36 @@ __device__ __forceinline__ uint4 unit_raw(const T* row, const Geom& g, int64_t u
   const int n = unit_count<T>(g, u);
   return n > 0 ? E::raw_partial(row + unit_first<T>(g, u), n) : E::raw_ninf();
 }
+// 16 bytes starting `s` bytes into the 32 bytes lo:hi (s in [0, 16), a multiple of
+// the element size): whole-word shift by selects, then a byte funnel shift.
+__device__ __forceinline__ uint4 window16(const uint4& lo, const uint4& hi, int s) {
+  const bool w2 = (s & 8) != 0, w1 = (s & 4) != 0;
+  const uint32_t b0 = w2 ? lo.z : lo.x, b1 = w2 ? lo.w : lo.y, b2 = w2 ? hi.x : lo.z, b3 = w2 ? hi.y : lo.w,
+                 b4 = w2 ? hi.z : hi.x, b5 = w2 ? hi.w : hi.y;
+  const uint32_t c0 = w1 ? b1 : b0, c1 = w1 ? b2 : b1, c2 = w1 ? b3 : b2, c3 = w1 ? b4 : b3, c4 = w1 ? b5 : b4;
+  const uint32_t sh = (uint32_t)(s & 3);
+  return make_uint4(__builtin_amdgcn_alignbyte(c1, c0, sh), __builtin_amdgcn_alignbyte(c2, c1, sh),
+                    __builtin_amdgcn_alignbyte(c3, c2, sh), __builtin_amdgcn_alignbyte(c4, c3, sh));
+}
+
 // The same elements of a second row whose 16-byte phase may differ (`same_phase`
-// tells whether it matches): one vector load when aligned, element loads otherwise.
+// tells whether it matches): one vector load when aligned; otherwise the two
+// aligned vectors the 16 bytes straddle (both hold wanted elements), realigned.
 template <typename T, bool NT>
 __device__ __forceinline__ uint4 unit_raw2(const T* row, const Geom& g, int64_t u, bool same_phase) {
   using E = Elem<T>;
-  if (same_phase && u >= 1 && u <= g.nvec) {
-    const uint4* p = reinterpret_cast<const uint4*>(row + g.head) + (u - 1);
-    return NT ? ld_stream(p) : *p;
+  if (u >= 1 && u <= g.nvec) {
+    const T* p = row + g.head + (u - 1) * E::VEC;
+    if (same_phase) {
+      const uint4* q = reinterpret_cast<const uint4*>(p);
+      return NT ? ld_stream(q) : *q;
+    }
+    const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+    const int s = int(a & 15u);
+    const uint4* q = reinterpret_cast<const uint4*>(a - (uintptr_t)s);
+    const uint4 lo = NT ? ld_stream(q) : q[0];
+    const uint4 hi = NT ? ld_stream(q + 1) : q[1];
+    return window16(lo, hi, s);
   }
   const int n = unit_count<T>(g, u);
   return n > 0 ? E::raw_partial(row + unit_first<T>(g, u), n) : E::raw_ninf();
@@ -1066,20 +1095,6 @@ __device__ __forceinline__ void unit_weights(const uint4& rt, const uint4& rd, f
       q[e] = et;
     }
   }
-}
-
-template <typename T, bool RESID>
-__device__ __forceinline__ double unit_sum(const T* trow, const T* drow, const Geom& g, bool same_phase, int64_t u,
-                                           float mst, float msd, double rho) {
-  constexpr int VEC = Elem<T>::VEC;
-  const uint4 rt = unit_raw<T, false>(trow, g, u);
-  const uint4 rd = RESID ? unit_raw2<T, false>(drow, g, u, same_phase) : rt;
-  double q[VEC];
-  unit_weights<T, RESID>(rt, rd, mst, msd, rho, q);
-  double s = 0.0;
-#pragma unroll
-  for (int e = 0; e < VEC; ++e) s += q[e];
-  return s;
 }
 
 // Block exclusive scan of one double per thread (wave scan by shuffles, wave totals

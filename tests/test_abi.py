@@ -104,9 +104,9 @@ def test_verify_argument_errors(kw, want):
 def test_workspace_size():
     f = cm.lib().cmsd_verify_workspace_bytes
     assert f(0, 8, 1000) == 0 and f(4, 8, 1) == 0 and f(4, 0, 1000) == 0 and f(4, 5000, 1000) == 0
-    # per sequence: one 32-byte record per slice of 1024 16-byte units (+ head and
+    # per sequence: one 32-byte record per slice of 256 16-byte units (+ head and
     # tail) and one 32-byte record per target row position
-    assert f(256, 16, 128256) == 256 * (32 * (((128256 // 4 + 2) + 1023) // 1024) + 17 * 32)
+    assert f(256, 16, 128256) == 256 * (32 * (((128256 // 4 + 2) + 255) // 256) + 17 * 32)
     assert f(1, 1, 2) == 32 + 2 * 32
 
 
@@ -126,4 +126,4 @@ def test_draft_sample_argument_errors(kw, want):
     assert cm.lib().cmsd_draft_sample(a["logits"], a["dtype"], a["n"], a["V"], a["stride"], a["st"], a["u"],
                                       a["out"], a["ws"], a["wsb"], None) == want
     f = cm.lib().cmsd_draft_sample_workspace_bytes
-    assert f(0, 100) == 0 and f(3, 1) == 0 and f(3, 4096) == 3 * 32 * ((4096 // 4 + 2 + 1023) // 1024)
+    assert f(0, 100) == 0 and f(3, 1) == 0 and f(3, 4096) == 3 * 32 * ((4096 // 4 + 2 + 255) // 256)
