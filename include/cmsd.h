@@ -56,8 +56,8 @@ typedef enum { CMSD_F32 = 0, CMSD_BF16 = 1 } cmsd_dtype;
 typedef enum {
   CMSD_MODE_STANDARD = 0, /* standard speculative sampling only                    */
   CMSD_MODE_CM = 1,       /* plus the confidence-modulated gate (OR-ed)            */
-  CMSD_MODE_GREEDY = 2    /* the paper's deterministic rule: the gate alone, and the
-                             target's top token after the accepted prefix          */
+  CMSD_MODE_GREEDY = 2    /* the paper's deterministic rule: the target's top token
+                             or the gate; the top token after the accepted prefix  */
 } cmsd_mode;
 
 /* Weights of the unified confidence, Sec. III.B(1): C = lambda_ent*(1 - H/ln V)
@@ -157,9 +157,10 @@ cmsd_status cmsd_draft_len(const cmsd_row_stats* stats, int32_t batch, const cms
  * A position is accepted when u < p_t(y)/p_d(y) (standard speculative sampling)
  * or, in CMSD_MODE_CM, when the gate passes: #{v: z_t,v > z_t,y} < top_beta and
  * z_t^(1) - z_t,y <= tau_base + gamma*(1 - C).  In CMSD_MODE_GREEDY a position is
- * accepted iff the gate passes and the final token is the target's top token
- * (lowest index) at the first rejected position, or at position k_b; with
- * top_beta = 1 and tau_base = gamma = 0 this is exact-match verification.
+ * accepted iff the draft is the target's top token (lowest index among equal
+ * maxima) or the gate passes, and the final token is the target's top token at the
+ * first rejected position, or at position k_b; with top_beta = 0 (gate off) this is
+ * exact-match verification.
  *
  *   draft_logits    device, batch*k_max drafter rows (row b*k_max+i), stride
  *                   draft_stride >= vocab elements (the rows cmsd_confidence saw).

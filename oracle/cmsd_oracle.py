@@ -226,9 +226,10 @@ def accept_position(z_t: np.ndarray, rs_t: RowStats, z_d: np.ndarray, rs_d: RowS
       a position is accepted when the stochastic test passes OR the gate passes;
       in STANDARD mode only the stochastic test applies (standard speculative
       sampling).
-    * GREEDY mode is the paper's deterministic rule as printed: accepted iff the
-      gate passes (no uniform is consumed).  With beta = 1 and tau_t = 0 this is
-      exact-match verification against the target's top token, Sec. III.A.
+    * GREEDY mode is the paper's deterministic verification (Sec. III.A step 2)
+      with the gate as its relaxation: accepted iff the draft is the target's top
+      token (lowest index among equal maxima) OR the gate passes; no uniform is
+      consumed.  With beta = 0 (gate off) this is exact-match verification.
 
     Returns a dict with acc, stoch, gate, n_greater_clamped (= min(#{v: z_v > z_y},
     beta)), and the slacks of the two inexact sub-decisions.
@@ -240,13 +241,14 @@ def accept_position(z_t: np.ndarray, rs_t: RowStats, z_d: np.ndarray, rs_d: RowS
     rank_ok = top_beta_inclusion(z_t, y, beta)
     gap_ok, gap, s_gap = gap_gate(z_t, y, rs_t, tau)
     gate = rank_ok and gap_ok
+    exact = y == int(np.argmax(z_t))
     if mode == MODE_GREEDY:
-        acc = gate
+        acc = exact or gate
     else:
         acc = stoch or (mode == MODE_CM and gate)
     n_greater = int(np.count_nonzero(z_t > z_t[y]))
     return {
-        "acc": acc, "stoch": stoch, "gate": gate, "rank_ok": rank_ok, "gap_ok": gap_ok,
+        "acc": acc, "stoch": stoch, "gate": gate, "exact": exact, "rank_ok": rank_ok, "gap_ok": gap_ok,
         "gap": gap, "tau": tau, "lp_t": lp_t, "lp_d": lp_d,
         "slack_stoch": s_stoch if mode != MODE_GREEDY else math.inf,
         "slack_gap": s_gap if mode in (MODE_CM, MODE_GREEDY) and rank_ok else math.inf,

@@ -702,7 +702,7 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
 
   // resolved by prep(), while the first rounds of the row load
   bool valid = false, layout = false, has_draft = false, count = false;
-  int b = 0, i = 0;
+  int b = 0, i = 0, yd = -1;
   float gz = -INFINITY, zd = -INFINITY, cm = 0.f, dm = 0.f, dA = 1.f;
   auto prep = [&] {
     // sequence owning row r: number of offsets[1..B] that are <= r
@@ -720,6 +720,7 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
     if (has_draft) {
       const int64_t drow = (int64_t)b * a.k_max + i;
       const int y = a.drafted[drow];
+      yd = y;
       if (y < 0 || (int64_t)y >= a.V) {
         valid = false;
         has_draft = false;
@@ -796,7 +797,7 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
       const bool gate = count && ngt < a.beta && gap <= tau;
       res.n_greater = ng;
       if (a.mode == CMSD_MODE_GREEDY)
-        res.accept = gate ? 1 : 0;  // the paper's deterministic rule
+        res.accept = (yd == top1 || gate) ? 1 : 0;  // the paper's deterministic rule, relaxed by the gate
       else
         res.accept = (stoch || (a.mode == CMSD_MODE_CM && gate)) ? 1 : 0;
     }

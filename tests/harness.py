@@ -101,7 +101,7 @@ def acc_allowed(p: dict, mode: int) -> set:
     stochs = {p["stoch"]} | ({not p["stoch"]} if p["slack_stoch"] < SLACK else set())
     gaps = {p["gap_ok"]} | ({not p["gap_ok"]} if p["slack_gap"] < SLACK else set())
     if mode == O.MODE_GREEDY:
-        return {p["rank_ok"] and gg for gg in gaps}
+        return {p["exact"] or (p["rank_ok"] and gg) for gg in gaps}
     return {s or (mode == O.MODE_CM and p["rank_ok"] and gg) for s in stochs for gg in gaps}
 
 

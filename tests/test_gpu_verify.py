@@ -254,30 +254,39 @@ def test_draft_len_edges(mods):
 
 
 def test_greedy_exact_match_on_device(mods):
-    # top_beta = 1, tau_base = gamma = 0: exact-match verification; drafts hit the
-    # target's top token at a seeded subset of positions; no uniforms are passed
+    # top_beta = 0 (gate off): exact-match verification against the lowest index of
+    # the target max; drafts hit it at a seeded subset of positions, and some rows get
+    # a tied max at a higher index that the draft names (rejected); no uniforms
     cmsd, _ = mods
     g = np.random.default_rng(21)
     B, K, V = 16, 8, 5000
     zd, zt, drafted, _ = _small_case(g, B, K, V, "bf16")
-    ztd = np.stack([Hn.decode(zt[r], "bf16") for r in range(B * (K + 1))])
     for b in range(B):
         for i in range(K):
-            if g.random() < 0.8:
-                drafted[b, i] = int(np.argmax(ztd[b * (K + 1) + i]))
+            r = b * (K + 1) + i
+            z = Hn.decode(zt[r], "bf16")
+            top = int(np.argmax(z))
+            u = g.random()
+            if u < 0.7:
+                drafted[b, i] = top
+            elif u < 0.8 and top < V - 1:
+                hi = int(g.integers(top + 1, V))
+                zt[r, hi] = zt[r, top]          # tied max at a higher index
+                drafted[b, i] = hi
+    ztd = np.stack([Hn.decode(zt[r], "bf16") for r in range(B * (K + 1))])
     dev = torch.device("cuda:0")
     dd, td = Hn.to_device(zd, "bf16", dev), Hn.to_device(zt, "bf16", dev)
     st = cmsd.cmsd_confidence(dd)
     k = torch.full((B,), K, dtype=torch.int32, device=dev)
     off = (torch.arange(B + 1, dtype=torch.int32, device=dev) * (K + 1)).contiguous()
     n_acc, nxt, ts = cmsd.cmsd_verify(dd, st, td, off, k, torch.from_numpy(drafted.reshape(-1)).to(dev), None,
-                                      batch=B, k_max=K, mode=cmsd.CMSD_MODE_GREEDY, top_beta=1, tau_base=0.0,
-                                      gamma=0.0)
+                                      batch=B, k_max=K, mode=cmsd.CMSD_MODE_GREEDY, top_beta=0, tau_base=0.5,
+                                      gamma=1.0)
     torch.cuda.synchronize()
     n_acc, nxt = n_acc.cpu().numpy(), nxt.cpu().numpy()
     for b in range(B):
         c = 0
-        while c < K and ztd[b * (K + 1) + c][drafted[b, c]] == ztd[b * (K + 1) + c].max():
+        while c < K and drafted[b, c] == int(np.argmax(ztd[b * (K + 1) + c])):
             c += 1
         assert n_acc[b] == c
         assert nxt[b] == int(np.argmax(ztd[b * (K + 1) + c]))

@@ -279,6 +279,42 @@ def test_greedy_exact_match_reduction(seed):
     assert res["next"] == top
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_greedy_without_gate_is_exact_match(seed):
+    # beta = 0 turns the gate off: a draft passes only as the target's top token, the
+    # lowest index among equal maxima (tied maxima at higher indices are rejected),
+    # whatever tau; written here as a direct scan
+    g = np.random.default_rng(500 + seed)
+    V, k = int(g.integers(2, 7)), int(g.integers(1, 6))
+    zt = [g.integers(-2, 3, V).astype(np.float64) for _ in range(k + 1)]
+    zd = _rows(g, V, k, 0.0)
+    ys = [int(v) for v in g.integers(0, V, k)]
+    for i in range(k):
+        if g.random() < 0.6:
+            ys[i] = int(np.flatnonzero(zt[i] == zt[i].max())[-1])   # the last tied max
+        if g.random() < 0.5:
+            ys[i] = int(np.flatnonzero(zt[i] == zt[i].max())[0])
+    res = O.verify_sequence(zt, zd, ys, [0.5] * (k + 1), [0.3] * k, k, O.MODE_GREEDY, 0, 5.0, 1.0)
+    c = 0
+    while c < k and ys[c] == min(v for v in range(V) if zt[c][v] == zt[c].max()):
+        c += 1
+    assert res["n_acc"] == c
+    assert res["next"] == min(v for v in range(V) if zt[c][v] == zt[c].max())
+
+
+def test_greedy_accepts_every_exact_match():
+    # the target's top token passes for any gate setting, even a negative threshold
+    g = np.random.default_rng(12)
+    V, k = 40, 6
+    for _ in range(20):
+        zd = _rows(g, V, k, 0.0)
+        zt = _rows(g, V, k + 1, 0.0)
+        ys = [int(np.argmax(zt[i])) for i in range(k)]
+        for beta, tau, gamma in ((0, 0.0, 0.0), (1, -1.0, 0.0), (3, 0.1, -5.0), (V, 100.0, 1.0)):
+            assert O.verify_sequence(zt, zd, ys, [0.0] * (k + 1), [0.5] * k, k, O.MODE_GREEDY, beta, tau,
+                                     gamma)["n_acc"] == k
+
+
 def test_greedy_gate_monotone_in_beta_and_tau():
     g = np.random.default_rng(11)
     V, k = 30, 5
