@@ -131,6 +131,19 @@ cmsd_status cmsd_confidence(const void* logits, int32_t dtype, int64_t n_rows, i
                             cmsd_row_stats* stats, void* stream);
 
 /*
+ * cmsd_confidence_var - cmsd_confidence plus, per row, the population variance of
+ * the row's finite logits: the logit-variance proxy for drafter uncertainty that
+ * Sec. I names beside entropy and the top-1/top-2 margin.  The paper gives it no
+ * normalisation, so it is reported and does not enter C.  Same arguments and
+ * errors as cmsd_confidence, plus:
+ *   logit_var   device, n_rows floats (output): sum_v (z_v - mean)^2 / n over the n
+ *               finite logits of the row (0 with a single finite logit).
+ */
+cmsd_status cmsd_confidence_var(const void* logits, int32_t dtype, int64_t n_rows, int64_t vocab,
+                                int64_t row_stride, const cmsd_conf_params* params,
+                                cmsd_row_stats* stats, float* logit_var, void* stream);
+
+/*
  * cmsd_draft_len - adaptive draft length per sequence (Sec. III.B(b)).
  *
  *   stats           device, batch*k_max records from cmsd_confidence (row b*k_max+i).

@@ -38,7 +38,7 @@ MODE_CM = 1
 MODE_GREEDY = 2
 
 __all__ = [
-    "MODE_STANDARD", "MODE_CM", "MODE_GREEDY", "RowStats", "decode_logits", "row_stats",
+    "MODE_STANDARD", "MODE_CM", "MODE_GREEDY", "RowStats", "decode_logits", "row_stats", "logit_variance",
     "normalised_signals", "confidence", "draft_len", "log_softmax_at",
     "stochastic_accept", "top_beta_inclusion", "gap_gate", "accept_position",
     "prefix_length", "residual_pmf", "inverse_cdf", "final_sample", "greedy_next", "draft_sample", "verify_sequence",
@@ -97,6 +97,18 @@ def row_stats(z: np.ndarray) -> RowStats:
     p1_minus_p2 = float(p[top1]) - p2
     margin_logit = m - z2 if z2 > -math.inf else math.inf
     return RowStats(m, A, H, top1, z2, p1_minus_p2, margin_logit)
+
+
+def logit_variance(z: np.ndarray) -> float:
+    """Population variance of the finite logits of a row: the logit-variance proxy
+    for drafter uncertainty that Sec. I names beside entropy and the top-1/top-2
+    margin.  The paper gives it no normalisation, so it is reported, not combined
+    into C.  Two-pass definition in fp64: the mean first, then the mean squared
+    deviation; -inf entries are left out, one finite entry gives 0."""
+    z = np.asarray(z, dtype=np.float64)
+    f = z[np.isfinite(z)]
+    mu = float(f.sum()) / f.size
+    return float(((f - mu) ** 2).sum()) / f.size
 
 
 def normalised_signals(rs: RowStats, V: int, beta_m: float) -> tuple[float, float, float]:

@@ -52,6 +52,8 @@ def _load() -> C.CDLL:
     vp, i32, i64 = C.c_void_p, C.c_int32, C.c_int64
     lib.cmsd_confidence.argtypes = [vp, i32, i64, i64, i64, C.POINTER(ConfParams), vp, vp]
     lib.cmsd_confidence.restype = C.c_int
+    lib.cmsd_confidence_var.argtypes = [vp, i32, i64, i64, i64, C.POINTER(ConfParams), vp, vp, vp]
+    lib.cmsd_confidence_var.restype = C.c_int
     lib.cmsd_draft_len.argtypes = [vp, i32, C.POINTER(DraftParams), vp, vp, vp]
     lib.cmsd_draft_len.restype = C.c_int
     lib.cmsd_verify.argtypes = [vp, i64, vp, vp, i64, i64, vp, vp, vp, vp, i32, i32, i32, i64,
@@ -127,6 +129,22 @@ def cmsd_confidence(logits: torch.Tensor, stats: torch.Tensor | None = None, *,
     _check("cmsd_confidence", _lib.cmsd_confidence(_ptr(logits), _dtype_code(logits), n, V, st, C.byref(p),
                                                    _ptr(stats), _stream(stream)))
     return stats
+
+
+def cmsd_confidence_var(logits: torch.Tensor, stats: torch.Tensor | None = None, logit_var: torch.Tensor | None = None,
+                        *, lambdas=(1 / 3, 1 / 3, 1 / 3), beta_margin: float = 1.0,
+                        stream=None) -> tuple[torch.Tensor, torch.Tensor]:
+    """cmsd_confidence plus the variance of each row's finite logits -> (stats
+    float32 [rows, 8], logit_var float32 [rows])."""
+    n, V, st = _rows(logits, "logits")
+    if stats is None:
+        stats = torch.empty((n, 8), dtype=torch.float32, device=logits.device)
+    if logit_var is None:
+        logit_var = torch.empty(n, dtype=torch.float32, device=logits.device)
+    p = ConfParams(float(lambdas[0]), float(lambdas[1]), float(lambdas[2]), float(beta_margin))
+    _check("cmsd_confidence_var", _lib.cmsd_confidence_var(_ptr(logits), _dtype_code(logits), n, V, st, C.byref(p),
+                                                           _ptr(stats), _ptr(logit_var), _stream(stream)))
+    return stats, logit_var
 
 
 def cmsd_draft_len(stats: torch.Tensor, batch: int, *, k_min: int, k_max: int, alpha: float,

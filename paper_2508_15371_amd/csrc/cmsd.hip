@@ -313,25 +313,55 @@ __device__ __forceinline__ float chunk_max(const float* f) {
 
 // Drafter-row state: normaliser plus the top-2 of chunk maxima and the first chunk
 // (in this thread's index order) that attains the thread's maximum.
+// With the logit variance: count, mean and centred second moment of this thread's
+// elements, merged chunk by chunk (Chan et al.'s pairwise update), so no sum of
+// squares of raw logits is ever formed.  A -inf element turns them into NaN; that
+// case is redone with the guarded pass.
 struct ConfState {
   NormState n;
   float t1 = -INFINITY;
   float t2 = -INFINITY;
   int gid = -1;
+  float vn = 0.f, vmean = 0.f, vm2 = 0.f;
 };
 
 template <int N, bool GUARD>
+__device__ __forceinline__ void var_chunk(ConfState& s, const float* f, uint32_t valid) {
+  float cs = 0.f;
+  int cnt = N;
+  if (GUARD) cnt = __popc(valid);
+#pragma unroll
+  for (int j = 0; j < N; ++j) cs += (!GUARD || ((valid >> j) & 1u)) ? f[j] : 0.f;
+  if (cnt == 0) return;
+  const float cm = GUARD ? cs / (float)cnt : cs * (1.f / (float)N);
+  float c2 = 0.f;
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    const float d = (!GUARD || ((valid >> j) & 1u)) ? f[j] - cm : 0.f;
+    c2 = fmaf(d, d, c2);
+  }
+  const float n1 = s.vn + (float)cnt;
+  const float delta = cm - s.vmean;
+  const float w = (float)cnt / n1;
+  s.vmean = fmaf(delta, w, s.vmean);
+  s.vm2 = s.vm2 + c2 + delta * delta * (s.vn * w);
+  s.vn = n1;
+}
+
+template <int N, bool GUARD, bool VAR>
 __device__ __forceinline__ void conf_chunk(ConfState& s, const float* f, uint32_t valid, int cid) {
   const float cmax = chunk_max<N>(f);
   s.gid = cmax > s.t1 ? cid : s.gid;
   s.t2 = __builtin_amdgcn_fmed3f(s.t1, s.t2, cmax);
   s.t1 = fmaxf(s.t1, cmax);
   norm_chunk<N, GUARD, true>(s.n, f, valid, cmax);
+  if (VAR) var_chunk<N, GUARD>(s, f, valid);
 }
 
+template <bool VAR>
 __device__ __forceinline__ void conf_one(ConfState& s, float z, int cid) {
   float f[1] = {z};
-  conf_chunk<1, false>(s, f, 1u, cid);
+  conf_chunk<1, false, VAR>(s, f, 1u, cid);
 }
 
 // Enumerates the elements of one chunk of thread t (chunk ids: 0 head element,
@@ -372,14 +402,16 @@ struct ConfArgs {
   double lnV;  // ln(vocab)
 };
 
-template <typename T, int BD>
+template <typename T, int BD, bool VAR>
 __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits, int64_t n_rows, int64_t V,
-                                                   int64_t stride, ConfArgs a, cmsd_row_stats* __restrict__ out) {
+                                                   int64_t stride, ConfArgs a, cmsd_row_stats* __restrict__ out,
+                                                   float* __restrict__ var_out) {
   using E = Elem<T>;
   constexpr int VEC = E::VEC, U = E::U, N = VEC * U;
-  __shared__ double sd[BD / 64];
+  constexpr int ND = VAR ? 5 : 2;  // fp64 sums of the epilogue: A, T (+ count, S1, S2)
+  __shared__ double sd[(VAR ? 3 : 1) * (BD / 64)];
   __shared__ float sf[BD / 64];
-  __shared__ double ep_d[2][BD / 64];
+  __shared__ double ep_d[ND][BD / 64];
   __shared__ float ep_f[2][BD / 64];
   __shared__ int ep_i[2][BD / 64];
   const int t = threadIdx.x;
@@ -392,14 +424,14 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
     const int64_t nr = g.nvec / per_round;
 
     ConfState s;
-    if (t < g.head) conf_one(s, E::load(row + t), 0);
+    if (t < g.head) conf_one<VAR>(s, E::load(row + t), 0);
 
     // full rounds, next round's loads issued before the current one is consumed
     stream_rounds<U, BD, CMSD_STREAM_DEPTH>(vp, nr, t, [] {}, [&](const uint4 (&raw)[U], int64_t k) {
       float f[N];
 #pragma unroll
       for (int u = 0; u < U; ++u) E::unpack(raw[u], f + u * VEC);
-      conf_chunk<N, false>(s, f, 0xffffffffu, int(k + 1));
+      conf_chunk<N, false, VAR>(s, f, 0xffffffffu, int(k + 1));
     });
     // partial round
     const int64_t rb = nr * per_round;
@@ -417,10 +449,10 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
           for (int e = 0; e < VEC; ++e) f[u * VEC + e] = -INFINITY;
         }
       }
-      conf_chunk<N, true>(s, f, valid, int(nr + 1));
+      conf_chunk<N, true, VAR>(s, f, valid, int(nr + 1));
     }
     const int64_t tail0 = g.head + g.nvec * VEC;
-    if (t < g.tail) conf_one(s, E::load(row + tail0 + t), int(nr + 2));
+    if (t < g.tail) conf_one<VAR>(s, E::load(row + tail0 + t), int(nr + 2));
 
     // ---- epilogue: row max, first index of the max, second logit, normaliser
     const float m = block_all_f<BD>(s.t1, OpMax(), sf);
@@ -438,12 +470,20 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
 
     // one LDS round for: sum A, sum T, max of the other chunk maxima, number of
     // threads holding the max, and the lowest max index with its chunk's other value
-    double A, Tsum;
+    double A, Tsum, vN = 0.0, vS1 = 0.0, vS2 = 0.0;
     float cmx, s_oth;
     int nmax, top1;
     {
       const double wA = wave_all_d(Ad, OpSumD());
       const double wT = wave_all_d(Td, OpSumD());
+      // variance moments about the row max: n, n (mean - m), M2 + n (mean - m)^2
+      double wN = 0.0, wS1 = 0.0, wS2 = 0.0;
+      if (VAR) {
+        const double n = (double)s.vn, dmu = (double)s.vmean - (double)m;
+        wN = wave_all_d(n, OpSumD());
+        wS1 = wave_all_d(n * dmu, OpSumD());
+        wS2 = wave_all_d(s.vn > 0.f ? (double)s.vm2 + n * dmu * dmu : 0.0, OpSumD());
+      }
       const float wc = wave_all_f(contrib, OpMax());
       const int wn = wave_all_i(is_max ? 1 : 0, OpSumI());
       const int wi = wave_all_i(idx32, OpMinI());
@@ -454,6 +494,11 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
         const int w = t >> 6;
         ep_d[0][w] = wA;
         ep_d[1][w] = wT;
+        if (VAR) {
+          ep_d[ND - 3][w] = wN;
+          ep_d[ND - 2][w] = wS1;
+          ep_d[ND - 1][w] = wS2;
+        }
         ep_f[0][w] = wc;
         ep_f[1][w] = wo;
         ep_i[0][w] = wn;
@@ -466,10 +511,20 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
       s_oth = ep_f[1][0];
       nmax = ep_i[0][0];
       top1 = ep_i[1][0];
+      if (VAR) {
+        vN = ep_d[ND - 3][0];
+        vS1 = ep_d[ND - 2][0];
+        vS2 = ep_d[ND - 1][0];
+      }
 #pragma unroll
       for (int w = 1; w < BD / 64; ++w) {
         A += ep_d[0][w];
         Tsum += ep_d[1][w];
+        if (VAR) {
+          vN += ep_d[ND - 3][w];
+          vS1 += ep_d[ND - 2][w];
+          vS2 += ep_d[ND - 1][w];
+        }
         cmx = fmaxf(cmx, ep_f[0][w]);
         nmax += ep_i[0][w];
         if (ep_i[1][w] < top1) {
@@ -480,13 +535,20 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
     }
     uint32_t flags = 0;
     if (Tsum != Tsum) {
-      // the row holds -inf logits: recompute T skipping them
+      // the row holds -inf logits: recompute T (and the variance moments) skipping them
       flags |= 1u;
       float tl = 0.f;
+      double vm[3] = {0.0, 0.0, 0.0};
       auto acc = [&](float z) {
         if (z > -INFINITY) {
           const float x = fmaf(z, kLog2e, -ms_row);
           tl = fmaf(fexp2(x), x, tl);
+          if (VAR) {
+            const double dz = (double)z - (double)m;
+            vm[0] += 1.0;
+            vm[1] += dz;
+            vm[2] += dz * dz;
+          }
         }
       };
       if (t < g.head) acc(E::load(row + t));
@@ -498,6 +560,12 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
       }
       if (t < g.tail) acc(E::load(row + tail0 + t));
       Tsum = block_all_d<BD>((double)tl, OpSumD(), sd);
+      if (VAR) {
+        block_sum_n<BD, 3>(vm, sd);
+        vN = vm[0];
+        vS1 = vm[1];
+        vS2 = vm[2];
+      }
     }
     __syncthreads();
     if (t == 0) {
@@ -524,6 +592,10 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
       o.top1 = top1;
       o.flags = flags;
       out[r] = o;
+      if (VAR) {
+        const double v = (vS2 - vS1 * (vS1 / vN)) / vN;
+        var_out[r] = (float)(v > 0.0 ? v : 0.0);
+      }
     }
     __syncthreads();
   }
@@ -1409,16 +1481,16 @@ int row_block(int64_t n_rows, int64_t row_bytes) {
   return 256;
 }
 
-template <typename T>
+template <typename T, bool VAR>
 void launch_confidence(int bd, const T* logits, int64_t n_rows, int64_t V, int64_t stride, const ConfArgs& a,
-                       cmsd_row_stats* out, hipStream_t st) {
+                       cmsd_row_stats* out, float* var, hipStream_t st) {
   const dim3 grid((unsigned)n_rows);
   if (bd == 64)
-    hipLaunchKernelGGL((k_confidence<T, 64>), grid, dim3(64), 0, st, logits, n_rows, V, stride, a, out);
+    hipLaunchKernelGGL((k_confidence<T, 64, VAR>), grid, dim3(64), 0, st, logits, n_rows, V, stride, a, out, var);
   else if (bd == 128)
-    hipLaunchKernelGGL((k_confidence<T, 128>), grid, dim3(128), 0, st, logits, n_rows, V, stride, a, out);
+    hipLaunchKernelGGL((k_confidence<T, 128, VAR>), grid, dim3(128), 0, st, logits, n_rows, V, stride, a, out, var);
   else
-    hipLaunchKernelGGL((k_confidence<T, 256>), grid, dim3(256), 0, st, logits, n_rows, V, stride, a, out);
+    hipLaunchKernelGGL((k_confidence<T, 256, VAR>), grid, dim3(256), 0, st, logits, n_rows, V, stride, a, out, var);
 }
 
 template <typename T>
@@ -1438,6 +1510,36 @@ void launch_target_rows(int bd, const VerifyArgs& a, hipStream_t st) {
 int verify_slices(int64_t vocab, int elem_bytes) {
   const int64_t units = vocab / (16 / elem_bytes) + 2;
   return (int)((units + kSliceUnits - 1) / kSliceUnits);
+}
+
+cmsd_status confidence_impl(const void* logits, int32_t dtype, int64_t n_rows, int64_t vocab, int64_t row_stride,
+                            const cmsd_conf_params* params, cmsd_row_stats* stats, float* logit_var, bool want_var,
+                            void* stream) {
+  if (dtype != CMSD_F32 && dtype != CMSD_BF16) return CMSD_ERR_DTYPE;
+  if (!params) return CMSD_ERR_ARG;
+  if (n_rows < 0 || n_rows > INT32_MAX || vocab < 2 || vocab > INT32_MAX || row_stride < vocab) return CMSD_ERR_ARG;
+  const float l1 = params->lambda_ent, l2 = params->lambda_margin, l3 = params->lambda_soft;
+  if (!(l1 >= 0.f && l1 <= 1.f && l2 >= 0.f && l2 <= 1.f && l3 >= 0.f && l3 <= 1.f)) return CMSD_ERR_ARG;
+  if (fabs((double)l1 + (double)l2 + (double)l3 - 1.0) > 1e-6) return CMSD_ERR_ARG;
+  if (!finite_f(params->beta_margin) || !(params->beta_margin > 0.f)) return CMSD_ERR_ARG;
+  const size_t es = dtype == CMSD_F32 ? 4 : 2;
+  if (n_rows == 0) return CMSD_OK;
+  if (!logits || !stats || !aligned(logits, es) || !aligned(stats, 4)) return CMSD_ERR_ARG;
+  if (want_var && (!logit_var || !aligned(logit_var, 4))) return CMSD_ERR_ARG;
+  if (row_stride > INT64_MAX / n_rows) return CMSD_ERR_ARG;
+  const ConfArgs a{l1, l2, l3, params->beta_margin, log((double)vocab)};
+  const int bd = row_block(n_rows, vocab * (int64_t)es);
+  const hipStream_t st = as_stream(stream);
+  if (dtype == CMSD_F32) {
+    const float* p = static_cast<const float*>(logits);
+    if (want_var) launch_confidence<float, true>(bd, p, n_rows, vocab, row_stride, a, stats, logit_var, st);
+    else launch_confidence<float, false>(bd, p, n_rows, vocab, row_stride, a, stats, nullptr, st);
+  } else {
+    const Bf16* p = static_cast<const Bf16*>(logits);
+    if (want_var) launch_confidence<Bf16, true>(bd, p, n_rows, vocab, row_stride, a, stats, logit_var, st);
+    else launch_confidence<Bf16, false>(bd, p, n_rows, vocab, row_stride, a, stats, nullptr, st);
+  }
+  return launched();
 }
 
 }  // namespace
@@ -1503,24 +1605,13 @@ size_t cmsd_verify_workspace_bytes(int32_t batch, int32_t k_max, int64_t vocab) 
 
 cmsd_status cmsd_confidence(const void* logits, int32_t dtype, int64_t n_rows, int64_t vocab, int64_t row_stride,
                             const cmsd_conf_params* params, cmsd_row_stats* stats, void* stream) {
-  if (dtype != CMSD_F32 && dtype != CMSD_BF16) return CMSD_ERR_DTYPE;
-  if (!params) return CMSD_ERR_ARG;
-  if (n_rows < 0 || n_rows > INT32_MAX || vocab < 2 || vocab > INT32_MAX || row_stride < vocab) return CMSD_ERR_ARG;
-  const float l1 = params->lambda_ent, l2 = params->lambda_margin, l3 = params->lambda_soft;
-  if (!(l1 >= 0.f && l1 <= 1.f && l2 >= 0.f && l2 <= 1.f && l3 >= 0.f && l3 <= 1.f)) return CMSD_ERR_ARG;
-  if (fabs((double)l1 + (double)l2 + (double)l3 - 1.0) > 1e-6) return CMSD_ERR_ARG;
-  if (!finite_f(params->beta_margin) || !(params->beta_margin > 0.f)) return CMSD_ERR_ARG;
-  const size_t es = dtype == CMSD_F32 ? 4 : 2;
-  if (n_rows == 0) return CMSD_OK;
-  if (!logits || !stats || !aligned(logits, es) || !aligned(stats, 4)) return CMSD_ERR_ARG;
-  if (row_stride > INT64_MAX / n_rows) return CMSD_ERR_ARG;
-  const ConfArgs a{l1, l2, l3, params->beta_margin, log((double)vocab)};
-  const int bd = row_block(n_rows, vocab * (int64_t)es);
-  if (dtype == CMSD_F32)
-    launch_confidence(bd, static_cast<const float*>(logits), n_rows, vocab, row_stride, a, stats, as_stream(stream));
-  else
-    launch_confidence(bd, static_cast<const Bf16*>(logits), n_rows, vocab, row_stride, a, stats, as_stream(stream));
-  return launched();
+  return confidence_impl(logits, dtype, n_rows, vocab, row_stride, params, stats, nullptr, false, stream);
+}
+
+cmsd_status cmsd_confidence_var(const void* logits, int32_t dtype, int64_t n_rows, int64_t vocab,
+                                int64_t row_stride, const cmsd_conf_params* params, cmsd_row_stats* stats,
+                                float* logit_var, void* stream) {
+  return confidence_impl(logits, dtype, n_rows, vocab, row_stride, params, stats, logit_var, true, stream);
 }
 
 cmsd_status cmsd_draft_len(const cmsd_row_stats* stats, int32_t batch, const cmsd_draft_params* params,

@@ -124,3 +124,56 @@ def test_empty_and_errors(cm):
         cm.cmsd_confidence(torch.zeros((4, 1), device=dev))            # V < 2
     with pytest.raises(cm.CmsdError):
         cm.cmsd_confidence(torch.zeros((4, 16), device=dev), lambdas=(0.5, 0.5, 0.5))
+
+
+def _check_var(got, ref, what):
+    assert abs(got - ref) <= 1e-4 * max(abs(ref), 1e-2), (what, got, ref)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("V", [2, 9, 1025, 4099, 50257, 131072 + 17])
+@pytest.mark.parametrize("pad", [0, 5])
+def test_logit_variance_rows(cm, dtype, V, pad):
+    # cmsd_confidence_var: the same stats as cmsd_confidence, and the variance of the
+    # finite logits against the oracle's two-pass definition (Sec. I proxy)
+    g = np.random.default_rng(V * 3 + pad)
+    rows = _invariant_rows(V, g)
+    rows.append(1000.0 + g.normal(0, 1, V))                      # large common offset
+    z = g.normal(0, 0.3, V); z[g.integers(0, V)] += 15.0; rows.append(z)   # near-one-hot
+    stored = _store(rows, dtype)
+    n = stored.shape[0]
+    buf = np.zeros((n, V + pad), dtype=stored.dtype)
+    buf[:, :V] = stored
+    tdev = Hn.to_device(buf, dtype, torch.device("cuda:0"))[:, :V]
+    st, var = cm.cmsd_confidence_var(tdev, lambdas=(0.2, 0.5, 0.3), beta_margin=0.7)
+    st0 = cm.cmsd_confidence(tdev, lambdas=(0.2, 0.5, 0.3), beta_margin=0.7)
+    torch.cuda.synchronize()
+    assert torch.equal(st.view(torch.int32), st0.view(torch.int32))
+    var = var.cpu().numpy()
+    for r in range(n):
+        _check_var(float(var[r]), O.logit_variance(Hn.decode(stored[r], dtype)), (r, V, dtype))
+
+
+@pytest.mark.parametrize("block", [64, 128, 256])
+def test_logit_variance_each_row_block(cm, monkeypatch, block):
+    monkeypatch.setenv("CMSD_ROW_BLOCK", str(block))
+    g = np.random.default_rng(block)
+    V = 20011
+    stored = _store(_invariant_rows(V, g), "bf16")
+    tdev = Hn.to_device(stored, "bf16", torch.device("cuda:0"))
+    _, var = cm.cmsd_confidence_var(tdev)
+    torch.cuda.synchronize()
+    var = var.cpu().numpy()
+    for r in range(stored.shape[0]):
+        _check_var(float(var[r]), O.logit_variance(Hn.decode(stored[r], "bf16")), (r, block))
+
+
+@pytest.mark.parametrize("name,nsample", [("c3", 64), ("c4", 24), ("c5", 24)])
+def test_logit_variance_config_rows(cm, name, nsample):
+    cfg = W.CONFIGS[name]
+    d = Hn.workload(name, 0)
+    _, var = cm.cmsd_confidence_var(d["draft_dev"])
+    torch.cuda.synchronize()
+    var = var.cpu().numpy()
+    for r in _sample_rows(cfg, nsample):
+        _check_var(float(var[r]), O.logit_variance(Hn.decode(d["draft"][r], cfg.dtype)), (name, r))

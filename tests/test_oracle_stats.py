@@ -152,3 +152,46 @@ def test_decode_logits_bf16():
     assert v[3] == pytest.approx(3.3895313892515355e38)
     assert v[4] == -math.inf
     assert v[5] == 0.125
+
+
+# ----------------------------------------------------------------------------- logit variance (Sec. I)
+@pytest.mark.parametrize("V", [1, 2, 1000])
+def test_logit_variance_constant_rows(V):
+    assert O.logit_variance(np.full(V, 3.25)) == 0.0
+    z = np.full(V + 5, -math.inf)
+    z[2] = 7.0                                    # one finite logit
+    assert O.logit_variance(z) == 0.0
+
+
+@pytest.mark.parametrize("n1,n2,a,b", [(1, 1, 0.0, 1.0), (3, 7, -2.5, 4.0), (1, 999, 10.0, 0.0), (500, 500, 1.0, -1.0)])
+def test_logit_variance_two_point_closed_form(n1, n2, a, b):
+    # n1 logits at a, n2 at b: variance n1 n2 (a - b)^2 / (n1 + n2)^2
+    z = np.concatenate([np.full(n1, a), np.full(n2, b), np.full(4, -math.inf)])
+    _rng(0).shuffle(z)
+    want = n1 * n2 * (a - b) ** 2 / (n1 + n2) ** 2
+    assert O.logit_variance(z) == pytest.approx(want, rel=1e-13, abs=1e-15)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_logit_variance_pairwise_identity(seed):
+    # brute force over pairs: var = sum_i sum_j (z_i - z_j)^2 / (2 n^2), -inf left out
+    g = _rng(40 + seed)
+    V = int(g.integers(2, 60))
+    z = g.normal(0, float(g.uniform(0.1, 20)), V)
+    z[g.random(V) < 0.2] = -math.inf
+    if not np.isfinite(z).any():
+        z[0] = 1.0
+    f = z[np.isfinite(z)]
+    n = f.size
+    want = sum((x - y) ** 2 for x in f for y in f) / (2 * n * n)
+    assert O.logit_variance(z) == pytest.approx(want, rel=1e-12, abs=1e-14)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_logit_variance_shift_and_scale(seed):
+    g = _rng(60 + seed)
+    z = g.normal(0, 3, 777)
+    v = O.logit_variance(z)
+    assert O.logit_variance(z + 1000.0) == pytest.approx(v, rel=1e-9)
+    assert O.logit_variance(2.0 * z) == pytest.approx(4.0 * v, rel=1e-13)
+    assert O.logit_variance(g.permutation(z)) == pytest.approx(v, rel=1e-13)
