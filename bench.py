@@ -103,6 +103,8 @@ def main() -> int:
     ap.add_argument("--workload", default="c4", choices=["c2", "c3", "c4", "c5"])
     ap.add_argument("--mode", default="cm", choices=["cm", "standard"])
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--event-every", type=int, default=4, metavar="N",
+                    help="bracket k_confidence with HIP events in every N-th timed step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run device-to-device copies of MIB MiB (calibrates HBM byte counters)")
@@ -159,21 +161,24 @@ def main() -> int:
     torch.cuda.synchronize()
 
     # timed region: K steps.  HIP events on the launch stream bracket the roofline
-    # kernel (k_confidence) in every step; each event marker costs a few us of GPU
-    # time, so no other call is bracketed here.
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    # kernel (k_confidence) in every `event_every`-th step; each event marker costs
+    # GPU time between kernels, so no other call is bracketed here.
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] if k % args.event_every == 0 else None
+          for k in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for e in ev:
-        e[0].record(stream)
+        if e is not None:
+            e[0].record(stream)
         lp.confidence(draft, stream)
-        e[1].record(stream)
+        if e is not None:
+            e[1].record(stream)
         lp.draft_len(stream)
         lp.verify(draft, target, drafted, unif, stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_step = 1e3 * elapsed / args.steps
-    t_conf = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) * 1e-3
+    t_conf = float(np.mean([e[0].elapsed_time(e[1]) for e in ev if e is not None])) * 1e-3
 
     # per-call split (outside the timed region)
     ev2 = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(max(3, args.steps // 4))]
