@@ -22,7 +22,7 @@ def cm():
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("V", [2, 7, 1000, 32000, 50257, 128259])
+@pytest.mark.parametrize("V", [2, 7, 1000, 32000, 50257, 128259, 600011])
 def test_draft_sample_rows(cm, dtype, V):
     g = np.random.default_rng(V + (7 if dtype == "bf16" else 0))
     n = 24

@@ -189,6 +189,29 @@ def test_each_row_block(mods, monkeypatch, block, dtype, mode):
     t.assert_ok()
 
 
+@pytest.mark.parametrize("dtype,V", [("f32", 300007), ("bf16", 600011)])
+@pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY])
+def test_vocab_beyond_one_slice_per_thread(mods, dtype, V, mode):
+    # more than 256 vocabulary slices: the sampling pass runs several slices per thread
+    g = np.random.default_rng(V + mode)
+    B, K = 3, 2
+    zd, zt_pad, drafted, unif_pad = _small_case(g, B, K, V, dtype)
+    k = np.array([2, 0, 1], dtype=np.int32)
+    zt = W.pack_ragged(k, K, zt_pad.reshape(B, K + 1, V))
+    unif = W.pack_ragged(k, K, unif_pad.reshape(B, K + 1, 1)).reshape(-1)
+    off = np.concatenate([[0], np.cumsum(k + 1)]).astype(np.int32)
+    gs, n_acc, nxt, ts = _run_small(mods, zd, zt, drafted, unif, k, dtype, B, K, V, mode=mode)
+    t = Hn.Tally()
+    for b in range(B):
+        kb = int(k[b])
+        zdr = [Hn.decode(zd[b * K + i], dtype) for i in range(K)]
+        ztr = [Hn.decode(zt[off[b] + i], dtype) for i in range(kb + 1)]
+        C = [Hn.oracle_conf(z, V) for z in zdr]
+        Hn.check_sequence(t, b, ztr, zdr, drafted[b], unif[off[b]:off[b] + kb + 1], C, kb, mode, Hn.PARAMS,
+                          ts, int(off[b]), int(n_acc[b]), int(nxt[b]))
+    t.assert_ok()
+
+
 def test_equal_rows_accept_everything_and_masked_targets(mods):
     g = np.random.default_rng(5)
     B, K, V = 4, 6, 3000
