@@ -2,19 +2,25 @@
 // speculative decoding (arXiv 2508.15371, Sec. III.B).  Interface: include/cmsd.h.
 //
 // Kernels (all bandwidth-bound streaming reductions; no MFMA):
-//   k_confidence   one workgroup per drafter row: single streaming pass with an
-//                  online max / sum-exp / sum(e*(z-m)) reduction, top-1 and top-2
-//                  tracking at chunk granularity, DPP wave reductions, LDS only for
-//                  the cross-wave combine; epilogue forms H, margins and C.
-//   k_draft_len    one workgroup: per-sequence mean confidence, clipped floor,
-//                  exclusive scan of k_b + 1 into packed target-row offsets.
-//   k_target_rows  one workgroup per packed target row: max / sum-exp of the row,
-//                  scalar (ballot + s_bcnt1) count of logits above the drafted
-//                  token's, and the acceptance decision of that position.
-//   k_final        one workgroup per sequence: ballot-based first-reject scan, then
-//                  an inverse-CDF sample from the residual (or bonus) row using a
-//                  per-thread contiguous span, a workgroup scan and a wave-level
-//                  locate that reproduces the scan's sums bit for bit.
+//   k_confidence    one workgroup (64/128/256 threads, by launch shape) per drafter
+//                   row: single streaming pass with an online max / sum-exp /
+//                   sum(e*(z-m)) reduction, top-1 and top-2 tracking at chunk
+//                   granularity, DPP wave reductions, LDS only for the cross-wave
+//                   combine; epilogue forms H, margins and C (optionally the
+//                   variance of the logits).
+//   k_draft_len     one workgroup: per-sequence mean confidence, clipped floor,
+//                   exclusive scan of k_b + 1 into packed target-row offsets.
+//   k_target_rows   one workgroup per packed target row: max / sum-exp of the row,
+//                   scalar (ballot + s_bcnt1) count of logits above the drafted
+//                   token's, the acceptance decision of that position, and the
+//                   row's slot in the workspace.
+//   k_final_parts   one wave per (sequence, vocabulary slice): first rejection from
+//                   the row slots (ballot), then fp64 slice partials of the
+//                   residual (or bonus) row.
+//   k_final_sample  one workgroup per sequence: slice scan, then an exact in-slice
+//                   inverse-CDF locate that repeats the scan's sums bit for bit.
+//   k_draft_parts / k_draft_pick   the same slice machinery for one softmax sample
+//                   per drafter row.
 //
 // Numerics: exponentials are evaluated as 2^(z*log2e - m*log2e) with one FMA and
 // v_exp_f32; per-thread partial sums are fp32 over 32-element chunks, the
@@ -123,19 +129,12 @@ template <int CTRL>
 __device__ __forceinline__ float dpp_f(float v) { return __int_as_float(dpp_i<CTRL>(__float_as_int(v))); }
 template <int CTRL>
 __device__ __forceinline__ double dpp_d(double v) {
-  const int2 p = *reinterpret_cast<int2*>(&v);
-  int2 r;
-  r.x = dpp_i<CTRL>(p.x);
-  r.y = dpp_i<CTRL>(p.y);
-  return *reinterpret_cast<double*>(&r);
+  return __hiloint2double(dpp_i<CTRL>(__double2hiint(v)), dpp_i<CTRL>(__double2loint(v)));
 }
 __device__ __forceinline__ float rl_f(float v, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l)); }
 __device__ __forceinline__ double rl_d(double v, int l) {
-  const int2 p = *reinterpret_cast<int2*>(&v);
-  int2 r;
-  r.x = __builtin_amdgcn_readlane(p.x, l);
-  r.y = __builtin_amdgcn_readlane(p.y, l);
-  return *reinterpret_cast<double*>(&r);
+  return __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(v), l),
+                          __builtin_amdgcn_readlane(__double2loint(v), l));
 }
 
 struct OpMax { __device__ float operator()(float a, float b) const { return fmaxf(a, b); } };
