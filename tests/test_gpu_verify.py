@@ -346,3 +346,28 @@ def test_long_drafts(mods, mode, K):
         Hn.check_sequence(t, b, ztr, zdr, drafted[b], unif[off[b]:off[b] + kb + 1], C, kb, mode, prm, ts,
                           int(off[b]), int(n_acc[b]), int(nxt[b]))
     t.assert_ok()
+
+
+def test_side_stream_matches_default_stream(mods):
+    # every call enqueues on the stream it is given: a full iteration on a side
+    # stream, ordered after the uploads by an event, gives the default stream's
+    # results bit for bit
+    cmsd, pipeline = mods
+    cfg = W.CONFIGS["c2"]
+    d = Hn.workload("c2", 0)
+    outs = []
+    for use_side in (False, True):
+        lp = pipeline.LogitPass(cfg.B, cfg.k_max, cfg.V, "cuda:0", _params(pipeline, O.MODE_CM))
+        if use_side:
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                lp.run(d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"], stream=side)
+            torch.cuda.current_stream().wait_stream(side)
+        else:
+            lp.run(d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"])
+        torch.cuda.synchronize()
+        outs.append([x.cpu().clone() for x in (lp.stats, lp.k, lp.off, lp.tstats, lp.n_acc, lp.next_tok)])
+    for a, b in zip(*outs):
+        assert torch.equal(a.view(torch.int32) if a.dtype == torch.float32 else a,
+                           b.view(torch.int32) if b.dtype == torch.float32 else b)
