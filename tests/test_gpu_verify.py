@@ -371,3 +371,36 @@ def test_side_stream_matches_default_stream(mods):
     for a, b in zip(*outs):
         assert torch.equal(a.view(torch.int32) if a.dtype == torch.float32 else a,
                            b.view(torch.int32) if b.dtype == torch.float32 else b)
+
+
+def test_graph_capture_replays_match_eager(mods):
+    # the iteration allocates nothing and synchronises nothing, so it can be captured
+    # in a HIP graph: every replay (with eager work in between) matches the eager run
+    cmsd, pipeline = mods
+    cfg = W.CONFIGS["c2"]
+    d = Hn.workload("c2", 0)
+    args = (d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"])
+    ref = pipeline.LogitPass(cfg.B, cfg.k_max, cfg.V, "cuda:0", _params(pipeline, O.MODE_CM))
+    ref.run(*args)
+    torch.cuda.synchronize()
+    want = [x.clone() for x in (ref.stats, ref.k, ref.off, ref.tstats, ref.n_acc, ref.next_tok)]
+    lp = pipeline.LogitPass(cfg.B, cfg.k_max, cfg.V, "cuda:0", _params(pipeline, O.MODE_CM))
+    lp.run(*args)                                  # warm-up outside the capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        lp.run(*args)
+    junk = torch.zeros(1 << 20, device="cuda:0")
+    for rep in range(4):
+        for x in (lp.stats, lp.tstats):
+            x.fill_(float("nan"))
+        lp.n_acc.fill_(-7)
+        lp.next_tok.fill_(-7)
+        junk.add_(1.0)                             # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = (lp.stats, lp.k, lp.off, lp.tstats, lp.n_acc, lp.next_tok)
+        for a, b in zip(got, want):
+            assert torch.equal(a.view(torch.int32) if a.dtype == torch.float32 else a,
+                               b.view(torch.int32) if b.dtype == torch.float32 else b), rep
