@@ -108,9 +108,24 @@ def _rows(t: torch.Tensor, name: str) -> tuple[int, int, int]:
     """(rows, vocab, row_stride) of a [rows, V] logit matrix with unit inner stride."""
     if t.dim() != 2 or t.stride(1) != 1:
         raise ValueError(f"{name} must be a 2-D [rows, vocab] tensor with unit inner stride")
+    return t.shape[0], t.shape[1], t.stride(0)
+
+
+def _on_device(t: torch.Tensor, name: str) -> None:
+    """Checked after every size check, so those also run on host tensors."""
     if not t.is_cuda:
         raise ValueError(f"{name} must be a device tensor")
-    return t.shape[0], t.shape[1], t.stride(0)
+
+
+def _buf(t: torch.Tensor, name: str, dtype: torch.dtype, min_elems: int, device: torch.device) -> None:
+    """A caller-owned buffer: a contiguous ``dtype`` tensor on ``device`` with at
+    least ``min_elems`` elements (the kernels take plain pointers and cannot check)."""
+    if t.dtype != dtype or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {dtype} tensor")
+    if t.numel() < min_elems:
+        raise ValueError(f"{name} has {t.numel()} elements; {min_elems} are needed")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device}, not {t.device}")
 
 
 def _check(fn: str, status: int) -> None:
@@ -125,7 +140,9 @@ def cmsd_confidence(logits: torch.Tensor, stats: torch.Tensor | None = None, *,
     n, V, st = _rows(logits, "logits")
     if stats is None:
         stats = torch.empty((n, 8), dtype=torch.float32, device=logits.device)
+    _buf(stats, "stats", torch.float32, 8 * n, logits.device)
     p = ConfParams(float(lambdas[0]), float(lambdas[1]), float(lambdas[2]), float(beta_margin))
+    _on_device(logits, "logits")
     _check("cmsd_confidence", _lib.cmsd_confidence(_ptr(logits), _dtype_code(logits), n, V, st, C.byref(p),
                                                    _ptr(stats), _stream(stream)))
     return stats
@@ -141,7 +158,10 @@ def cmsd_confidence_var(logits: torch.Tensor, stats: torch.Tensor | None = None,
         stats = torch.empty((n, 8), dtype=torch.float32, device=logits.device)
     if logit_var is None:
         logit_var = torch.empty(n, dtype=torch.float32, device=logits.device)
+    _buf(stats, "stats", torch.float32, 8 * n, logits.device)
+    _buf(logit_var, "logit_var", torch.float32, n, logits.device)
     p = ConfParams(float(lambdas[0]), float(lambdas[1]), float(lambdas[2]), float(beta_margin))
+    _on_device(logits, "logits")
     _check("cmsd_confidence_var", _lib.cmsd_confidence_var(_ptr(logits), _dtype_code(logits), n, V, st, C.byref(p),
                                                            _ptr(stats), _ptr(logit_var), _stream(stream)))
     return stats, logit_var
@@ -157,7 +177,11 @@ def cmsd_draft_len(stats: torch.Tensor, batch: int, *, k_min: int, k_max: int, a
         draft_len = torch.empty(batch, dtype=torch.int32, device=dev)
     if target_offsets is None:
         target_offsets = torch.empty(batch + 1, dtype=torch.int32, device=dev)
+    _buf(stats, "stats", torch.float32, 8 * batch * k_max, dev)
+    _buf(draft_len, "draft_len", torch.int32, batch, dev)
+    _buf(target_offsets, "target_offsets", torch.int32, batch + 1, dev)
     p = DraftParams(int(k_min), int(k_max), float(alpha))
+    _on_device(stats, "stats")
     _check("cmsd_draft_len", _lib.cmsd_draft_len(_ptr(stats), int(batch), C.byref(p), _ptr(draft_len),
                                                  _ptr(target_offsets), _stream(stream)))
     return draft_len, target_offsets
@@ -196,13 +220,26 @@ def cmsd_verify(draft_logits: torch.Tensor, draft_stats: torch.Tensor, target_lo
         next_token = torch.empty(batch, dtype=torch.int32, device=dev)
     if workspace is None:
         workspace = verify_workspace(batch, k_max, V, dev)
-    for name, t, dt in (("target_offsets", target_offsets, torch.int32), ("draft_len", draft_len, torch.int32),
-                        ("drafted", drafted, torch.int32), ("uniforms", uniforms, torch.float32)):
+    drows = draft_logits.shape[0]
+    if drows < batch * k_max:
+        raise ValueError(f"draft_logits has {drows} rows; batch*k_max = {batch * k_max} are needed")
+    if draft_logits.device != dev:
+        raise ValueError("draft and target logits must be on one device")
+    for name, t, dt, n in (("draft_stats", draft_stats, torch.float32, 8 * batch * k_max),
+                           ("target_offsets", target_offsets, torch.int32, batch + 1),
+                           ("draft_len", draft_len, torch.int32, batch),
+                           ("drafted", drafted, torch.int32, batch * k_max),
+                           ("uniforms", uniforms, torch.float32, trows),
+                           ("target_stats", target_stats, torch.float32, 8 * trows),
+                           ("n_accepted", n_accepted, torch.int32, batch),
+                           ("next_token", next_token, torch.int32, batch)):
         if t is None and name == "uniforms":
             continue
-        if t.dtype != dt or not t.is_contiguous():
-            raise ValueError(f"{name} must be a contiguous {dt} tensor")
+        _buf(t, name, dt, n, dev)
+    if workspace.dtype != torch.float64 or not workspace.is_contiguous() or workspace.device != dev:
+        raise ValueError(f"workspace must be a contiguous float64 tensor on {dev}")
     p = VerifyParams(int(mode), int(top_beta), float(tau_base), float(gamma))
+    _on_device(target_logits, "target_logits")
     _check("cmsd_verify", _lib.cmsd_verify(
         _ptr(draft_logits), dst, _ptr(draft_stats), _ptr(target_logits), tst, trows,
         _ptr(target_offsets), _ptr(draft_len), _ptr(drafted), _ptr(uniforms), _dtype_code(target_logits),
@@ -227,8 +264,12 @@ def cmsd_draft_sample(logits: torch.Tensor, stats: torch.Tensor, uniforms: torch
     if workspace is None:
         workspace = torch.empty(max(1, (cmsd_draft_sample_workspace_bytes(n, V) + 7) // 8), dtype=torch.float64,
                                 device=dev)
-    if uniforms.dtype != torch.float32 or not uniforms.is_contiguous():
-        raise ValueError("uniforms must be a contiguous float32 tensor")
+    _buf(stats, "stats", torch.float32, 8 * n, dev)
+    _buf(uniforms, "uniforms", torch.float32, n, dev)
+    _buf(drafted, "drafted", torch.int32, n, dev)
+    if workspace.dtype != torch.float64 or not workspace.is_contiguous() or workspace.device != dev:
+        raise ValueError(f"workspace must be a contiguous float64 tensor on {dev}")
+    _on_device(logits, "logits")
     _check("cmsd_draft_sample", _lib.cmsd_draft_sample(
         _ptr(logits), _dtype_code(logits), n, V, st, _ptr(stats), _ptr(uniforms), _ptr(drafted), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
