@@ -103,6 +103,8 @@ def main() -> int:
     ap.add_argument("--workload", default="c4", choices=["c2", "c3", "c4", "c5"])
     ap.add_argument("--mode", default="cm", choices=["cm", "standard"])
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--streams", type=int, default=1, metavar="G",
+                    help="split the batch into G sequence groups, each on its own stream")
     ap.add_argument("--event-every", type=int, default=4, metavar="N",
                     help="bracket k_confidence with HIP events in every N-th timed step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -143,61 +145,87 @@ def main() -> int:
     drafted = torch.from_numpy(d["drafted"].reshape(-1)).to(dev)
     unif = torch.from_numpy(d["uniforms"].reshape(-1)).to(dev)
     del d
-    lp = pipeline.LogitPass(cfg.B, cfg.k_max, cfg.V, dev, pipeline.Params(mode=mode), dense=not cfg.ragged)
-    stream = torch.cuda.current_stream(dev)
-    R_d, R_t = cfg.draft_rows, cfg.dense_target_rows
-    if cfg.ragged:
-        # the verifier scores k_b + 1 positions per sequence, packed by the device
-        # offsets: pack the target rows and uniforms once (untimed); every timed step
-        # recomputes the same draft lengths from the same drafter rows
-        lp.confidence(draft, stream)
-        lp.draft_len(stream)
-        target = W.pack_device(target, lp.k, lp.off, cfg.k_max)
-        unif = W.pack_device(unif, lp.k, lp.off, cfg.k_max)
-        R_t = int(lp.off[cfg.B].item())
+    G = args.streams
+    if G < 1 or cfg.B % G:
+        print(f"bench.py: --streams must divide B={cfg.B}", file=sys.stderr)
+        return 2
+    # G groups of B/G sequences, each on its own stream: sequences are independent,
+    # so the latency-bound tail of one group overlaps the row passes of another
+    K, bg = cfg.k_max, cfg.B // G
+    prm = pipeline.Params(mode=mode)
+    main = torch.cuda.current_stream(dev)
+    groups = []
+    for g in range(G):
+        b0, b1 = g * bg, (g + 1) * bg
+        lpg = pipeline.LogitPass(bg, K, cfg.V, dev, prm, dense=not cfg.ragged)
+        a = [draft[b0 * K:b1 * K], target[b0 * (K + 1):b1 * (K + 1)], drafted[b0 * K:b1 * K],
+             unif[b0 * (K + 1):b1 * (K + 1)]]
+        if cfg.ragged:
+            # the verifier scores k_b + 1 positions per sequence, packed by the device
+            # offsets: pack the target rows and uniforms once (untimed); every timed
+            # step recomputes the same draft lengths from the same drafter rows
+            lpg.confidence(a[0], main)
+            lpg.draft_len(main)
+            a[1] = W.pack_device(a[1], lpg.k, lpg.off, K)
+            a[3] = W.pack_device(a[3], lpg.k, lpg.off, K)
+        groups.append((lpg, a, main if G == 1 else torch.cuda.Stream(dev)))
+    torch.cuda.synchronize()
+    R_d = cfg.draft_rows
+    R_t = sum(int(lpg.off[bg].item()) for lpg, _, _ in groups) if cfg.ragged else cfg.dense_target_rows
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
-        lp.run(draft, target, drafted, unif, stream)
+        for lpg, a, st in groups:
+            lpg.run(*a, st)
     torch.cuda.synchronize()
 
     # timed region: K steps.  HIP events on the launch stream bracket the roofline
-    # kernel (k_confidence) in every `event_every`-th step; each event marker costs
-    # GPU time between kernels, so no other call is bracketed here.
+    # kernel (k_confidence of group 0) in every `event_every`-th step; each event
+    # marker costs GPU time between kernels, so no other call is bracketed here.
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] if k % args.event_every == 0 else None
           for k in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for e in ev:
-        if e is not None:
-            e[0].record(stream)
-        lp.confidence(draft, stream)
-        if e is not None:
-            e[1].record(stream)
-        lp.draft_len(stream)
-        lp.verify(draft, target, drafted, unif, stream)
+        for gi, (lpg, a, st) in enumerate(groups):
+            if e is not None and gi == 0:
+                e[0].record(st)
+            lpg.confidence(a[0], st)
+            if e is not None and gi == 0:
+                e[1].record(st)
+            lpg.draft_len(st)
+            lpg.verify(a[0], a[1], a[2], a[3], st)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_step = 1e3 * elapsed / args.steps
     t_conf = float(np.mean([e[0].elapsed_time(e[1]) for e in ev if e is not None])) * 1e-3
+    conf_rows_timed = R_d // G
 
-    # per-call split (outside the timed region)
-    ev2 = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(max(3, args.steps // 4))]
+    # per-call split, one group after another on one stream (outside the timed region)
+    ev2 = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(max(3, args.steps // 4))]
     for e in ev2:
-        lp.confidence(draft, stream)
-        e[0].record(stream)
-        lp.draft_len(stream)
-        e[1].record(stream)
-        lp.verify(draft, target, drafted, unif, stream)
-        e[2].record(stream)
+        e[0].record(main)
+        for lpg, a, _ in groups:
+            lpg.confidence(a[0], main)
+        e[1].record(main)
+        for lpg, a, _ in groups:
+            lpg.draft_len(main)
+        e[2].record(main)
+        for lpg, a, _ in groups:
+            lpg.verify(a[0], a[1], a[2], a[3], main)
+        e[3].record(main)
     torch.cuda.synchronize()
-    t_dl = float(np.mean([e[0].elapsed_time(e[1]) for e in ev2])) * 1e-3
-    t_ver = float(np.mean([e[1].elapsed_time(e[2]) for e in ev2])) * 1e-3
+    t_conf1 = float(np.mean([e[0].elapsed_time(e[1]) for e in ev2])) * 1e-3
+    t_dl = float(np.mean([e[1].elapsed_time(e[2]) for e in ev2])) * 1e-3
+    t_ver = float(np.mean([e[2].elapsed_time(e[3]) for e in ev2])) * 1e-3
 
-    n_acc = lp.n_acc.cpu().numpy()
-    k_used = lp.k.cpu().numpy() if cfg.ragged else np.full(cfg.B, cfg.k_max)
+    n_acc = np.concatenate([lpg.n_acc.cpu().numpy() for lpg, _, _ in groups])
+    k_all = np.concatenate([lpg.k.cpu().numpy() for lpg, _, _ in groups])
+    k_used = k_all if cfg.ragged else np.full(cfg.B, cfg.k_max)
     rej = int((n_acc < k_used).sum())
     s = cfg.elem_bytes
     conf_bytes = R_d * cfg.V * s + R_d * 32
+    # the roofline kernel's launch: one group's drafter rows (the whole batch when G = 1)
+    launch_bytes = conf_rows_timed * cfg.V * s + conf_rows_timed * 32
     verify_bytes = R_t * cfg.V * s + rej * cfg.V * s + R_t * 32 + cfg.B * cfg.k_max * 8
     step_bytes = conf_bytes + cfg.B * cfg.k_max * 32 + verify_bytes
 
@@ -219,12 +247,12 @@ def main() -> int:
                                f"mode={args.mode}", "batch": cfg.B, "k_max": cfg.k_max, "vocab": cfg.V,
                    "drafter_rows": R_d, "target_rows": R_t},
         "gbps_algorithmic": step_bytes / (ms_step * 1e-3) / 1e9,
-        "per_call_ms": {"cmsd_confidence": t_conf * 1e3, "cmsd_draft_len": t_dl * 1e3, "cmsd_verify": t_ver * 1e3},
-        "roofline": {"kernel": "k_confidence", "bound": "hbm", "achieved": conf_bytes / t_conf / 1e9,
-                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": conf_bytes / t_conf / 1e9 / PEAK_HBM_GBS,
-                     "traffic": _traffic(cfg.name)},
+        "per_call_ms": {"cmsd_confidence": t_conf1 * 1e3, "cmsd_draft_len": t_dl * 1e3, "cmsd_verify": t_ver * 1e3},
+        "roofline": {"kernel": "k_confidence", "bound": "hbm", "achieved": launch_bytes / t_conf / 1e9,
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": launch_bytes / t_conf / 1e9 / PEAK_HBM_GBS,
+                     "traffic": _traffic(cfg.name) if G == 1 else None},
         "workload_stats": {"mean_n_acc": float(n_acc.mean()), "rejecting_sequences": rej,
-                           "mean_draft_len": float(lp.k.float().mean().item())},
+                           "mean_draft_len": float(k_all.mean()), "streams": G},
     }
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
