@@ -100,7 +100,7 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="c4", choices=["c2", "c3", "c4", "c5"])
+    ap.add_argument("--workload", default="c4", choices=["c2", "c3", "c4", "c5", "v152k"])
     ap.add_argument("--mode", default="cm", choices=["cm", "standard"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--streams", type=int, default=1, metavar="G",

@@ -90,7 +90,7 @@ def _sample_rows(cfg, k):
     return sorted(set([0, n - 1] + g.choice(n, k, replace=False).tolist()))
 
 
-@pytest.mark.parametrize("name,nsample", [("tiny", 99), ("c2", 99), ("c3", 512), ("c4", 40), ("c5", 48)])
+@pytest.mark.parametrize("name,nsample", [("tiny", 99), ("c2", 99), ("c3", 512), ("c4", 40), ("c5", 48), ("v152k", 40)])
 def test_config_rows(cm, name, nsample):
     cfg = W.CONFIGS[name]
     print(f"[confidence parity] {name}", flush=True)

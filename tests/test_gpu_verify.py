@@ -95,7 +95,7 @@ def _verify_check(mods, name, mode, nseq):
 
 
 @pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY])
-@pytest.mark.parametrize("name,nseq", [("tiny", 1), ("c2", 8), ("c3", 64), ("c4", 6), ("c5", 24)])
+@pytest.mark.parametrize("name,nseq", [("tiny", 1), ("c2", 8), ("c3", 64), ("c4", 6), ("c5", 24), ("v152k", 8)])
 def test_verify_configs(mods, name, nseq, mode):
     print(f"[verify parity] start {name} mode={mode}", flush=True)
     _verify_check(mods, name, mode, nseq)

@@ -58,3 +58,14 @@ def test_pack_ragged():
     k = np.array([1, 4, 2])
     out = W.pack_ragged(k, K, pad)
     assert out.tolist() == [0, 4, 5, 6, 7, 8, 9, 10, 11, 14]
+
+
+def test_sweep_point_uses_c2_recipe():
+    # v152k draws c2-style rows: same construction, its own config id in the seeds
+    cfg = W.CONFIGS["v152k"]
+    assert cfg.kind == "c2" and cfg.V == 152064
+    z = W.f32_from_bf16_bits(W.draft_row(cfg, 0, 3)).astype(np.float64)
+    assert z.shape == (152064,) and 0.2 < z.std() < 12.0
+    t = W.f32_from_bf16_bits(W.target_row(cfg, 0, 0, 3)).astype(np.float64)
+    assert np.corrcoef(z, t)[0, 1] > 0.5
+    assert not np.array_equal(W.draft_row(cfg, 0, 3)[:32000], W.draft_row(W.CONFIGS["c2"], 0, 3))

@@ -34,6 +34,8 @@ drafter and verifier outputs):
   row at k_b is a fresh s'*N(0,1) row.  Draft lengths k_b come from the
   draft-length step on the device, so targets and uniforms are produced padded
   ``[B, k_max+1, V]`` (bonus row stored at slot k_max) and packed afterwards.
+* ``v152k``: a sweep point, not one of the five: B=64, k_max=8, V=152064 (the top
+  of the metric's vocabulary range), bf16, with c2's row recipe.
 
 Uniforms are ``randint(0, 2^24) * 2^-24`` as fp32: exactly representable and
 strictly below 1.  Drafted ids (except ``tiny``) are exact samples from the
@@ -75,6 +77,11 @@ class Config:
     V: int
     dtype: str          # "f32" or "bf16"
     ragged: bool = False
+    style: str = ""     # row recipe of another config (a sweep point), else the config's own
+
+    @property
+    def kind(self) -> str:
+        return self.style or self.name
 
     @property
     def draft_rows(self) -> int:
@@ -95,6 +102,8 @@ CONFIGS = {
     "c3": Config("c3", 2, 64, 8, 50257, "bf16"),
     "c4": Config("c4", 3, 256, 16, 128256, "bf16"),
     "c5": Config("c5", 4, 512, 16, 32000, "bf16", ragged=True),
+    # sweep point at the top of the metric's vocabulary range, with c2's row recipe
+    "v152k": Config("v152k", 5, 64, 8, 152064, "bf16", style="c2"),
 }
 
 
@@ -182,20 +191,20 @@ def _draft_row_f64(cfg: Config, seed: int, row: int) -> np.ndarray:
     """Unrounded drafter row ``row`` (= b*k_max + i) as float64."""
     V = cfg.V
     g = _rng(cfg, seed, _S_DRAFT_ROW, row)
-    if cfg.name == "tiny":
+    if cfg.kind == "tiny":
         s = (0.5, 2.0, 8.0, 0.5)[row % 4]
         return s * g.standard_normal(V)
-    if cfg.name in ("c2", "c5"):
+    if cfg.kind in ("c2", "c5"):
         s = math.exp(g.uniform(math.log(0.3), math.log(10.0)))
         return s * g.standard_normal(V, dtype=np.float32).astype(np.float64)
-    if cfg.name == "c3":
+    if cfg.kind == "c3":
         a = g.uniform(0.5, 3.0)
         perm = g.permutation(V)
         return _zipf_row(V, perm, a, 0.2 * g.standard_normal(V, dtype=np.float32).astype(np.float64))
-    if cfg.name == "c4":
+    if cfg.kind == "c4":
         reg = _c4_regime(cfg, seed, row)
         return _c4_regime_row(V, reg, g)
-    raise KeyError(cfg.name)
+    raise KeyError(cfg.kind)
 
 
 def _c4_regime_row(V: int, reg: int, g: np.random.Generator) -> np.ndarray:
@@ -232,7 +241,7 @@ def target_row(cfg: Config, seed: int, b: int, i: int, draft_stored: np.ndarray 
     """
     V, K = cfg.V, cfg.k_max
     bonus = i == K
-    if cfg.name == "tiny":
+    if cfg.kind == "tiny":
         g = _rng(cfg, seed, _S_TARGET_ROW, b * (K + 1) + i)
         if bonus:
             return _store(cfg, 2.0 * g.standard_normal(V))
@@ -240,32 +249,32 @@ def target_row(cfg: Config, seed: int, b: int, i: int, draft_stored: np.ndarray 
         return _store(cfg, d.astype(np.float64) + 0.5 * g.standard_normal(V))
     if bonus:
         g = _rng(cfg, seed, _S_BONUS_ROW, b)
-        if cfg.name in ("c2", "c5"):
+        if cfg.kind in ("c2", "c5"):
             s = math.exp(g.uniform(math.log(0.3), math.log(10.0)))
             return _store(cfg, s * g.standard_normal(V, dtype=np.float32).astype(np.float64))
-        if cfg.name == "c3":
+        if cfg.kind == "c3":
             a = g.uniform(0.5, 3.0)
             perm = g.permutation(V)
             return _store(cfg, _zipf_row(V, perm, a, 0.2 * g.standard_normal(V, dtype=np.float32).astype(np.float64)))
-        if cfg.name == "c4":
+        if cfg.kind == "c4":
             reg = _c4_regime(cfg, seed, b * K + K - 1)
             return _store(cfg, _c4_regime_row(V, reg, g))
-        raise KeyError(cfg.name)
+        raise KeyError(cfg.kind)
     row = b * K + i
     g = _rng(cfg, seed, _S_TARGET_ROW, b * (K + 1) + i)
-    if cfg.name == "c3":
+    if cfg.kind == "c3":
         a, perm = _c3_params(cfg, seed, row)
         if (b * (K + 1) + i) in _c3_indep_rows(cfg, seed):
             perm = g.permutation(V)
         return _store(cfg, _zipf_row(V, perm, a, 0.2 * g.standard_normal(V, dtype=np.float32).astype(np.float64)))
     d = _stored_as_f32(cfg, draft_stored if draft_stored is not None else draft_row(cfg, seed, row)).astype(np.float64)
-    if cfg.name == "c2":
+    if cfg.kind == "c2":
         n1 = g.standard_normal(V, dtype=np.float32).astype(np.float64)
         n2 = g.standard_normal(V, dtype=np.float32).astype(np.float64)
         return _store(cfg, d * (1.0 + 0.1 * n1) + 0.3 * n2)
-    if cfg.name in ("c4", "c5"):
+    if cfg.kind in ("c4", "c5"):
         return _store(cfg, d + 0.5 * g.standard_normal(V, dtype=np.float32).astype(np.float64))
-    raise KeyError(cfg.name)
+    raise KeyError(cfg.kind)
 
 
 def drafted_id(cfg: Config, seed: int, row: int, draft_stored: np.ndarray | None = None) -> int:
@@ -276,7 +285,7 @@ def drafted_id(cfg: Config, seed: int, row: int, draft_stored: np.ndarray | None
     """
     d = draft_stored if draft_stored is not None else draft_row(cfg, seed, row)
     z = _stored_as_f32(cfg, d).astype(np.float64)
-    if cfg.name == "tiny":
+    if cfg.kind == "tiny":
         return int(np.argmax(z))
     g = _rng(cfg, seed, _S_GUMBEL, row)
     u = g.random(cfg.V)                      # [0, 1)
@@ -317,9 +326,9 @@ def generate(cfg: Config | str, seed: int = 0, threads: int | None = None) -> di
     target = np.empty((B * (K + 1), V), dtype=st)
     drafted = np.empty((B, K), dtype=np.int32)
     unif = np.empty((B, K + 1), dtype=np.float32)
-    if cfg.name == "c4":
+    if cfg.kind == "c4":
         _c4_perm_cache(cfg, seed)
-    if cfg.name == "c3":
+    if cfg.kind == "c3":
         _c3_indep_rows(cfg, seed)
     _log_rank(V)
 
