@@ -177,3 +177,32 @@ def test_logit_variance_config_rows(cm, name, nsample):
     var = var.cpu().numpy()
     for r in _sample_rows(cfg, nsample):
         _check_var(float(var[r]), O.logit_variance(Hn.decode(d["draft"][r], cfg.dtype)), (name, r))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_many_short_rows(cm, dtype):
+    # more rows than the chip holds workgroups at once (one-wave groups); odd V and a
+    # padded stride make consecutive rows start at different alignments
+    g = np.random.default_rng(77)
+    n, V, pad = 20011, 37, 3
+    z = g.normal(0, 2, (n, V))
+    z[::7, ::5] = -math.inf                       # masked entries on some rows
+    z[::11, 4] = z[::11].max(axis=1) + 1.0         # a clear max on others
+    z[::13, 9] = z[::13, 4]                        # ties with it
+    stored = _store(list(z), dtype)
+    buf = np.zeros((n, V + pad), dtype=stored.dtype)
+    buf[:, :V] = stored
+    tdev = Hn.to_device(buf, dtype, torch.device("cuda:0"))[:, :V]
+    st, var = cm.cmsd_confidence_var(tdev, lambdas=(0.2, 0.5, 0.3), beta_margin=0.7)
+    st0 = cm.cmsd_confidence(tdev, lambdas=(0.2, 0.5, 0.3), beta_margin=0.7)
+    torch.cuda.synchronize()
+    assert torch.equal(st.view(torch.int32), st0.view(torch.int32))
+    gs = Hn.stats_np(st)
+    var = var.cpu().numpy()
+    t = Hn.Tally()
+    lam32 = tuple(Hn.f32(x) for x in (0.2, 0.5, 0.3))
+    for r in range(0, n, 3):
+        zr = Hn.decode(stored[r], dtype)
+        Hn.check_row_stats(t, gs, r, zr, V, lam32, Hn.f32(0.7))
+        _check_var(float(var[r]), O.logit_variance(zr), r)
+    t.assert_ok()
