@@ -255,7 +255,7 @@ size_t cmsd_draft_sample_workspace_bytes(int64_t n_rows, int64_t vocab);
 /* Human-readable name of a status code (static string). */
 const char* cmsd_status_string(cmsd_status s);
 
-/* Library ABI version, (major << 16) | minor. */
+/* Library ABI version, (major << 16) | minor: 1.2 (1.1 plus cmsd_confidence_var). */
 int32_t cmsd_version(void);
 
 #ifdef __cplusplus

@@ -1556,7 +1556,7 @@ const char* cmsd_status_string(cmsd_status s) {
   return "unknown status";
 }
 
-int32_t cmsd_version(void) { return (1 << 16) | 1; }
+int32_t cmsd_version(void) { return (1 << 16) | 2; }
 
 size_t cmsd_draft_sample_workspace_bytes(int64_t n_rows, int64_t vocab) {
   if (n_rows <= 0 || n_rows > INT32_MAX || vocab < 2 || vocab > INT32_MAX) return 0;

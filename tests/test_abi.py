@@ -12,13 +12,14 @@ P = 0x10000          # fake, aligned device addresses: never dereferenced on the
 
 def test_exports_every_declared_symbol():
     syms = cm.header_symbols()
-    assert set(syms) >= {"cmsd_confidence", "cmsd_draft_len", "cmsd_verify", "cmsd_verify_workspace_bytes",
+    assert set(syms) >= {"cmsd_confidence", "cmsd_confidence_var", "cmsd_draft_len", "cmsd_verify",
+                         "cmsd_verify_workspace_bytes",
                          "cmsd_draft_sample", "cmsd_draft_sample_workspace_bytes", "cmsd_status_string",
                          "cmsd_version"}
     lib = cm.lib()
     for s in syms:
         assert hasattr(lib, s), s
-    assert lib.cmsd_version() >> 16 == 1
+    assert lib.cmsd_version() == (1 << 16) | 2
     assert lib.cmsd_status_string(0) == b"ok"
     assert lib.cmsd_status_string(1) == b"invalid argument"
 
