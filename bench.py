@@ -28,7 +28,7 @@ PEAK_HBM_GBS = 8000.0   # MI355X HBM3E
 # --pmc runs (FETCH_SIZE, WRITE_SIZE) scaled by what the same counters read for a
 # 1 GiB device copy (x2.0 and x1.0).  Valid only for the kernel source they were
 # taken on (sha256 prefix of the .hip file); otherwise "traffic" is reported null.
-TRAFFIC = {"kernel_sha256_16": "f2f981b7409ec2b8", "k_confidence_c4": 1052.89e6 + 0.131e6,
+TRAFFIC = {"kernel_sha256_16": "a0f3997e76f880ba", "k_confidence_c4": 1052.89e6 + 0.131e6,
            "profile": "profiles/c4_cm_logit_pass.md"}
 
 
