@@ -13,6 +13,9 @@
  *                    accepted-prefix length, and the final token sampled from
  *                    the residual (or bonus) distribution     (Sec. III.A, III.B(c))
  *
+ * cmsd_logit_pass does all three in one call (three launches) for a dense target
+ * layout.
+ *
  * Conventions shared by every call
  *   - All array pointers are DEVICE pointers (hipMalloc / torch CUDA tensors);
  *     params structs are HOST pointers read during the call.  The caller owns
@@ -222,6 +225,58 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
                         int32_t* n_accepted, int32_t* next_token, void* workspace, size_t workspace_bytes,
                         void* stream);
 
+/*
+ * cmsd_logit_pass - the whole logit pass of one decoding iteration in one call, for
+ * a dense target layout: cmsd_confidence on the drafter rows, cmsd_draft_len's draft
+ * length and cmsd_verify on target rows stored k_max + 1 per sequence (Sec. III.B(1)
+ * to (c), Sec. III.A), in three launches instead of five: one row pass over the
+ * drafter and target rows together (they do not depend on each other), then the
+ * final-token pass, which also makes the accept tests and forms the draft length.
+ *
+ *   draft_logits    device, batch*k_max drafter rows (row b*k_max+i), stride
+ *                   draft_stride >= vocab elements.
+ *   target_logits   device, batch*(k_max+1) target rows, stride target_stride >=
+ *                   vocab: row b*(k_max+1)+i scores position i, the last row of each
+ *                   sequence is the row after its final draft.
+ *   drafted         device, batch*k_max int32 token ids; all k_max of a sequence must
+ *                   lie in [0, vocab), else the sequence is reported invalid.
+ *   uniforms        device, batch*(k_max+1) floats in [0,1), slot b*(k_max+1)+i:
+ *                   slot i < k_v the accept test of position i, slot k_v the final
+ *                   sample (k_v below).  Unused (may be NULL) in CMSD_MODE_GREEDY.
+ *   dtype           logit dtype of both logit arrays.
+ *   batch >= 0 (0: nothing is enqueued); k_max in [1, 63]; vocab in [2, 2^31).
+ *   conf, draft, verify  host; as for the separate calls (draft->k_max == k_max).
+ *   adaptive        0: all k_max drafts are verified (k_v = k_max), as cmsd_verify with
+ *                   draft_len[b] = k_max and dense offsets; 1: only the first k_b, the
+ *                   draft length computed here (k_v = k_b), and target row k_b is the
+ *                   final row.
+ *   draft_stats     device, batch*k_max records (output), as cmsd_confidence writes.
+ *   draft_len       device, batch int32 (output): k_b, as cmsd_draft_len computes it
+ *                   (no packed offsets are formed: the layout is dense).
+ *   target_stats    device, batch*(k_max+1) records (output): row i < k_v holds the
+ *                   accept test of position i and row k_v has n_greater = accept = -1,
+ *                   as cmsd_verify writes them; in adaptive mode rows k_b+1 .. k_max
+ *                   hold the tests of the positions beyond the draft, made all the same.
+ *   n_accepted      device, batch int32 (output): accepted prefix c_b in [0, k_v];
+ *                   -1 when a drafted id of the sequence is outside [0, vocab).
+ *   next_token      device, batch int32 (output): the final token; -1 when invalid.
+ *   workspace       device scratch of at least cmsd_verify_workspace_bytes(batch,
+ *                   k_max, vocab) bytes, 8-byte aligned, owned by the caller, as for
+ *                   cmsd_verify (calls sharing it must be ordered).
+ *   workspace_bytes its size.
+ * The arithmetic is the separate calls': the outputs are bit-identical to theirs
+ * whenever the row kernels run with the same workgroup size (chosen from the number
+ * of rows in the launch), else equal up to the rounding of the reduction order.
+ * Errors: CMSD_ERR_ARG, CMSD_ERR_DTYPE, CMSD_ERR_LAUNCH.
+ */
+cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, const void* target_logits,
+                            int64_t target_stride, const int32_t* drafted, const float* uniforms,
+                            int32_t dtype, int32_t batch, int32_t k_max, int64_t vocab,
+                            const cmsd_conf_params* conf, const cmsd_draft_params* draft,
+                            const cmsd_verify_params* verify, int32_t adaptive, cmsd_row_stats* draft_stats,
+                            int32_t* draft_len, cmsd_target_stats* target_stats, int32_t* n_accepted,
+                            int32_t* next_token, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Workspace cmsd_verify needs for `batch` sequences of up to `k_max` drafts over
  * `vocab`: per sequence, one 32-byte record per vocabulary slice (256 16-byte
  * vectors of a row) and one 32-byte record per target row position (k_max + 1);
@@ -255,7 +310,7 @@ size_t cmsd_draft_sample_workspace_bytes(int64_t n_rows, int64_t vocab);
 /* Human-readable name of a status code (static string). */
 const char* cmsd_status_string(cmsd_status s);
 
-/* Library ABI version, (major << 16) | minor: 1.2 (1.1 plus cmsd_confidence_var). */
+/* Library ABI version, (major << 16) | minor: 1.3 (1.2 plus cmsd_logit_pass). */
 int32_t cmsd_version(void);
 
 #ifdef __cplusplus

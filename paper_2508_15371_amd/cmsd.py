@@ -65,6 +65,10 @@ def _load() -> C.CDLL:
     lib.cmsd_draft_sample.restype = C.c_int
     lib.cmsd_draft_sample_workspace_bytes.argtypes = [i64, i64]
     lib.cmsd_draft_sample_workspace_bytes.restype = C.c_size_t
+    lib.cmsd_logit_pass.argtypes = [vp, i64, vp, i64, vp, vp, i32, i32, i32, i64, C.POINTER(ConfParams),
+                                    C.POINTER(DraftParams), C.POINTER(VerifyParams), i32, vp, vp, vp, vp, vp, vp,
+                                    C.c_size_t, vp]
+    lib.cmsd_logit_pass.restype = C.c_int
     lib.cmsd_status_string.argtypes = [C.c_int]
     lib.cmsd_status_string.restype = C.c_char_p
     lib.cmsd_version.argtypes = []
@@ -274,3 +278,63 @@ def cmsd_draft_sample(logits: torch.Tensor, stats: torch.Tensor, uniforms: torch
         _ptr(logits), _dtype_code(logits), n, V, st, _ptr(stats), _ptr(uniforms), _ptr(drafted), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
     return drafted
+
+
+def cmsd_logit_pass(draft_logits: torch.Tensor, target_logits: torch.Tensor, drafted: torch.Tensor,
+                    uniforms: torch.Tensor | None, *, batch: int, k_max: int, lambdas=(1 / 3, 1 / 3, 1 / 3),
+                    beta_margin: float = 1.0, k_min: int = 1, alpha: float = 1.0, mode: int = CMSD_MODE_CM,
+                    top_beta: int = 3, tau_base: float = 0.1, gamma: float = 1.0, adaptive: bool = False,
+                    draft_stats: torch.Tensor | None = None, draft_len: torch.Tensor | None = None,
+                    target_stats: torch.Tensor | None = None, n_accepted: torch.Tensor | None = None,
+                    next_token: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                    stream=None) -> dict:
+    """Confidence, draft length and verification of a dense draft in one call.
+    ``draft_logits`` [batch*k_max, V], ``target_logits`` [batch*(k_max+1), V] (same
+    dtype), ``drafted`` int32 [batch*k_max], ``uniforms`` float32 [batch*(k_max+1)]
+    (None in GREEDY mode).  Returns the output tensors by name."""
+    drows, V, dst = _rows(draft_logits, "draft_logits")
+    trows, V2, tst = _rows(target_logits, "target_logits")
+    if V2 != V or target_logits.dtype != draft_logits.dtype:
+        raise ValueError("draft and target logits must share vocab size and dtype")
+    if drows < batch * k_max:
+        raise ValueError(f"draft_logits has {drows} rows; batch*k_max = {batch * k_max} are needed")
+    if trows < batch * (k_max + 1):
+        raise ValueError(f"target_logits has {trows} rows; batch*(k_max+1) = {batch * (k_max + 1)} are needed")
+    dev = target_logits.device
+    if draft_logits.device != dev:
+        raise ValueError("draft and target logits must be on one device")
+    nt = batch * (k_max + 1)
+    out = {"draft_stats": draft_stats, "draft_len": draft_len, "target_stats": target_stats,
+           "n_accepted": n_accepted, "next_token": next_token}
+    shapes = {"draft_stats": ((batch * k_max, 8), torch.float32), "draft_len": ((batch,), torch.int32),
+              "target_stats": ((nt, 8), torch.float32), "n_accepted": ((batch,), torch.int32),
+              "next_token": ((batch,), torch.int32)}
+    for k, (shape, dt) in shapes.items():
+        if out[k] is None:
+            out[k] = torch.empty(shape, dtype=dt, device=dev)
+    for name, t, dt, n in (("drafted", drafted, torch.int32, batch * k_max),
+                           ("uniforms", uniforms, torch.float32, nt),
+                           ("draft_stats", out["draft_stats"], torch.float32, 8 * batch * k_max),
+                           ("draft_len", out["draft_len"], torch.int32, batch),
+                           ("target_stats", out["target_stats"], torch.float32, 8 * nt),
+                           ("n_accepted", out["n_accepted"], torch.int32, batch),
+                           ("next_token", out["next_token"], torch.int32, batch)):
+        if t is None and name == "uniforms":
+            continue
+        _buf(t, name, dt, n, dev)
+    if workspace is None:
+        workspace = verify_workspace(batch, k_max, V, dev)
+    if workspace.dtype != torch.float64 or not workspace.is_contiguous() or workspace.device != dev:
+        raise ValueError(f"workspace must be a contiguous float64 tensor on {dev}")
+    out["workspace"] = workspace
+    cp = ConfParams(float(lambdas[0]), float(lambdas[1]), float(lambdas[2]), float(beta_margin))
+    dp = DraftParams(int(k_min), int(k_max), float(alpha))
+    vp_ = VerifyParams(int(mode), int(top_beta), float(tau_base), float(gamma))
+    _on_device(target_logits, "target_logits")
+    _check("cmsd_logit_pass", _lib.cmsd_logit_pass(
+        _ptr(draft_logits), dst, _ptr(target_logits), tst, _ptr(drafted), _ptr(uniforms),
+        _dtype_code(target_logits), int(batch), int(k_max), V, C.byref(cp), C.byref(dp), C.byref(vp_),
+        1 if adaptive else 0, _ptr(out["draft_stats"]), _ptr(out["draft_len"]), _ptr(out["target_stats"]),
+        _ptr(out["n_accepted"]), _ptr(out["next_token"]), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+    return out

@@ -401,10 +401,40 @@ struct ConfArgs {
   double lnV;  // ln(vocab)
 };
 
+// The drafter-row record from the row's reductions: max m, second value z2 (the
+// largest value other than the first occurrence of m; -inf with one finite logit),
+// A = sum 2^(z log2e - m log2e) and T = sum of 2^x x over the same terms.
+__device__ __forceinline__ cmsd_row_stats row_stats_record(float m, float z2, double A, double Tsum, uint32_t flags,
+                                                           int top1, int64_t V, const ConfArgs& a) {
+  const double Vd = (double)V;
+  const double Tn = Tsum * kLn2;
+  double H = (double)log1pf((float)(A - 1.0)) - Tn / A;  // ln A = log1p(A - 1), A - 1 exact in fp64
+  H = H < 0.0 ? 0.0 : H;
+  const double dm = (double)m, dz2 = (double)z2;
+  const double margin = z2 == -INFINITY ? INFINITY : dm - dz2;
+  const double msoft = z2 == -INFINITY ? 1.0 / A : (double)(-expm1f((float)(dz2 - dm))) / A;
+  const double c_ent = 1.0 - H / a.lnV;
+  const double tm = (double)a.beta_m * margin;
+  const double c_m = tm == INFINITY ? 1.0 : 1.0 / (1.0 + (double)expf((float)-tm));
+  const double c_s = fmin(1.0, msoft / (1.0 - 1.0 / Vd));
+  const double C = (double)a.l_ent * c_ent + (double)a.l_margin * c_m + (double)a.l_soft * c_s;
+  cmsd_row_stats o;
+  o.max_logit = m;
+  o.sum_exp = (float)A;
+  o.entropy = (float)H;
+  o.margin_soft = (float)msoft;
+  o.margin_logit = (float)margin;
+  o.conf = (float)C;
+  o.top1 = top1;
+  o.flags = flags;
+  return o;
+}
+
+// One drafter row -> its stats record (and, with VAR, its logit variance), by one
+// workgroup of BD threads.
 template <typename T, int BD, bool VAR>
-__global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits, int64_t n_rows, int64_t V,
-                                                   int64_t stride, ConfArgs a, cmsd_row_stats* __restrict__ out,
-                                                   float* __restrict__ var_out) {
+__device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, const ConfArgs& a,
+                                         cmsd_row_stats* __restrict__ out, float* __restrict__ var_out) {
   using E = Elem<T>;
   constexpr int VEC = E::VEC, U = E::U, N = VEC * U;
   constexpr int ND = VAR ? 5 : 2;  // fp64 sums of the epilogue: A, T (+ count, S1, S2)
@@ -414,9 +444,7 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
   __shared__ float ep_f[2][BD / 64];
   __shared__ int ep_i[2][BD / 64];
   const int t = threadIdx.x;
-
-  for (int64_t r = blockIdx.x; r < n_rows; r += gridDim.x) {
-    const T* row = logits + r * stride;
+  {
     const Geom g = row_geom(row, V);
     const uint4* vp = reinterpret_cast<const uint4*>(row + g.head);
     const int64_t per_round = (int64_t)U * BD;
@@ -493,7 +521,7 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
         const int w = t >> 6;
         ep_d[0][w] = wA;
         ep_d[1][w] = wT;
-        if (VAR) {
+        if constexpr (VAR) {
           ep_d[ND - 3][w] = wN;
           ep_d[ND - 2][w] = wS1;
           ep_d[ND - 1][w] = wS2;
@@ -510,7 +538,7 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
       s_oth = ep_f[1][0];
       nmax = ep_i[0][0];
       top1 = ep_i[1][0];
-      if (VAR) {
+      if constexpr (VAR) {
         vN = ep_d[ND - 3][0];
         vS1 = ep_d[ND - 2][0];
         vS2 = ep_d[ND - 1][0];
@@ -519,7 +547,7 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
       for (int w = 1; w < BD / 64; ++w) {
         A += ep_d[0][w];
         Tsum += ep_d[1][w];
-        if (VAR) {
+        if constexpr (VAR) {
           vN += ep_d[ND - 3][w];
           vS1 += ep_d[ND - 2][w];
           vS2 += ep_d[ND - 1][w];
@@ -568,36 +596,22 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
     }
     __syncthreads();
     if (t == 0) {
-      const float z2 = nmax >= 2 ? m : fmaxf(cmx, s_oth);
-      const double Vd = (double)V;
-      const double Tn = Tsum * kLn2;
-      double H = (double)log1pf((float)(A - 1.0)) - Tn / A;  // ln A = log1p(A - 1), A - 1 exact in fp64
-      H = H < 0.0 ? 0.0 : H;
-      const double dm = (double)m, dz2 = (double)z2;
-      const double margin = z2 == -INFINITY ? INFINITY : dm - dz2;
-      const double msoft = z2 == -INFINITY ? 1.0 / A : (double)(-expm1f((float)(dz2 - dm))) / A;
-      const double c_ent = 1.0 - H / a.lnV;
-      const double tm = (double)a.beta_m * margin;
-      const double c_m = tm == INFINITY ? 1.0 : 1.0 / (1.0 + (double)expf((float)-tm));
-      const double c_s = fmin(1.0, msoft / (1.0 - 1.0 / Vd));
-      const double C = (double)a.l_ent * c_ent + (double)a.l_margin * c_m + (double)a.l_soft * c_s;
-      cmsd_row_stats o;
-      o.max_logit = m;
-      o.sum_exp = (float)A;
-      o.entropy = (float)H;
-      o.margin_soft = (float)msoft;
-      o.margin_logit = (float)margin;
-      o.conf = (float)C;
-      o.top1 = top1;
-      o.flags = flags;
-      out[r] = o;
+      *out = row_stats_record(m, nmax >= 2 ? m : fmaxf(cmx, s_oth), A, Tsum, flags, top1, V, a);
       if (VAR) {
         const double v = (vS2 - vS1 * (vS1 / vN)) / vN;
-        var_out[r] = (float)(v > 0.0 ? v : 0.0);
+        *var_out = (float)(v > 0.0 ? v : 0.0);
       }
     }
     __syncthreads();
   }
+}
+
+template <typename T, int BD, bool VAR>
+__global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits, int64_t n_rows, int64_t V,
+                                                   int64_t stride, ConfArgs a, cmsd_row_stats* __restrict__ out,
+                                                   float* __restrict__ var_out) {
+  for (int64_t r = blockIdx.x; r < n_rows; r += gridDim.x)
+    conf_row<T, BD, VAR>(logits + r * stride, V, a, out + r, VAR ? var_out + r : nullptr);
 }
 
 // ----------------------------------------------------------------------------- K2 draft length
@@ -675,6 +689,26 @@ struct VerifyArgs {
   int32_t* n_acc;
   int32_t* next_tok;
   struct RowSlot* slots;  // workspace: [B][k_max+1], by sequence and position
+  // the single-call pass (cmsd_logit_pass): dense rows, draft length and decisions made
+  // from the row results by the final-token kernels
+  struct PassSlot* pslots;  // workspace: [B][k_max+1]
+  cmsd_row_stats* dstats_out;
+  ConfArgs ca;
+  int32_t* klen_out;
+  int k_min;
+  float alpha;
+  int adaptive;
+};
+
+// Target-row results of the single-call pass by (sequence, position): everything the
+// accept test of the position needs from the target row.
+struct PassSlot {
+  double A;       // sum 2^(z log2e - m log2e) of the row
+  float m;        // row max
+  float gz, zd;   // target and drafter logits of the drafted token
+  int32_t ngt;    // logits above gz seen (wave counts stop once one reaches top_beta)
+  int32_t top1;   // lowest index of the row max (GREEDY mode), else -1
+  int32_t st;     // 1 drafted position, -1 the row after the last draft, -2 invalid drafted id
 };
 
 // Target-row results by (sequence, position), so the final-token pass reads a whole
@@ -758,16 +792,43 @@ __device__ __forceinline__ void target_stream(const T* row, const Geom& g, const
   }
 }
 
-template <typename T, int BD>
-__global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
+// The accept test of one drafted position y: standard speculative sampling
+// u < p_t(y) / p_d(y) in logs and fp64 (Sec. III.A), or in CM mode the
+// confidence-modulated gate: fewer than top_beta target logits above z_t[y] and
+// gap m_t - z_t[y] <= tau_base + gamma (1 - C) (Sec. III.B(c)).  GREEDY mode accepts
+// the target's top token, or what the gate passes.  `count` says whether the gate's
+// rank count was taken; *ng receives the reported count.
+__device__ __forceinline__ int accept_test(int mode, int beta, float tau_base, float gamma, bool count, int ngt,
+                                           float gz, float zd, float m, double A, float dm, float dA, float cm,
+                                           float u, int yd, int top1, int* ng) {
+  const double lpt = gz == -INFINITY ? -INFINITY : ((double)gz - (double)m) - log(A);
+  const double lpd = zd == -INFINITY ? -INFINITY : ((double)zd - (double)dm) - log((double)dA);
+  bool stoch;
+  if (lpt == -INFINITY) stoch = false;
+  else if (u == 0.f || lpd == -INFINITY) stoch = true;
+  else stoch = log((double)u) < lpt - lpd;
+  *ng = count ? (ngt < beta ? ngt : beta) : 0;
+  const double gap = gz == -INFINITY ? INFINITY : (double)m - (double)gz;
+  const double tau = (double)tau_base + (double)gamma * (1.0 - (double)cm);
+  const bool gate = count && ngt < beta && gap <= tau;
+  if (mode == CMSD_MODE_GREEDY) return (yd == top1 || gate) ? 1 : 0;  // the paper's rule, relaxed by the gate
+  return (stoch || (mode == CMSD_MODE_CM && gate)) ? 1 : 0;
+}
+
+// One target row.  PASS = false: a packed row of cmsd_verify (sequence found from the
+// offsets, accept test made here).  PASS = true: dense row r = b*(k_max+1) + i of the
+// single-call pass, whose accept test waits for the drafter stats (PassSlot).
+template <typename T, int BD, bool PASS>
+__device__ __forceinline__ void target_row(const VerifyArgs& a, int64_t r) {
   using E = Elem<T>;
   __shared__ double sd[BD / 64];
   __shared__ float sf[BD / 64];
   __shared__ int si[BD / 64];
   const int t = threadIdx.x;
-  const int64_t r = blockIdx.x;
-  const int total = a.off[a.B];
-  if (r >= total || r >= a.target_rows) return;
+  if (!PASS) {
+    const int total = a.off[a.B];
+    if (r >= total || r >= a.target_rows) return;
+  }
   const T* trow = reinterpret_cast<const T*>(a.target) + r * a.tstride;
   const Geom g = row_geom(trow, a.V);
 
@@ -776,6 +837,27 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
   int b = 0, i = 0, yd = -1;
   float gz = -INFINITY, zd = -INFINITY, cm = 0.f, dm = 0.f, dA = 1.f;
   auto prep = [&] {
+    if (PASS) {
+      b = int(r / (a.k_max + 1));
+      i = int(r - (int64_t)b * (a.k_max + 1));
+      layout = true;
+      valid = true;
+      has_draft = i < a.k_max;
+      if (has_draft) {
+        const int64_t drow = (int64_t)b * a.k_max + i;
+        const int y = a.drafted[drow];
+        yd = y;
+        if (y < 0 || (int64_t)y >= a.V) {
+          valid = false;
+          has_draft = false;
+        } else {
+          gz = E::load(trow + y);
+          zd = E::load(reinterpret_cast<const T*>(a.draft) + drow * a.dstride + y);
+        }
+      }
+      count = has_draft && a.mode != CMSD_MODE_STANDARD && a.beta > 0;
+      return;
+    }
     // sequence owning row r: number of offsets[1..B] that are <= r
     int cnt = 0;
     for (int j = 1 + t; j <= a.B; j += BD) cnt += a.off[j] <= r ? 1 : 0;
@@ -842,7 +924,9 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
       ngt += si[w];
     }
   }
-  if (t == 0) {
+  if (t == 0 && PASS) {
+    a.pslots[r] = PassSlot{A, m, gz, zd, ngt, top1, !valid ? -2 : (has_draft ? 1 : -1)};
+  } else if (t == 0) {
     cmsd_target_stats res{};
     res.max_logit = m;
     res.sum_exp = (float)A;
@@ -853,28 +937,30 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
       res.n_greater = -1;
       res.accept = -1;
     } else {
-      // standard speculative sampling: u < p_t(y) / p_d(y), in logs and fp64
-      const double lpt = gz == -INFINITY ? -INFINITY : ((double)gz - (double)m) - log(A);
-      const double lpd = zd == -INFINITY ? -INFINITY : ((double)zd - (double)dm) - log((double)dA);
       const float u = a.mode == CMSD_MODE_GREEDY ? 0.f : a.unif[r];
-      bool stoch;
-      if (lpt == -INFINITY) stoch = false;
-      else if (u == 0.f || lpd == -INFINITY) stoch = true;
-      else stoch = log((double)u) < lpt - lpd;
-      // confidence-modulated gate: top-beta inclusion and gap <= tau_base + gamma (1 - C)
-      const int ng = count ? (ngt < a.beta ? ngt : a.beta) : 0;
-      const double gap = gz == -INFINITY ? INFINITY : (double)m - (double)gz;
-      const double tau = (double)a.tau_base + (double)a.gamma * (1.0 - (double)cm);
-      const bool gate = count && ngt < a.beta && gap <= tau;
-      res.n_greater = ng;
-      if (a.mode == CMSD_MODE_GREEDY)
-        res.accept = (yd == top1 || gate) ? 1 : 0;  // the paper's deterministic rule, relaxed by the gate
-      else
-        res.accept = (stoch || (a.mode == CMSD_MODE_CM && gate)) ? 1 : 0;
+      res.accept = accept_test(a.mode, a.beta, a.tau_base, a.gamma, count, ngt, gz, zd, m, A, dm, dA, cm, u, yd,
+                               top1, &res.n_greater);
     }
     a.tstats[r] = res;
     if (layout) a.slots[(int64_t)b * (a.k_max + 1) + i] = RowSlot{m, (float)A, res.accept, (int32_t)r, top1, {0, 0, 0}};
   }
+}
+
+template <typename T, int BD>
+__global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
+  target_row<T, BD, false>(a, blockIdx.x);
+}
+
+// The row pass of cmsd_logit_pass: drafter rows (stats) and dense target rows in one
+// grid, drafter rows first; the two kinds of row do not depend on each other.
+template <typename T, int BD>
+__global__ __launch_bounds__(BD) void k_row_pass(VerifyArgs a) {
+  const int64_t nd = (int64_t)a.B * a.k_max;
+  const int64_t r = blockIdx.x;
+  if (r < nd)
+    conf_row<T, BD, false>(reinterpret_cast<const T*>(a.draft) + r * a.dstride, a.V, a.ca, a.dstats_out + r, nullptr);
+  else
+    target_row<T, BD, true>(a, r - nd);
 }
 
 // ----------------------------------------------------------------------------- K4 final token
@@ -1046,6 +1132,82 @@ __device__ __forceinline__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo*
   return r;
 }
 
+// seq_info of the single-call pass: wave 0 reads the sequence's row results, drafter
+// stats, drafted ids and uniforms (one round trip, k_max < 64), forms the draft length
+// and every accept test (as the separate calls would), and with WRITE (the final
+// kernel) stores the draft length and the target-row records.
+template <bool WRITE>
+__device__ __forceinline__ SeqInfo seq_info_pass(const VerifyArgs& a, int b, SeqInfo* lds) {
+  const int t = threadIdx.x, lane = t & 63;
+  if (t < 64) {
+    const int K = a.k_max;
+    const bool greedy = a.mode == CMSD_MODE_GREEDY;
+    const int64_t off = (int64_t)b * (K + 1);
+    const PassSlot sl = lane <= K ? a.pslots[off + lane] : PassSlot{1.0, 0.f, -INFINITY, -INFINITY, 0, -1, -1};
+    float dmx = 0.f, dA = 1.f, cf = 0.f, u = 0.f;
+    int y = -1;
+    if (lane < K) {
+      const cmsd_row_stats ds = a.dstats[(int64_t)b * K + lane];
+      dmx = ds.max_logit;
+      dA = ds.sum_exp;
+      cf = ds.conf;
+      y = a.drafted[(int64_t)b * K + lane];
+      if (!greedy) u = a.unif[off + lane];
+    }
+    // draft length from the confidences, summed in position order in fp64
+    double csum = 0.0;
+    for (int j = 0; j < K; ++j) csum += (double)rl_f(cf, j);
+    const double x = (double)a.alpha * (csum / (double)K) * (double)K;
+    const double fl = floor(x);
+    const int kb = fl < (double)a.k_min ? a.k_min : (fl > (double)K ? K : (int)fl);
+    const int kv = a.adaptive ? kb : K;
+    const bool count = a.mode != CMSD_MODE_STANDARD && a.beta > 0;
+    int ng = 0, acc = -1;
+    if (lane < K && sl.st == 1)
+      acc = accept_test(a.mode, a.beta, a.tau_base, a.gamma, count, sl.ngt, sl.gz, sl.zd, sl.m, sl.A, dmx, dA, cf,
+                        u, y, sl.top1, &ng);
+    const bool bad = __ballot(lane < K && sl.st == -2) != 0ull;
+    const unsigned long long rej = __ballot(lane < kv && acc == 0);
+    const int c = rej ? __builtin_ctzll(rej) : kv;
+    SeqInfo q{};
+    q.nacc = bad ? -1 : c;
+    q.kb = kv;
+    q.off = off;
+    q.tr = off + c;
+    q.dr = (int64_t)b * K + (c < kv ? c : 0);
+    q.mst = rl_f(sl.m, c) * kLog2e;
+    q.top1 = __builtin_amdgcn_readlane(sl.top1, c);
+    if (c < kv) {
+      q.msd = rl_f(dmx, c) * kLog2e;
+      q.rho0 = (float)((double)(float)rl_d(sl.A, c) / (double)rl_f(dA, c));  // as from the verify slots
+    }
+    if (WRITE) {
+      if (lane == 0) a.klen_out[b] = kb;
+      if (lane <= K) {
+        cmsd_target_stats res{};
+        res.max_logit = sl.m;
+        res.sum_exp = (float)sl.A;
+        res.top1 = sl.top1;
+        if (sl.st == -2) {
+          res = cmsd_target_stats{NAN, NAN, -1, -2, -1, {0, 0, 0}};
+        } else if (lane == kv || sl.st == -1) {
+          res.n_greater = -1;  // the final row
+          res.accept = -1;
+        } else {
+          res.n_greater = ng;
+          res.accept = acc;
+        }
+        a.tstats[off + lane] = res;
+      }
+    }
+    if (lane == 0) *lds = q;
+  }
+  __syncthreads();
+  const SeqInfo r = *lds;
+  __syncthreads();
+  return r;
+}
+
 // Partial sums of one raw unit: e_t, e_d, q0 and e_d where q0 > 0.
 template <typename T, bool RESID>
 __device__ __forceinline__ void part_unit(const uint4& rt, const uint4& rd, float mst, float msd, float rho0,
@@ -1099,7 +1261,7 @@ __device__ __forceinline__ void parts_group(const T* trow, const T* drow, const 
   }
 }
 
-template <typename T>
+template <typename T, bool PASS>
 __global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, int SW, SlicePart* __restrict__ ws) {
   constexpr int BD = kPartBD;
   __shared__ double sd[kSubPerWG * 4 * (BD / 64)];
@@ -1107,7 +1269,7 @@ __global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, in
   const int t = threadIdx.x;
   const int b = blockIdx.x / SW, sl0 = (blockIdx.x % SW) * kSubPerWG;
   if (b >= a.B) return;
-  const SeqInfo q = seq_info(a, b, &s_q);
+  const SeqInfo q = PASS ? seq_info_pass<false>(a, b, &s_q) : seq_info(a, b, &s_q);
   if (q.nacc < 0) return;
   const bool resid = q.nacc < q.kb;
   const T* trow = reinterpret_cast<const T*>(a.target) + q.tr * a.tstride;
@@ -1353,7 +1515,7 @@ __device__ __forceinline__ int sample_from_parts(const T* trow, const T* drow, i
   return y;
 }
 
-template <typename T>
+template <typename T, bool PASS>
 __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S, const SlicePart* __restrict__ ws) {
   constexpr int BD = kSampleBD;
   __shared__ double sd[2 * (BD / 64)];
@@ -1364,7 +1526,7 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
   const int t = threadIdx.x;
   const int b = blockIdx.x;
   if (b >= a.B) return;
-  const SeqInfo q = seq_info(a, b, &s_q);
+  const SeqInfo q = PASS ? seq_info_pass<true>(a, b, &s_q) : seq_info(a, b, &s_q);
   if (q.nacc < 0) {
     if (t == 0) {
       a.n_acc[b] = -1;
@@ -1503,6 +1665,17 @@ void launch_target_rows(int bd, const VerifyArgs& a, hipStream_t st) {
     hipLaunchKernelGGL((k_target_rows<T, 256>), grid, dim3(256), 0, st, a);
 }
 
+template <typename T>
+void launch_row_pass(int bd, const VerifyArgs& a, int64_t rows, hipStream_t st) {
+  const dim3 grid((unsigned)rows);
+  if (bd == 64)
+    hipLaunchKernelGGL((k_row_pass<T, 64>), grid, dim3(64), 0, st, a);
+  else if (bd == 128)
+    hipLaunchKernelGGL((k_row_pass<T, 128>), grid, dim3(128), 0, st, a);
+  else
+    hipLaunchKernelGGL((k_row_pass<T, 256>), grid, dim3(256), 0, st, a);
+}
+
 // Number of vocabulary slices of the final-token pass: units are 16-byte vectors
 // plus a head and a tail unit (the head shortens the vector run, so nvec + 2 is at
 // most vocab / VEC + 2).  The workspace is sized for fp32, the dtype with most units.
@@ -1511,22 +1684,38 @@ int verify_slices(int64_t vocab, int elem_bytes) {
   return (int)((units + kSliceUnits - 1) / kSliceUnits);
 }
 
+// Checked confidence parameters: each lambda in [0,1] with |sum - 1| <= 1e-6 and a
+// finite beta_margin > 0.
+bool conf_args(const cmsd_conf_params* p, int64_t vocab, ConfArgs& a) {
+  const float l1 = p->lambda_ent, l2 = p->lambda_margin, l3 = p->lambda_soft;
+  if (!(l1 >= 0.f && l1 <= 1.f && l2 >= 0.f && l2 <= 1.f && l3 >= 0.f && l3 <= 1.f)) return false;
+  if (fabs((double)l1 + (double)l2 + (double)l3 - 1.0) > 1e-6) return false;
+  if (!finite_f(p->beta_margin) || !(p->beta_margin > 0.f)) return false;
+  a = ConfArgs{l1, l2, l3, p->beta_margin, log((double)vocab)};
+  return true;
+}
+bool draft_params_ok(const cmsd_draft_params* p) {
+  return p->k_min >= 1 && p->k_min <= p->k_max && p->k_max <= 4096 && finite_f(p->alpha) && p->alpha > 0.f &&
+         p->alpha <= 1.f;
+}
+bool verify_params_ok(const cmsd_verify_params* p) {
+  return (p->mode == CMSD_MODE_STANDARD || p->mode == CMSD_MODE_CM || p->mode == CMSD_MODE_GREEDY) &&
+         p->top_beta >= 0 && finite_f(p->tau_base) && finite_f(p->gamma);
+}
+
 cmsd_status confidence_impl(const void* logits, int32_t dtype, int64_t n_rows, int64_t vocab, int64_t row_stride,
                             const cmsd_conf_params* params, cmsd_row_stats* stats, float* logit_var, bool want_var,
                             void* stream) {
   if (dtype != CMSD_F32 && dtype != CMSD_BF16) return CMSD_ERR_DTYPE;
   if (!params) return CMSD_ERR_ARG;
   if (n_rows < 0 || n_rows > INT32_MAX || vocab < 2 || vocab > INT32_MAX || row_stride < vocab) return CMSD_ERR_ARG;
-  const float l1 = params->lambda_ent, l2 = params->lambda_margin, l3 = params->lambda_soft;
-  if (!(l1 >= 0.f && l1 <= 1.f && l2 >= 0.f && l2 <= 1.f && l3 >= 0.f && l3 <= 1.f)) return CMSD_ERR_ARG;
-  if (fabs((double)l1 + (double)l2 + (double)l3 - 1.0) > 1e-6) return CMSD_ERR_ARG;
-  if (!finite_f(params->beta_margin) || !(params->beta_margin > 0.f)) return CMSD_ERR_ARG;
+  ConfArgs a;
+  if (!conf_args(params, vocab, a)) return CMSD_ERR_ARG;
   const size_t es = dtype == CMSD_F32 ? 4 : 2;
   if (n_rows == 0) return CMSD_OK;
   if (!logits || !stats || !aligned(logits, es) || !aligned(stats, 4)) return CMSD_ERR_ARG;
   if (want_var && (!logit_var || !aligned(logit_var, 4))) return CMSD_ERR_ARG;
   if (row_stride > INT64_MAX / n_rows) return CMSD_ERR_ARG;
-  const ConfArgs a{l1, l2, l3, params->beta_margin, log((double)vocab)};
   const int bd = row_block(n_rows, vocab * (int64_t)es);
   const hipStream_t st = as_stream(stream);
   if (dtype == CMSD_F32) {
@@ -1556,7 +1745,7 @@ const char* cmsd_status_string(cmsd_status s) {
   return "unknown status";
 }
 
-int32_t cmsd_version(void) { return (1 << 16) | 2; }
+int32_t cmsd_version(void) { return (1 << 16) | 3; }
 
 size_t cmsd_draft_sample_workspace_bytes(int64_t n_rows, int64_t vocab) {
   if (n_rows <= 0 || n_rows > INT32_MAX || vocab < 2 || vocab > INT32_MAX) return 0;
@@ -1615,10 +1804,8 @@ cmsd_status cmsd_confidence_var(const void* logits, int32_t dtype, int64_t n_row
 
 cmsd_status cmsd_draft_len(const cmsd_row_stats* stats, int32_t batch, const cmsd_draft_params* params,
                            int32_t* draft_len, int32_t* target_offsets, void* stream) {
-  if (!params || batch < 0) return CMSD_ERR_ARG;
+  if (!params || batch < 0 || !draft_params_ok(params)) return CMSD_ERR_ARG;
   const int k_min = params->k_min, k_max = params->k_max;
-  if (k_min < 1 || k_min > k_max || k_max > 4096) return CMSD_ERR_ARG;
-  if (!finite_f(params->alpha) || !(params->alpha > 0.f) || !(params->alpha <= 1.f)) return CMSD_ERR_ARG;
   if ((int64_t)batch * (k_max + 1) > INT32_MAX) return CMSD_ERR_ARG;
   if (!target_offsets || !aligned(target_offsets, 4)) return CMSD_ERR_ARG;
   if (batch > 0 && (!stats || !draft_len || !aligned(stats, 4) || !aligned(draft_len, 4))) return CMSD_ERR_ARG;
@@ -1636,9 +1823,7 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   if (dtype != CMSD_F32 && dtype != CMSD_BF16) return CMSD_ERR_DTYPE;
   if (!params) return CMSD_ERR_ARG;
   if (batch < 0 || k_max < 1 || k_max > 4096 || vocab < 2 || vocab > INT32_MAX) return CMSD_ERR_ARG;
-  if (params->mode != CMSD_MODE_STANDARD && params->mode != CMSD_MODE_CM && params->mode != CMSD_MODE_GREEDY)
-    return CMSD_ERR_ARG;
-  if (params->top_beta < 0 || !finite_f(params->tau_base) || !finite_f(params->gamma)) return CMSD_ERR_ARG;
+  if (!verify_params_ok(params)) return CMSD_ERR_ARG;
   if (batch == 0) return CMSD_OK;
   if (target_rows < 1 || target_rows > INT32_MAX) return CMSD_ERR_ARG;
   if (draft_stride < vocab || target_stride < vocab) return CMSD_ERR_ARG;
@@ -1685,13 +1870,87 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   if (dtype == CMSD_F32) {
     launch_target_rows<float>(bd, a, st);
     if (a.mode != CMSD_MODE_GREEDY)
-      hipLaunchKernelGGL((k_final_parts<float>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
-    hipLaunchKernelGGL((k_final_sample<float>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
+      hipLaunchKernelGGL((k_final_parts<float, false>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
+    hipLaunchKernelGGL((k_final_sample<float, false>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   } else {
     launch_target_rows<Bf16>(bd, a, st);
     if (a.mode != CMSD_MODE_GREEDY)
-      hipLaunchKernelGGL((k_final_parts<Bf16>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
-    hipLaunchKernelGGL((k_final_sample<Bf16>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
+      hipLaunchKernelGGL((k_final_parts<Bf16, false>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
+    hipLaunchKernelGGL((k_final_sample<Bf16, false>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
+  }
+  return launched();
+}
+
+cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, const void* target_logits,
+                            int64_t target_stride, const int32_t* drafted, const float* uniforms, int32_t dtype,
+                            int32_t batch, int32_t k_max, int64_t vocab, const cmsd_conf_params* conf,
+                            const cmsd_draft_params* draft, const cmsd_verify_params* verify, int32_t adaptive,
+                            cmsd_row_stats* draft_stats, int32_t* draft_len, cmsd_target_stats* target_stats,
+                            int32_t* n_accepted, int32_t* next_token, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  if (dtype != CMSD_F32 && dtype != CMSD_BF16) return CMSD_ERR_DTYPE;
+  if (!conf || !draft || !verify) return CMSD_ERR_ARG;
+  if (batch < 0 || k_max < 1 || k_max > 63 || vocab < 2 || vocab > INT32_MAX) return CMSD_ERR_ARG;
+  if (adaptive != 0 && adaptive != 1) return CMSD_ERR_ARG;
+  VerifyArgs a{};
+  if (!conf_args(conf, vocab, a.ca) || !draft_params_ok(draft) || draft->k_max != k_max || !verify_params_ok(verify))
+    return CMSD_ERR_ARG;
+  if (draft_stride < vocab || target_stride < vocab) return CMSD_ERR_ARG;
+  if (batch == 0) return CMSD_OK;
+  const size_t es = dtype == CMSD_F32 ? 4 : 2;
+  const int64_t drows = (int64_t)batch * k_max, trows = (int64_t)batch * (k_max + 1);
+  if (drows + trows > INT32_MAX || draft_stride > INT64_MAX / drows || target_stride > INT64_MAX / trows)
+    return CMSD_ERR_ARG;
+  if ((int64_t)batch * verify_slices(vocab, 4) > INT32_MAX) return CMSD_ERR_ARG;
+  if (!draft_logits || !target_logits || !drafted || (!uniforms && verify->mode != CMSD_MODE_GREEDY) ||
+      !draft_stats || !draft_len || !target_stats || !n_accepted || !next_token || !workspace)
+    return CMSD_ERR_ARG;
+  if (workspace_bytes < cmsd_verify_workspace_bytes(batch, k_max, vocab) || !aligned(workspace, 8)) return CMSD_ERR_ARG;
+  if (!aligned(draft_logits, es) || !aligned(target_logits, es) || !aligned(drafted, 4) || !aligned(uniforms, 4) ||
+      !aligned(draft_stats, 4) || !aligned(draft_len, 4) || !aligned(target_stats, 4) || !aligned(n_accepted, 4) ||
+      !aligned(next_token, 4))
+    return CMSD_ERR_ARG;
+  a.draft = draft_logits;
+  a.dstride = draft_stride;
+  a.dstats = draft_stats;
+  a.dstats_out = draft_stats;
+  a.target = target_logits;
+  a.tstride = target_stride;
+  a.target_rows = trows;
+  a.drafted = drafted;
+  a.unif = uniforms;
+  a.B = batch;
+  a.k_max = k_max;
+  a.V = vocab;
+  a.mode = verify->mode;
+  a.beta = verify->top_beta;
+  a.tau_base = verify->tau_base;
+  a.gamma = verify->gamma;
+  a.tstats = target_stats;
+  a.n_acc = n_accepted;
+  a.next_tok = next_token;
+  a.klen_out = draft_len;
+  a.k_min = draft->k_min;
+  a.alpha = draft->alpha;
+  a.adaptive = adaptive;
+  const hipStream_t st = as_stream(stream);
+  const int S = verify_slices(vocab, (int)es);
+  const int SW = (S + kSubPerWG - 1) / kSubPerWG;
+  SlicePart* ws = static_cast<SlicePart*>(workspace);
+  a.pslots = reinterpret_cast<PassSlot*>(ws + (size_t)batch * verify_slices(vocab, 4));
+  static_assert(sizeof(PassSlot) == sizeof(RowSlot), "the pass uses the verify workspace layout");
+  const unsigned gp = (unsigned)((int64_t)batch * SW);
+  const int bd = row_block(drows + trows, vocab * (int64_t)es);
+  if (dtype == CMSD_F32) {
+    launch_row_pass<float>(bd, a, drows + trows, st);
+    if (a.mode != CMSD_MODE_GREEDY)
+      hipLaunchKernelGGL((k_final_parts<float, true>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
+    hipLaunchKernelGGL((k_final_sample<float, true>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
+  } else {
+    launch_row_pass<Bf16>(bd, a, drows + trows, st);
+    if (a.mode != CMSD_MODE_GREEDY)
+      hipLaunchKernelGGL((k_final_parts<Bf16, true>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
+    hipLaunchKernelGGL((k_final_sample<Bf16, true>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   }
   return launched();
 }

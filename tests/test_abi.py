@@ -15,11 +15,11 @@ def test_exports_every_declared_symbol():
     assert set(syms) >= {"cmsd_confidence", "cmsd_confidence_var", "cmsd_draft_len", "cmsd_verify",
                          "cmsd_verify_workspace_bytes",
                          "cmsd_draft_sample", "cmsd_draft_sample_workspace_bytes", "cmsd_status_string",
-                         "cmsd_version"}
+                         "cmsd_version", "cmsd_logit_pass"}
     lib = cm.lib()
     for s in syms:
         assert hasattr(lib, s), s
-    assert lib.cmsd_version() == (1 << 16) | 2
+    assert lib.cmsd_version() == (1 << 16) | 3
     assert lib.cmsd_status_string(0) == b"ok"
     assert lib.cmsd_status_string(1) == b"invalid argument"
 
@@ -128,3 +128,45 @@ def test_draft_sample_argument_errors(kw, want):
                                       a["out"], a["ws"], a["wsb"], None) == want
     f = cm.lib().cmsd_draft_sample_workspace_bytes
     assert f(0, 100) == 0 and f(3, 1) == 0 and f(3, 4096) == 3 * 32 * ((4096 // 4 + 2 + 255) // 256)
+
+
+def _lpass(**kw):
+    a = dict(dl=P, ds=1024, tl=P, ts=1024, dr=P, u=P, dtype=cm.CMSD_BF16, B=4, K=8, V=1024,
+             cp=cm.ConfParams(0.25, 0.25, 0.5, 1.0), dp=cm.DraftParams(1, 8, 1.0), vp=cm.VerifyParams(1, 3, 0.1, 1.0),
+             ad=0, dst=P, kl=P, tst=P, na=P, nt=P, ws=P, wsb=1 << 20)
+    a.update(kw)
+    ref = lambda x: C.byref(x) if x is not None else None  # noqa: E731
+    return cm.lib().cmsd_logit_pass(a["dl"], a["ds"], a["tl"], a["ts"], a["dr"], a["u"], a["dtype"], a["B"], a["K"],
+                                    a["V"], ref(a["cp"]), ref(a["dp"]), ref(a["vp"]), a["ad"], a["dst"], a["kl"],
+                                    a["tst"], a["na"], a["nt"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(dtype=3), cm.CMSD_ERR_DTYPE),
+    (dict(cp=None), cm.CMSD_ERR_ARG),
+    (dict(dp=None), cm.CMSD_ERR_ARG),
+    (dict(vp=None), cm.CMSD_ERR_ARG),
+    (dict(cp=cm.ConfParams(0.5, 0.5, 0.5, 1.0)), cm.CMSD_ERR_ARG),
+    (dict(dp=cm.DraftParams(1, 7, 1.0)), cm.CMSD_ERR_ARG),          # draft k_max differs from k_max
+    (dict(dp=cm.DraftParams(9, 8, 1.0)), cm.CMSD_ERR_ARG),
+    (dict(dp=cm.DraftParams(1, 8, 0.0)), cm.CMSD_ERR_ARG),
+    (dict(vp=cm.VerifyParams(7, 3, 0.1, 1.0)), cm.CMSD_ERR_ARG),
+    (dict(K=0, dp=cm.DraftParams(1, 0, 1.0)), cm.CMSD_ERR_ARG),
+    (dict(K=64, dp=cm.DraftParams(1, 64, 1.0)), cm.CMSD_ERR_ARG),   # at most 63 drafts per sequence
+    (dict(V=1), cm.CMSD_ERR_ARG),
+    (dict(ws=None), cm.CMSD_ERR_ARG),
+    (dict(wsb=64), cm.CMSD_ERR_ARG),                                # workspace too small
+    (dict(ws=P + 4), cm.CMSD_ERR_ARG),
+    (dict(ds=1000), cm.CMSD_ERR_ARG),
+    (dict(ts=1000), cm.CMSD_ERR_ARG),
+    (dict(ad=2), cm.CMSD_ERR_ARG),
+    (dict(B=-1), cm.CMSD_ERR_ARG),
+    (dict(u=None), cm.CMSD_ERR_ARG),                                # needed outside GREEDY mode
+    (dict(dr=None), cm.CMSD_ERR_ARG),
+    (dict(kl=None), cm.CMSD_ERR_ARG),
+    (dict(tl=P + 1), cm.CMSD_ERR_ARG),
+    (dict(na=P + 2), cm.CMSD_ERR_ARG),
+    (dict(B=0, dl=None, tl=None, dr=None, ws=None, wsb=0), cm.CMSD_OK),
+])
+def test_logit_pass_argument_errors(kw, want):
+    assert _lpass(**kw) == want

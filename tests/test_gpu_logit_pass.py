@@ -1,0 +1,233 @@
+"""GPU parity of cmsd_logit_pass, the one-call logit pass of a dense draft
+(Sec. III.B(1)-(c), Sec. III.A), against the oracle through the C ABI: drafter
+stats, draft lengths, target-row results, accept tests, prefixes and final tokens,
+on the dense workloads, in both verification lengths, and on edge cases."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import cmsd_oracle as O
+from tests import harness as Hn
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def cm():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2508_15371_amd import cmsd
+    return cmsd
+
+
+def _pass(cm, dd, td, drafted, unif, B, K, mode, adaptive=False, **kw):
+    P = dict(Hn.PARAMS)
+    P.update(kw)
+    out = cm.cmsd_logit_pass(dd, td, drafted, None if mode == O.MODE_GREEDY and unif is None else unif,
+                             batch=B, k_max=K, lambdas=P["lambdas"], beta_margin=P["beta_margin"],
+                             k_min=P["k_min"], alpha=P["alpha"], mode=mode, top_beta=P["top_beta"],
+                             tau_base=P["tau_base"], gamma=P["gamma"], adaptive=adaptive)
+    torch.cuda.synchronize()
+    return out, P
+
+
+def _check(t, cfg_B, K, V, dtype, draft, target, drafted, uniforms, out, P, mode, adaptive, seqs, stats_rows=True):
+    """draft/target: stored host rows; drafted [B, K]; uniforms [B, K+1]."""
+    gs = Hn.stats_np(out["draft_stats"])
+    ts = Hn.tstats_np(out["target_stats"])
+    k_gpu = out["draft_len"].cpu().numpy()
+    n_acc = out["n_accepted"].cpu().numpy()
+    nxt = out["next_token"].cpu().numpy()
+    lam = tuple(Hn.f32(x) for x in P["lambdas"])
+    # draft length from the GPU's confidences (stage isolation): bit-exact
+    Cg = gs["C"].astype(np.float64).reshape(cfg_B, K)
+    k_o, _, _ = O.draft_len(Cg, P["k_min"], K, Hn.f32(P["alpha"]))
+    t.value("k(stage)", np.array_equal(k_o, k_gpu), (k_o[:8], k_gpu[:8]))
+    for b in seqs:
+        zd = [Hn.decode(draft[b * K + i], dtype) for i in range(K)]
+        if stats_rows:
+            for i in range(K):
+                Hn.check_row_stats(t, gs, b * K + i, zd[i], V, lam, Hn.f32(P["beta_margin"]))
+        C = [O.confidence(O.row_stats(z), V, lam, Hn.f32(P["beta_margin"])) for z in zd]
+        kb_o, _, sl = O.draft_len(np.array([C]), P["k_min"], K, Hn.f32(P["alpha"]))
+        t.decision(f"k[{b}]", int(k_gpu[b]), int(kb_o[0]), float(sl[0]))
+        kv = int(k_gpu[b]) if adaptive else K
+        pos = list(range(kv + 1))
+        zt = [Hn.decode(target[b * (K + 1) + i], dtype) for i in pos]
+        unif = [float(uniforms[b, i]) for i in pos]
+        Hn.check_sequence(t, b, zt, zd, drafted[b], unif, C, kv, mode, P, ts, b * (K + 1), int(n_acc[b]),
+                          int(nxt[b]))
+    return n_acc, k_gpu
+
+
+def _seqs(B, n, salt):
+    if B <= n:
+        return list(range(B))
+    g = np.random.default_rng(300 + salt)
+    return sorted(set([0, B - 1] + g.choice(B, n, replace=False).tolist()))
+
+
+@pytest.mark.parametrize("adaptive", [False, True])
+@pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY])
+@pytest.mark.parametrize("name,nseq", [("tiny", 1), ("c2", 8), ("c3", 24), ("c4", 3), ("c5", 12), ("v152k", 6)])
+def test_logit_pass_configs(cm, name, nseq, mode, adaptive):
+    print(f"[logit pass parity] start {name} mode={mode} adaptive={adaptive}", flush=True)
+    cfg = W.CONFIGS[name]
+    d = Hn.workload(name)
+    out, P = _pass(cm, d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"], cfg.B, cfg.k_max, mode,
+                   adaptive)
+    t = Hn.Tally()
+    seqs = _seqs(cfg.B, nseq, cfg.cid)
+    n_acc, k = _check(t, cfg.B, cfg.k_max, cfg.V, cfg.dtype, d["draft"], d["target"], d["drafted"], d["uniforms"],
+                      out, P, mode, adaptive, seqs, stats_rows=len(seqs) * cfg.k_max <= 256)
+    print(f"[logit pass parity] {name} mode={mode} adaptive={adaptive}: checked={t.checked} "
+          f"exceptions={t.exceptions} mean n_acc={n_acc.mean():.3f} mean k={k.mean():.3f}", flush=True)
+    t.assert_ok()
+
+
+@pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY])
+def test_bitwise_equal_to_separate_calls(cm, mode):
+    # same arithmetic as confidence + draft_len + verify (dense offsets, k = k_max); on
+    # c3 both launch their row kernels with 256 threads, so every output is bit-equal
+    from paper_2508_15371_amd import pipeline
+    cfg = W.CONFIGS["c3"]
+    d = Hn.workload("c3")
+    out, _ = _pass(cm, d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"], cfg.B, cfg.k_max, mode)
+    lp = pipeline.LogitPass(cfg.B, cfg.k_max, cfg.V, "cuda:0", pipeline.Params(mode=mode))
+    lp.run(d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"])
+    torch.cuda.synchronize()
+    pairs = {"draft_stats": lp.stats, "draft_len": lp.k, "target_stats": lp.tstats, "n_accepted": lp.n_acc,
+             "next_token": lp.next_tok}
+    for k, ref in pairs.items():
+        assert torch.equal(out[k].view(torch.int32), ref.view(torch.int32)), k
+
+
+def test_repeat_bitwise_identical(cm):
+    cfg = W.CONFIGS["c2"]
+    d = Hn.workload("c2")
+    o1, _ = _pass(cm, d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"], cfg.B, cfg.k_max, O.MODE_CM)
+    o1 = {k: v.clone() for k, v in o1.items()}
+    o2, _ = _pass(cm, d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"], cfg.B, cfg.k_max, O.MODE_CM)
+    for k in o1:
+        assert torch.equal(o1[k].view(torch.int32), o2[k].view(torch.int32)), k
+
+
+# ----------------------------------------------------------------------------- edge cases
+def _case(g, B, K, V, dtype, scale=2.0, mask=None):
+    zd = g.normal(0, scale, (B * K, V)).astype(np.float32)
+    zt = g.normal(0, scale, (B * (K + 1), V)).astype(np.float32)
+    for b in range(B):
+        for i in range(K):
+            zt[b * (K + 1) + i] = zd[b * K + i] + g.normal(0, 0.5, V).astype(np.float32)
+    if mask is not None:
+        zd[:, mask] = -np.inf
+        zt[:, mask] = -np.inf
+    store = (lambda x: x) if dtype == "f32" else W.bf16_bits_from_f32
+    zds, zts = store(zd), store(zt)
+    drafted = np.array([[int(np.argmax(Hn.decode(zds[b * K + i], dtype) + g.gumbel(size=V))) for i in range(K)]
+                        for b in range(B)], dtype=np.int32)
+    unif = (g.integers(0, 1 << 24, (B, K + 1)) * 2.0 ** -24).astype(np.float32)
+    return zds, zts, drafted, unif
+
+
+def _run_case(cm, zd, zt, drafted, unif, B, K, V, dtype, mode=O.MODE_CM, adaptive=False, pad=0, **kw):
+    dev = torch.device("cuda:0")
+    dd = Hn.to_device(zd, dtype, dev)
+    td = Hn.to_device(zt, dtype, dev)
+    if pad:
+        # rows with a stride beyond the vocabulary
+        dd = torch.nn.functional.pad(dd, (0, pad))[:, :V]
+        td = torch.nn.functional.pad(td, (0, pad))[:, :V]
+    out, P = _pass(cm, dd, td, torch.from_numpy(drafted.reshape(-1)).to(dev),
+                   torch.from_numpy(unif.reshape(-1)).to(dev), B, K, mode, adaptive, **kw)
+    t = Hn.Tally()
+    n_acc, k = _check(t, B, K, V, dtype, zd, zt, drafted, unif, out, P, mode, adaptive, list(range(B)))
+    t.assert_ok()
+    return out, n_acc, k
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("V,K,B,pad", [(2, 1, 3, 0), (37, 3, 5, 3), (1000, 63, 2, 0), (4099, 5, 4, 5),
+                                       (50257, 7, 3, 1), (300007, 2, 2, 0)])
+def test_shapes(cm, dtype, V, K, B, pad):
+    g = np.random.default_rng(V * 7 + K)
+    zd, zt, dr, u = _case(g, B, K, V, dtype)
+    for mode in (O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY):
+        _run_case(cm, zd, zt, dr, u, B, K, V, dtype, mode=mode, adaptive=bool(mode == O.MODE_CM), pad=pad)
+
+
+def test_masked_logits(cm):
+    # -inf entries: flags bit 0, entropy over the finite entries, final tokens never masked
+    V, K, B = 3001, 4, 4
+    g = np.random.default_rng(5)
+    mask = g.random(V) < 0.4
+    zd, zt, dr, u = _case(g, B, K, V, "bf16", mask=mask)
+    out, n_acc, _ = _run_case(cm, zd, zt, dr, u, B, K, V, "bf16")
+    assert np.all(Hn.stats_np(out["draft_stats"])["flags"] & 1)
+    assert not np.any(mask[out["next_token"].cpu().numpy()])
+
+
+def test_invalid_drafted_id(cm):
+    V, K, B = 500, 4, 3
+    g = np.random.default_rng(8)
+    zd, zt, dr, u = _case(g, B, K, V, "f32")
+    dr[1, 3] = V          # out of range: sequence 1 is invalid, the others are not
+    dev = torch.device("cuda:0")
+    out, _ = _pass(cm, Hn.to_device(zd, "f32", dev), Hn.to_device(zt, "f32", dev),
+                   torch.from_numpy(dr.reshape(-1)).to(dev), torch.from_numpy(u.reshape(-1)).to(dev), B, K,
+                   O.MODE_CM)
+    n_acc = out["n_accepted"].cpu().numpy()
+    nxt = out["next_token"].cpu().numpy()
+    ts = Hn.tstats_np(out["target_stats"])
+    assert n_acc[1] == -1 and nxt[1] == -1 and ts["acc"][1 * (K + 1) + 3] == -2
+    assert n_acc[0] >= 0 and n_acc[2] >= 0 and nxt[0] >= 0 and nxt[2] >= 0
+
+
+def test_greedy_exact_match(cm):
+    # top_beta = 0: exact-match verification; drafts equal to the target's top token
+    # up to a chosen position are accepted, and the final token is that row's top token
+    V, K, B = 2000, 6, 4
+    g = np.random.default_rng(13)
+    zd, zt, _, u = _case(g, B, K, V, "f32")
+    dr = np.zeros((B, K), dtype=np.int32)
+    for b in range(B):
+        for i in range(K):
+            top = int(np.argmax(zt[b * (K + 1) + i]))
+            dr[b, i] = top if i < b + 1 else (top + 1) % V
+    out, n_acc, _ = _run_case(cm, zd, zt, dr, u, B, K, V, "f32", mode=O.MODE_GREEDY, top_beta=0)
+    nxt = out["next_token"].cpu().numpy()
+    for b in range(B):
+        assert n_acc[b] == b + 1
+        assert nxt[b] == int(np.argmax(zt[b * (K + 1) + b + 1]))
+
+
+def test_adaptive_lengths_cover_range(cm):
+    # alpha sweeps k_b over [k_min, k_max]; the prefix never passes k_b and row k_b is final
+    V, K, B = 4096, 8, 16
+    g = np.random.default_rng(21)
+    spikes = [(r, int(g.integers(0, V)), float(g.uniform(9, 22))) for r in range(B * K // 2)]
+    zd, zt, dr, u = _case(g, B, K, V, "f32", scale=2.0)
+    for r, v, h in spikes:       # the first half of the sequences: confident drafter rows
+        zd[r, v] += h
+        zt[(r // K) * (K + 1) + r % K, v] += h
+        dr[r // K, r % K] = v
+    seen = set()
+    for alpha in (0.05, 0.3, 0.6, 1.0):
+        out, n_acc, k = _run_case(cm, zd, zt, dr, u, B, K, V, "f32", adaptive=True, alpha=alpha)
+        ts = Hn.tstats_np(out["target_stats"])
+        assert np.all(n_acc <= k)
+        assert all(ts["acc"][b * (K + 1) + k[b]] == -1 for b in range(B))
+        seen |= set(k.tolist())
+    assert min(seen) == 1 and max(seen) >= 6, seen
+
+
+def test_empty_batch(cm):
+    dev = torch.device("cuda:0")
+    z = torch.zeros((0, 100), dtype=torch.float32, device=dev)
+    out = cm.cmsd_logit_pass(z, z, torch.zeros(0, dtype=torch.int32, device=dev),
+                             torch.zeros(0, dtype=torch.float32, device=dev), batch=0, k_max=4)
+    torch.cuda.synchronize()
+    assert out["n_accepted"].numel() == 0

@@ -23,7 +23,7 @@ int main(void) {
   cmsd_row_stats st;
   float x = 0.f;
   int32_t k = 0, off = 0;
-  if (cmsd_version() != ((1 << 16) | 2)) bad |= 1;
+  if (cmsd_version() != ((1 << 16) | 3)) bad |= 1;
   if (strcmp(cmsd_status_string(CMSD_OK), "ok") != 0) bad |= 2;
   if (cmsd_verify_workspace_bytes(0, 8, 1000) != 0) bad |= 4;
   if (cmsd_verify_workspace_bytes(4, 8, 1000) == 0) bad |= 8;
