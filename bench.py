@@ -1,13 +1,16 @@
 """Benchmark of the logit pass (confidence + draft length + verify) on one MI355X.
 
 One step = one decoding iteration of the hot path over a resident synthetic batch:
-cmsd_confidence over all drafter rows, cmsd_draft_len, cmsd_verify over all target
-rows (accept decisions, prefix scan, final residual/bonus sample).  Prints one JSON
-line.  Default workload: B=256 sequences, k_max=16, V=128256, bf16 (the largest
-configuration; inputs 2.17 GB).
+drafter stats over all drafter rows, the draft lengths, and verification of all target
+rows (accept decisions, prefix scan, final residual/bonus sample).  On the dense
+workloads a step is one cmsd_logit_pass call (a joint row pass over drafter and target
+rows, then the final-token pass); on the ragged one, whose target rows are packed by
+the draft lengths, it is cmsd_confidence + cmsd_draft_len + cmsd_verify (--path calls
+forces the separate calls everywhere).  Prints one JSON line.  Default workload: B=256
+sequences, k_max=16, V=128256, bf16 (the largest configuration; inputs 2.17 GB).
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4] [--mode cm|standard]
-                  [--no-cpu-baseline]
+                  [--path auto|pass|calls] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -24,9 +27,9 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0   # MI355X HBM3E
 
-# HBM bytes per launch of k_confidence on the default workload, from two rocprofv3
-# --pmc runs (FETCH_SIZE, WRITE_SIZE) scaled by what the same counters read for a
-# 1 GiB device copy (x2.0 and x1.0).  Valid only for the kernel source they were
+# HBM bytes per launch of the roofline kernel on the default workload, from two
+# rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) scaled by what the same counters read
+# for a 1 GiB device copy (x2.0 and x1.0).  Valid only for the kernel source they were
 # taken on (sha256 prefix of the .hip file); otherwise "traffic" is reported null.
 TRAFFIC = {"kernel_sha256_16": "a0f3997e76f880ba", "k_confidence_c4": 1052.89e6 + 0.131e6,
            "profile": "profiles/c4_cm_logit_pass.md"}
@@ -84,12 +87,12 @@ def cpu_baseline(name: str, seed: int, mode: int, budget_s: float = 20.0) -> dic
                       f"{workers} processes"}
 
 
-def _traffic(workload: str):
-    """Measured HBM bytes per k_confidence launch, if the kernel source is the profiled one."""
+def _traffic(kernel: str, workload: str):
+    """Measured HBM bytes per launch of `kernel`, if the kernel source is the profiled one."""
     import hashlib
     src = os.path.join(ROOT, "paper_2508_15371_amd", "csrc", "cmsd.hip")
     sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    key = f"k_confidence_{workload}"
+    key = f"{kernel}_{workload}"
     if sha != TRAFFIC["kernel_sha256_16"] or key not in TRAFFIC:
         return None
     return TRAFFIC[key]
@@ -103,10 +106,13 @@ def main() -> int:
     ap.add_argument("--workload", default="c4", choices=["c2", "c3", "c4", "c5", "v152k"])
     ap.add_argument("--mode", default="cm", choices=["cm", "standard"])
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--path", default="auto", choices=["auto", "pass", "calls"],
+                    help="one cmsd_logit_pass call per step (dense layouts; auto: dense workloads) "
+                         "or the three separate calls")
     ap.add_argument("--streams", type=int, default=1, metavar="G",
                     help="split the batch into G sequence groups, each on its own stream")
     ap.add_argument("--event-every", type=int, default=4, metavar="N",
-                    help="bracket k_confidence with HIP events in every N-th timed step")
+                    help="bracket the roofline kernel with HIP events in every N-th timed step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run device-to-device copies of MIB MiB (calibrates HBM byte counters)")
@@ -178,27 +184,50 @@ def main() -> int:
             lpg.run(*a, st)
     torch.cuda.synchronize()
 
+    # one cmsd_logit_pass call per step on dense workloads (one stream), else the three calls
+    use_pass = args.path == "pass" or (args.path == "auto" and not cfg.ragged)
+    if use_pass and (cfg.ragged or G != 1):
+        print("bench.py: --path pass needs a dense workload and one stream", file=sys.stderr)
+        return 2
+    rk = "k_row_pass" if use_pass else "k_confidence"
+
+    def step(lpg, a, st, e=None):
+        if use_pass:
+            lpg.logit_pass(a[0], a[1], a[2], a[3], st, row_events=e)
+            return
+        if e is not None:
+            e[0].record(st)
+        lpg.confidence(a[0], st)
+        if e is not None:
+            e[1].record(st)
+        lpg.draft_len(st)
+        lpg.verify(a[0], a[1], a[2], a[3], st)
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        for lpg, a, st in groups:
+            step(lpg, a, st)
+    torch.cuda.synchronize()
+
     # timed region: K steps.  HIP events on the launch stream bracket the roofline
-    # kernel (k_confidence of group 0) in every `event_every`-th step; each event
-    # marker costs GPU time between kernels, so no other call is bracketed here.
+    # kernel (the joint row pass of cmsd_logit_pass, or k_confidence of group 0 on the
+    # three-call path) in every `event_every`-th step; each event marker costs GPU time
+    # between kernels, so no other kernel is bracketed here.
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] if k % args.event_every == 0 else None
           for k in range(args.steps)]
+    for e in ev:
+        if e is not None:      # the binding hands the library events that exist
+            e[0].record(main)
+            e[1].record(main)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for e in ev:
         for gi, (lpg, a, st) in enumerate(groups):
-            if e is not None and gi == 0:
-                e[0].record(st)
-            lpg.confidence(a[0], st)
-            if e is not None and gi == 0:
-                e[1].record(st)
-            lpg.draft_len(st)
-            lpg.verify(a[0], a[1], a[2], a[3], st)
+            step(lpg, a, st, e if gi == 0 else None)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_step = 1e3 * elapsed / args.steps
-    t_conf = float(np.mean([e[0].elapsed_time(e[1]) for e in ev if e is not None])) * 1e-3
-    conf_rows_timed = R_d // G
+    t_roof = float(np.mean([e[0].elapsed_time(e[1]) for e in ev if e is not None])) * 1e-3
 
     # per-call split, one group after another on one stream (outside the timed region)
     ev2 = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(max(3, args.steps // 4))]
@@ -224,8 +253,14 @@ def main() -> int:
     rej = int((n_acc < k_used).sum())
     s = cfg.elem_bytes
     conf_bytes = R_d * cfg.V * s + R_d * 32
-    # the roofline kernel's launch: one group's drafter rows (the whole batch when G = 1)
-    launch_bytes = conf_rows_timed * cfg.V * s + conf_rows_timed * 32
+    # the roofline kernel's launch: the joint row pass reads every drafter and target row
+    # once and writes a 32-byte record per drafter row, a 32-byte record and a 32-byte
+    # slot per target row, after gathering two logits per drafted position; k_confidence
+    # reads one group's drafter rows (the whole batch when G = 1) and writes their records
+    if use_pass:
+        launch_bytes = R_d * (cfg.V * s + 32) + R_t * (cfg.V * s + 64) + cfg.B * cfg.k_max * 8
+    else:
+        launch_bytes = (R_d // G) * (cfg.V * s + 32)
     verify_bytes = R_t * cfg.V * s + rej * cfg.V * s + R_t * 32 + cfg.B * cfg.k_max * 8
     step_bytes = conf_bytes + cfg.B * cfg.k_max * 32 + verify_bytes
 
@@ -248,11 +283,12 @@ def main() -> int:
                    "drafter_rows": R_d, "target_rows": R_t},
         "gbps_algorithmic": step_bytes / (ms_step * 1e-3) / 1e9,
         "per_call_ms": {"cmsd_confidence": t_conf1 * 1e3, "cmsd_draft_len": t_dl * 1e3, "cmsd_verify": t_ver * 1e3},
-        "roofline": {"kernel": "k_confidence", "bound": "hbm", "achieved": launch_bytes / t_conf / 1e9,
-                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": launch_bytes / t_conf / 1e9 / PEAK_HBM_GBS,
-                     "traffic": _traffic(cfg.name) if G == 1 else None},
+        "roofline": {"kernel": rk, "bound": "hbm", "achieved": launch_bytes / t_roof / 1e9,
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": launch_bytes / t_roof / 1e9 / PEAK_HBM_GBS,
+                     "traffic": _traffic(rk, cfg.name) if G == 1 else None},
         "workload_stats": {"mean_n_acc": float(n_acc.mean()), "rejecting_sequences": rej,
-                           "mean_draft_len": float(k_all.mean()), "streams": G},
+                           "mean_draft_len": float(k_all.mean()), "streams": G,
+                           "path": "cmsd_logit_pass" if use_pass else "three calls"},
     }
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)

@@ -13,8 +13,8 @@
  *                    accepted-prefix length, and the final token sampled from
  *                    the residual (or bonus) distribution     (Sec. III.A, III.B(c))
  *
- * cmsd_logit_pass does all three in one call (three launches) for a dense target
- * layout.
+ * cmsd_logit_pass does all three in one call (four launches, two in GREEDY mode)
+ * for a dense target layout.
  *
  * Conventions shared by every call
  *   - All array pointers are DEVICE pointers (hipMalloc / torch CUDA tensors);
@@ -229,9 +229,11 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
  * cmsd_logit_pass - the whole logit pass of one decoding iteration in one call, for
  * a dense target layout: cmsd_confidence on the drafter rows, cmsd_draft_len's draft
  * length and cmsd_verify on target rows stored k_max + 1 per sequence (Sec. III.B(1)
- * to (c), Sec. III.A), in three launches instead of five: one row pass over the
- * drafter and target rows together (they do not depend on each other), then the
- * final-token pass, which also makes the accept tests and forms the draft length.
+ * to (c), Sec. III.A), in four launches instead of five: one row pass over the
+ * drafter and target rows together (they do not depend on each other), one wave per
+ * sequence that forms the draft length and the accept tests, then the two
+ * final-token kernels (skipped in GREEDY mode, whose final token is the row's top
+ * token).
  *
  *   draft_logits    device, batch*k_max drafter rows (row b*k_max+i), stride
  *                   draft_stride >= vocab elements.
@@ -275,7 +277,8 @@ cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, cons
                             const cmsd_conf_params* conf, const cmsd_draft_params* draft,
                             const cmsd_verify_params* verify, int32_t adaptive, cmsd_row_stats* draft_stats,
                             int32_t* draft_len, cmsd_target_stats* target_stats, int32_t* n_accepted,
-                            int32_t* next_token, void* workspace, size_t workspace_bytes, void* stream);
+                            int32_t* next_token, void* workspace, size_t workspace_bytes,
+                            void* const* row_events, void* stream);
 
 /* Workspace cmsd_verify needs for `batch` sequences of up to `k_max` drafts over
  * `vocab`: per sequence, one 32-byte record per vocabulary slice (256 16-byte

@@ -67,7 +67,7 @@ def _load() -> C.CDLL:
     lib.cmsd_draft_sample_workspace_bytes.restype = C.c_size_t
     lib.cmsd_logit_pass.argtypes = [vp, i64, vp, i64, vp, vp, i32, i32, i32, i64, C.POINTER(ConfParams),
                                     C.POINTER(DraftParams), C.POINTER(VerifyParams), i32, vp, vp, vp, vp, vp, vp,
-                                    C.c_size_t, vp]
+                                    C.c_size_t, C.POINTER(vp), vp]
     lib.cmsd_logit_pass.restype = C.c_int
     lib.cmsd_status_string.argtypes = [C.c_int]
     lib.cmsd_status_string.restype = C.c_char_p
@@ -130,6 +130,15 @@ def _buf(t: torch.Tensor, name: str, dtype: torch.dtype, min_elems: int, device:
         raise ValueError(f"{name} has {t.numel()} elements; {min_elems} are needed")
     if t.device != device:
         raise ValueError(f"{name} must be on {device}, not {t.device}")
+
+
+def _events(evs):
+    """A pair of torch.cuda.Event as the C array of two hipEvent_t, or None."""
+    if evs is None:
+        return None
+    if len(evs) != 2 or any(e.cuda_event == 0 for e in evs):
+        raise ValueError("row_events must be two torch.cuda.Event objects that have been recorded once")
+    return (C.c_void_p * 2)(evs[0].cuda_event, evs[1].cuda_event)
 
 
 def _check(fn: str, status: int) -> None:
@@ -287,11 +296,13 @@ def cmsd_logit_pass(draft_logits: torch.Tensor, target_logits: torch.Tensor, dra
                     draft_stats: torch.Tensor | None = None, draft_len: torch.Tensor | None = None,
                     target_stats: torch.Tensor | None = None, n_accepted: torch.Tensor | None = None,
                     next_token: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
-                    stream=None) -> dict:
+                    row_events=None, stream=None) -> dict:
     """Confidence, draft length and verification of a dense draft in one call.
     ``draft_logits`` [batch*k_max, V], ``target_logits`` [batch*(k_max+1), V] (same
     dtype), ``drafted`` int32 [batch*k_max], ``uniforms`` float32 [batch*(k_max+1)]
-    (None in GREEDY mode).  Returns the output tensors by name."""
+    (None in GREEDY mode).  ``row_events``: optional pair of recorded-once
+    ``torch.cuda.Event`` objects, recorded again around the row-pass kernel.  Returns
+    the output tensors by name."""
     drows, V, dst = _rows(draft_logits, "draft_logits")
     trows, V2, tst = _rows(target_logits, "target_logits")
     if V2 != V or target_logits.dtype != draft_logits.dtype:
@@ -336,5 +347,5 @@ def cmsd_logit_pass(draft_logits: torch.Tensor, target_logits: torch.Tensor, dra
         _dtype_code(target_logits), int(batch), int(k_max), V, C.byref(cp), C.byref(dp), C.byref(vp_),
         1 if adaptive else 0, _ptr(out["draft_stats"]), _ptr(out["draft_len"]), _ptr(out["target_stats"]),
         _ptr(out["n_accepted"]), _ptr(out["next_token"]), _ptr(workspace),
-        workspace.numel() * workspace.element_size(), _stream(stream)))
+        workspace.numel() * workspace.element_size(), _events(row_events), _stream(stream)))
     return out

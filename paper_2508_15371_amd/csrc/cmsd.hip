@@ -19,6 +19,11 @@
 //                   residual (or bonus) row.
 //   k_final_sample  one workgroup per sequence: slice scan, then an exact in-slice
 //                   inverse-CDF locate that repeats the scan's sums bit for bit.
+//   k_row_pass      cmsd_logit_pass's row pass: drafter rows (as k_confidence) and
+//                   dense target rows (as k_target_rows, decisions deferred) in one
+//                   grid.
+//   k_pass_decide   cmsd_logit_pass, one wave per sequence: draft length, accept
+//                   tests and first rejection, written once for the final kernels.
 //   k_draft_parts / k_draft_pick   the same slice machinery for one softmax sample
 //                   per drafter row.
 //
@@ -1134,9 +1139,8 @@ __device__ __forceinline__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo*
 
 // seq_info of the single-call pass: wave 0 reads the sequence's row results, drafter
 // stats, drafted ids and uniforms (one round trip, k_max < 64), forms the draft length
-// and every accept test (as the separate calls would), and with WRITE (the final
-// kernel) stores the draft length and the target-row records.
-template <bool WRITE>
+// and every accept test (as the separate calls would), and stores the draft length and
+// the target-row records.
 __device__ __forceinline__ SeqInfo seq_info_pass(const VerifyArgs& a, int b, SeqInfo* lds) {
   const int t = threadIdx.x, lane = t & 63;
   if (t < 64) {
@@ -1181,24 +1185,22 @@ __device__ __forceinline__ SeqInfo seq_info_pass(const VerifyArgs& a, int b, Seq
       q.msd = rl_f(dmx, c) * kLog2e;
       q.rho0 = (float)((double)(float)rl_d(sl.A, c) / (double)rl_f(dA, c));  // as from the verify slots
     }
-    if (WRITE) {
-      if (lane == 0) a.klen_out[b] = kb;
-      if (lane <= K) {
-        cmsd_target_stats res{};
-        res.max_logit = sl.m;
-        res.sum_exp = (float)sl.A;
-        res.top1 = sl.top1;
-        if (sl.st == -2) {
-          res = cmsd_target_stats{NAN, NAN, -1, -2, -1, {0, 0, 0}};
-        } else if (lane == kv || sl.st == -1) {
-          res.n_greater = -1;  // the final row
-          res.accept = -1;
-        } else {
-          res.n_greater = ng;
-          res.accept = acc;
-        }
-        a.tstats[off + lane] = res;
+    if (lane == 0) a.klen_out[b] = kb;
+    if (lane <= K) {
+      cmsd_target_stats res{};
+      res.max_logit = sl.m;
+      res.sum_exp = (float)sl.A;
+      res.top1 = sl.top1;
+      if (sl.st == -2) {
+        res = cmsd_target_stats{NAN, NAN, -1, -2, -1, {0, 0, 0}};
+      } else if (lane == kv || sl.st == -1) {
+        res.n_greater = -1;  // the final row
+        res.accept = -1;
+      } else {
+        res.n_greater = ng;
+        res.accept = acc;
       }
+      a.tstats[off + lane] = res;
     }
     if (lane == 0) *lds = q;
   }
@@ -1206,6 +1208,34 @@ __device__ __forceinline__ SeqInfo seq_info_pass(const VerifyArgs& a, int b, Seq
   const SeqInfo r = *lds;
   __syncthreads();
   return r;
+}
+
+// The sequence record of the single-call pass sits over the first two row slots of the
+// sequence (k_max >= 1), which k_pass_decide has read before it writes the record.
+static_assert(sizeof(SeqInfo) <= 2 * sizeof(PassSlot), "a sequence record fits two row slots");
+__device__ __forceinline__ SeqInfo* pass_info(const VerifyArgs& a, int b) {
+  return reinterpret_cast<SeqInfo*>(a.pslots + (int64_t)b * (a.k_max + 1));
+}
+
+// Decisions of the single-call pass, one wave per sequence: draft length, accept
+// tests, first rejection (seq_info_pass); the outputs of an invalid sequence and, in
+// GREEDY mode, the final outputs; and the sequence record that the final-token
+// kernels read in one load instead of repeating the decisions per slice.
+__global__ __launch_bounds__(64) void k_pass_decide(VerifyArgs a) {
+  __shared__ SeqInfo s_q;
+  const int b = blockIdx.x;
+  if (b >= a.B) return;
+  const SeqInfo q = seq_info_pass(a, b, &s_q);
+  if (threadIdx.x == 0) {
+    *pass_info(a, b) = q;
+    if (q.nacc < 0) {
+      a.n_acc[b] = -1;
+      a.next_tok[b] = -1;
+    } else if (a.mode == CMSD_MODE_GREEDY) {
+      a.n_acc[b] = q.nacc;
+      a.next_tok[b] = q.top1;
+    }
+  }
 }
 
 // Partial sums of one raw unit: e_t, e_d, q0 and e_d where q0 > 0.
@@ -1269,7 +1299,7 @@ __global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, in
   const int t = threadIdx.x;
   const int b = blockIdx.x / SW, sl0 = (blockIdx.x % SW) * kSubPerWG;
   if (b >= a.B) return;
-  const SeqInfo q = PASS ? seq_info_pass<false>(a, b, &s_q) : seq_info(a, b, &s_q);
+  const SeqInfo q = PASS ? *pass_info(a, b) : seq_info(a, b, &s_q);
   if (q.nacc < 0) return;
   const bool resid = q.nacc < q.kb;
   const T* trow = reinterpret_cast<const T*>(a.target) + q.tr * a.tstride;
@@ -1526,7 +1556,8 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
   const int t = threadIdx.x;
   const int b = blockIdx.x;
   if (b >= a.B) return;
-  const SeqInfo q = PASS ? seq_info_pass<true>(a, b, &s_q) : seq_info(a, b, &s_q);
+  const SeqInfo q = PASS ? *pass_info(a, b) : seq_info(a, b, &s_q);
+  if (PASS && (q.nacc < 0 || a.mode == CMSD_MODE_GREEDY)) return;  // written by k_pass_decide
   if (q.nacc < 0) {
     if (t == 0) {
       a.n_acc[b] = -1;
@@ -1887,9 +1918,10 @@ cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, cons
                             const cmsd_draft_params* draft, const cmsd_verify_params* verify, int32_t adaptive,
                             cmsd_row_stats* draft_stats, int32_t* draft_len, cmsd_target_stats* target_stats,
                             int32_t* n_accepted, int32_t* next_token, void* workspace, size_t workspace_bytes,
-                            void* stream) {
+                            void* const* row_events, void* stream) {
   if (dtype != CMSD_F32 && dtype != CMSD_BF16) return CMSD_ERR_DTYPE;
   if (!conf || !draft || !verify) return CMSD_ERR_ARG;
+  if (row_events && (!row_events[0] || !row_events[1])) return CMSD_ERR_ARG;
   if (batch < 0 || k_max < 1 || k_max > 63 || vocab < 2 || vocab > INT32_MAX) return CMSD_ERR_ARG;
   if (adaptive != 0 && adaptive != 1) return CMSD_ERR_ARG;
   VerifyArgs a{};
@@ -1941,15 +1973,19 @@ cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, cons
   static_assert(sizeof(PassSlot) == sizeof(RowSlot), "the pass uses the verify workspace layout");
   const unsigned gp = (unsigned)((int64_t)batch * SW);
   const int bd = row_block(drows + trows, vocab * (int64_t)es);
-  if (dtype == CMSD_F32) {
+  if (row_events && hipEventRecord(static_cast<hipEvent_t>(row_events[0]), st) != hipSuccess) return CMSD_ERR_LAUNCH;
+  if (dtype == CMSD_F32)
     launch_row_pass<float>(bd, a, drows + trows, st);
-    if (a.mode != CMSD_MODE_GREEDY)
-      hipLaunchKernelGGL((k_final_parts<float, true>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
+  else
+    launch_row_pass<Bf16>(bd, a, drows + trows, st);
+  if (row_events && hipEventRecord(static_cast<hipEvent_t>(row_events[1]), st) != hipSuccess) return CMSD_ERR_LAUNCH;
+  hipLaunchKernelGGL(k_pass_decide, dim3((unsigned)batch), dim3(64), 0, st, a);
+  if (a.mode == CMSD_MODE_GREEDY) return launched();  // the final token is the row's top token
+  if (dtype == CMSD_F32) {
+    hipLaunchKernelGGL((k_final_parts<float, true>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
     hipLaunchKernelGGL((k_final_sample<float, true>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   } else {
-    launch_row_pass<Bf16>(bd, a, drows + trows, st);
-    if (a.mode != CMSD_MODE_GREEDY)
-      hipLaunchKernelGGL((k_final_parts<Bf16, true>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
+    hipLaunchKernelGGL((k_final_parts<Bf16, true>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
     hipLaunchKernelGGL((k_final_sample<Bf16, true>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   }
   return launched();

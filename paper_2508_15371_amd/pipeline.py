@@ -94,3 +94,17 @@ class LogitPass:
         self.confidence(draft, stream)
         self.draft_len(stream)
         self.verify(draft, target, drafted, uniforms, stream)
+
+    def logit_pass(self, draft, target, drafted, uniforms, stream=None, row_events=None, adaptive=False) -> None:
+        """The same iteration as one cmsd_logit_pass call (dense target layout only):
+        drafter and target rows in one row pass, then the final-token pass.
+        ``adaptive``: verify only the first k_b drafts of each sequence."""
+        if not self.dense:
+            raise ValueError("cmsd_logit_pass takes the dense target layout; this LogitPass is packed")
+        p = self.p
+        cmsd.cmsd_logit_pass(draft, target, drafted, uniforms, batch=self.B, k_max=self.k_max, lambdas=p.lambdas,
+                             beta_margin=p.beta_margin, k_min=p.k_min, alpha=p.alpha, mode=p.mode,
+                             top_beta=p.top_beta, tau_base=p.tau_base, gamma=p.gamma, adaptive=adaptive,
+                             draft_stats=self.stats, draft_len=self.k, target_stats=self.tstats,
+                             n_accepted=self.n_acc, next_token=self.next_tok, workspace=self.ws,
+                             row_events=row_events, stream=stream)

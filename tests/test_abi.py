@@ -138,7 +138,7 @@ def _lpass(**kw):
     ref = lambda x: C.byref(x) if x is not None else None  # noqa: E731
     return cm.lib().cmsd_logit_pass(a["dl"], a["ds"], a["tl"], a["ts"], a["dr"], a["u"], a["dtype"], a["B"], a["K"],
                                     a["V"], ref(a["cp"]), ref(a["dp"]), ref(a["vp"]), a["ad"], a["dst"], a["kl"],
-                                    a["tst"], a["na"], a["nt"], a["ws"], a["wsb"], None)
+                                    a["tst"], a["na"], a["nt"], a["ws"], a["wsb"], a.get("ev"), None)
 
 
 @pytest.mark.parametrize("kw,want", [
@@ -166,6 +166,7 @@ def _lpass(**kw):
     (dict(kl=None), cm.CMSD_ERR_ARG),
     (dict(tl=P + 1), cm.CMSD_ERR_ARG),
     (dict(na=P + 2), cm.CMSD_ERR_ARG),
+    (dict(ev=(C.c_void_p * 2)(P, None)), cm.CMSD_ERR_ARG),          # an event pair with a null entry
     (dict(B=0, dl=None, tl=None, dr=None, ws=None, wsb=0), cm.CMSD_OK),
 ])
 def test_logit_pass_argument_errors(kw, want):

@@ -231,3 +231,29 @@ def test_empty_batch(cm):
                              torch.zeros(0, dtype=torch.float32, device=dev), batch=0, k_max=4)
     torch.cuda.synchronize()
     assert out["n_accepted"].numel() == 0
+
+
+def test_row_events_time_the_row_pass(cm):
+    # events handed to the call bracket the row-pass kernel on the call's stream and
+    # leave the outputs unchanged
+    cfg = W.CONFIGS["c2"]
+    d = Hn.workload("c2")
+    ref, _ = _pass(cm, d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"], cfg.B, cfg.k_max, O.MODE_CM)
+    ref = {k: v.clone() for k, v in ref.items()}
+    st = torch.cuda.Stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for e in ev:
+        e.record(st)
+    with pytest.raises(ValueError):
+        cm.cmsd_logit_pass(d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"], batch=cfg.B,
+                           k_max=cfg.k_max, row_events=ev[:1], stream=st)
+    out = cm.cmsd_logit_pass(d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"], batch=cfg.B,
+                             k_max=cfg.k_max, lambdas=Hn.PARAMS["lambdas"], beta_margin=Hn.PARAMS["beta_margin"],
+                             k_min=Hn.PARAMS["k_min"], alpha=Hn.PARAMS["alpha"], mode=O.MODE_CM,
+                             top_beta=Hn.PARAMS["top_beta"], tau_base=Hn.PARAMS["tau_base"],
+                             gamma=Hn.PARAMS["gamma"], row_events=ev, stream=st)
+    st.synchronize()
+    ms = ev[0].elapsed_time(ev[1])
+    assert 0.0 < ms < 100.0, ms
+    for k in ref:
+        assert torch.equal(out[k].view(torch.int32), ref[k].view(torch.int32)), k
