@@ -31,8 +31,8 @@ PEAK_HBM_GBS = 8000.0   # MI355X HBM3E
 # rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) scaled by what the same counters read
 # for a 1 GiB device copy (x2.0 and x1.0).  Valid only for the kernel source they were
 # taken on (sha256 prefix of the .hip file); otherwise "traffic" is reported null.
-TRAFFIC = {"kernel_sha256_16": "a0f3997e76f880ba", "k_confidence_c4": 1052.89e6 + 0.131e6,
-           "profile": "profiles/c4_cm_logit_pass.md"}
+TRAFFIC = {"kernel_sha256_16": "2fcb9e8e8d919dd6", "k_row_pass_c4": 2170.12e6 + 0.270e6,
+           "k_confidence_c4": 1052.89e6 + 0.131e6, "profile": "profiles/c4_cm_logit_pass.md"}
 
 
 def _cpu_baseline_worker(args):
