@@ -114,6 +114,9 @@ def main() -> int:
     ap.add_argument("--event-every", type=int, default=4, metavar="N",
                     help="bracket the roofline kernel with HIP events in every N-th timed step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-rotate", action="store_true",
+                    help="reuse one copy of the logits in every step (by default small workloads rotate "
+                         "copies totalling more than 512 MiB)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run device-to-device copies of MIB MiB (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -175,6 +178,11 @@ def main() -> int:
             a[1] = W.pack_device(a[1], lpg.k, lpg.off, K)
             a[3] = W.pack_device(a[3], lpg.k, lpg.off, K)
         groups.append((lpg, a, main if G == 1 else torch.cuda.Stream(dev)))
+    # successive steps read different copies of the logits, together more than 512 MiB
+    # (twice the 256 MB last-level cache), so no step finds rows a recent one left there
+    in_bytes = sum(a[0].nbytes + a[1].nbytes for _, a, _ in groups)
+    n_sets = 1 if args.no_rotate else max(1, -(-(512 << 20) // in_bytes))
+    sets = [[a] + [[a[0].clone(), a[1].clone(), a[2], a[3]] for _ in range(n_sets - 1)] for _, a, _ in groups]
     torch.cuda.synchronize()
     R_d = cfg.draft_rows
     R_t = sum(int(lpg.off[bg].item()) for lpg, _, _ in groups) if cfg.ragged else cfg.dense_target_rows
@@ -204,9 +212,9 @@ def main() -> int:
         lpg.verify(a[0], a[1], a[2], a[3], st)
 
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        for lpg, a, st in groups:
-            step(lpg, a, st)
+    for k in range(args.warmup):
+        for gi, (lpg, _, st) in enumerate(groups):
+            step(lpg, sets[gi][k % n_sets], st)
     torch.cuda.synchronize()
 
     # timed region: K steps.  HIP events on the launch stream bracket the roofline
@@ -221,9 +229,9 @@ def main() -> int:
             e[1].record(main)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for e in ev:
-        for gi, (lpg, a, st) in enumerate(groups):
-            step(lpg, a, st, e if gi == 0 else None)
+    for k, e in enumerate(ev):
+        for gi, (lpg, _, st) in enumerate(groups):
+            step(lpg, sets[gi][(args.warmup + k) % n_sets], st, e if gi == 0 else None)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_step = 1e3 * elapsed / args.steps
@@ -231,15 +239,16 @@ def main() -> int:
 
     # per-call split, one group after another on one stream (outside the timed region)
     ev2 = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(max(3, args.steps // 4))]
-    for e in ev2:
+    for i, e in enumerate(ev2):
+        cur = [(lpg, sets[gi][i % n_sets]) for gi, (lpg, _, _) in enumerate(groups)]
         e[0].record(main)
-        for lpg, a, _ in groups:
+        for lpg, a in cur:
             lpg.confidence(a[0], main)
         e[1].record(main)
-        for lpg, a, _ in groups:
+        for lpg, a in cur:
             lpg.draft_len(main)
         e[2].record(main)
-        for lpg, a, _ in groups:
+        for lpg, a in cur:
             lpg.verify(a[0], a[1], a[2], a[3], main)
         e[3].record(main)
     torch.cuda.synchronize()
@@ -288,7 +297,7 @@ def main() -> int:
                      "traffic": _traffic(rk, cfg.name) if G == 1 else None},
         "workload_stats": {"mean_n_acc": float(n_acc.mean()), "rejecting_sequences": rej,
                            "mean_draft_len": float(k_all.mean()), "streams": G,
-                           "path": "cmsd_logit_pass" if use_pass else "three calls"},
+                           "path": "cmsd_logit_pass" if use_pass else "three calls", "input_copies": n_sets},
     }
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)

@@ -635,12 +635,12 @@ __global__ __launch_bounds__(kDraftBD) void k_draft_len(const cmsd_row_stats* __
     if (b < B) {
       const cmsd_row_stats* p = stats + (int64_t)b * k_max;
       double s = 0.0;
-      for (int i0 = 0; i0 < k_max; i0 += 8) {
-        float c[8];
+      for (int i0 = 0; i0 < k_max; i0 += 16) {  // up to 16 loads in flight per thread
+        float c[16];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) c[j] = i0 + j < k_max ? p[i0 + j].conf : 0.f;
+        for (int j = 0; j < 16; ++j) c[j] = i0 + j < k_max ? p[i0 + j].conf : 0.f;
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
+        for (int j = 0; j < 16; ++j)
           if (i0 + j < k_max) s += (double)c[j];
       }
       const double x = (double)alpha * (s / (double)k_max) * (double)k_max;
