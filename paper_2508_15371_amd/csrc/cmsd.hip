@@ -983,13 +983,10 @@ __global__ __launch_bounds__(BD) void k_row_pass(VerifyArgs a) {
 // the target row, always handled as one raw 16-byte vector padded with -inf (whose
 // weights are exactly 0); slices are runs of kSliceUnits units.  Small slices and
 // one-wave partial groups keep every stage of this latency-bound pass short.
-#ifndef CMSD_PART_BD
-#define CMSD_PART_BD 64
-#endif
 #ifndef CMSD_SLICE_UNITS
 #define CMSD_SLICE_UNITS 256
 #endif
-constexpr int kPartBD = CMSD_PART_BD;
+constexpr int kPartBD = 64;  // one wave per slice group
 constexpr int kSliceUnits = CMSD_SLICE_UNITS;
 #ifndef CMSD_SUB_PER_WG
 #define CMSD_SUB_PER_WG 1
@@ -1261,23 +1258,22 @@ __device__ __forceinline__ void part_unit(const uint4& rt, const uint4& rd, floa
   }
 }
 
-// The kSubPerWG slices of one workgroup: every unit load of every slice is issued
-// before any is summed, so the group costs one memory latency.
-template <typename T, bool RESID>
-__device__ __forceinline__ void parts_group(const T* trow, const T* drow, const Geom& g, bool same_phase,
-                                            int64_t u_first, float mst, float msd, float rho0,
-                                            double (&sum)[kSubPerWG][4]) {
-  constexpr int BD = kPartBD, UPT = kSliceUnits / BD, NU = kSubPerWG * UPT;
-  const int t = threadIdx.x;
+// NSUB consecutive slices by one wave (lane = its lane index): every unit load of
+// every slice is issued before any is summed, so the wave costs one memory latency.
+template <typename T, bool RESID, int NSUB>
+__device__ __forceinline__ void parts_wave(const T* trow, const T* drow, const Geom& g, bool same_phase,
+                                           int64_t u_first, int lane, float mst, float msd, float rho0,
+                                           double (&sum)[NSUB][4]) {
+  constexpr int UPT = kSliceUnits / 64, NU = NSUB * UPT;
   uint4 rt[NU], rd[NU];
 #pragma unroll
   for (int j = 0; j < NU; ++j) {
-    const int64_t u = u_first + (int64_t)j * BD + t;
+    const int64_t u = u_first + (int64_t)j * 64 + lane;
     rt[j] = unit_raw<T, true>(trow, g, u);
     if (RESID) rd[j] = unit_raw2<T, true>(drow, g, u, same_phase);
   }
 #pragma unroll
-  for (int k = 0; k < kSubPerWG; ++k) {
+  for (int k = 0; k < NSUB; ++k) {
 #pragma unroll
     for (int jj = 0; jj < UPT; ++jj) {
       const int j = k * UPT + jj;
@@ -1313,9 +1309,9 @@ __global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, in
   const int64_t u_first = (int64_t)sl0 * kSliceUnits;
   if (u_first < nu) {
     if (resid)
-      parts_group<T, true>(trow, drow, g, same_phase, u_first, mst, msd, rho0, sum);
+      parts_wave<T, true, kSubPerWG>(trow, drow, g, same_phase, u_first, t, mst, msd, rho0, sum);
     else
-      parts_group<T, false>(trow, trow, g, true, u_first, mst, 0.f, 0.f, sum);
+      parts_wave<T, false, kSubPerWG>(trow, trow, g, true, u_first, t, mst, 0.f, 0.f, sum);
   }
   double ws_w[kSubPerWG][4];
 #pragma unroll
@@ -1382,22 +1378,26 @@ __device__ __forceinline__ double block_excl_scan(double v, double* sd) {
   return pre + ex;
 }
 
-// Units of one slice per thread of the sampling workgroup.
-constexpr int kLocUPT = kSliceUnits / kSampleBD;
-static_assert(kLocUPT * kSampleBD == kSliceUnits, "a slice splits evenly over the sampling workgroup");
+// Units of one slice per thread of a BD-thread sampling workgroup (one each, and
+// none for the threads past the slice, when the workgroup is wider than a slice).
+template <int BD>
+constexpr int loc_upt() {
+  return BD >= kSliceUnits ? 1 : kSliceUnits / BD;
+}
+static_assert(kSliceUnits % kSampleBD == 0, "a slice splits evenly over the sampling workgroup");
 
 // Smallest element y in units [ulo, uhi) with q_y > 0 and base + C(y) > x, C the
-// cumulative weight from ulo in a fixed order: thread t owns the kLocUPT units from
-// ulo + t*kLocUPT (kept in registers) and sums them unit by unit, a block scan
+// cumulative weight from ulo in a fixed order: thread t owns the loc_upt<BD>() units
+// from ulo + t*loc_upt<BD>() (kept in registers) and sums them unit by unit, a block scan
 // orders the threads, and the thread whose span crosses x repeats its own sums
 // exactly.  If none qualifies, the last element with q_y > 0.  Returns -1 if every
 // weight is 0.  The result passes through *s_y.
-template <typename T, bool RESID>
+template <typename T, bool RESID, int BD>
 __device__ __forceinline__ int locate_units(const T* trow, const T* drow, const Geom& g, bool same_phase, int64_t ulo, int64_t uhi,
                             float mst, float msd, double rho, double base, double x, double* sd, int* si,
                             int* s_y) {
   using E = Elem<T>;
-  constexpr int BD = kSampleBD, VEC = E::VEC, UPT = kLocUPT;
+  constexpr int VEC = E::VEC, UPT = loc_upt<BD>();
   const int t = threadIdx.x;
   const int64_t u0 = ulo + (int64_t)t * UPT;
   uint4 rt[UPT], rd[UPT];
@@ -1466,12 +1466,12 @@ __device__ __forceinline__ int locate_units(const T* trow, const T* drow, const 
 // slice masses corrected to first order in rho - rho0 and scanned in slice order
 // (each thread a contiguous run of slices, its first partial kept in registers),
 // then an exact scan/locate inside the chosen slice.  A zero residual falls back to
-// the target row.  Run by one workgroup of kSampleBD threads; s_sc holds 3 doubles.
-template <typename T>
+// the target row.  Run by one workgroup of BD threads; s_sc holds 3 doubles, sd
+// 2*BD/64 and si BD/64.
+template <typename T, int BD>
 __device__ __forceinline__ int sample_from_parts(const T* trow, const T* drow, int64_t V, bool resid, float mst, float msd,
                                  float rho0, float u, const SlicePart* __restrict__ P, int S, double* sd, int* si,
                                  double* s_sc, int* s_y) {
-  constexpr int BD = kSampleBD;
   const int t = threadIdx.x;
   const bool same_phase = ((reinterpret_cast<uintptr_t>(trow) ^ reinterpret_cast<uintptr_t>(drow)) & 15u) == 0;
   const int slo = (int)((int64_t)t * S / BD), shi = (int)((int64_t)(t + 1) * S / BD);
@@ -1533,9 +1533,9 @@ __device__ __forceinline__ int sample_from_parts(const T* trow, const T* drow, i
     const int64_t ulo = (int64_t)s_sc[2] * kSliceUnits;
     const int64_t uhi = ulo + kSliceUnits < nu ? ulo + kSliceUnits : nu;
     if (resid)
-      y = locate_units<T, true>(trow, drow, g, same_phase, ulo, uhi, mst, msd, rho, sbase, x, sd, si, s_y);
+      y = locate_units<T, true, BD>(trow, drow, g, same_phase, ulo, uhi, mst, msd, rho, sbase, x, sd, si, s_y);
     else
-      y = locate_units<T, false>(trow, trow, g, true, ulo, uhi, mst, mst, 0.0, sbase, x, sd, si, s_y);
+      y = locate_units<T, false, BD>(trow, trow, g, true, ulo, uhi, mst, mst, 0.0, sbase, x, sd, si, s_y);
     if (y < 0 && resid) {
       resid = false;
       continue;
@@ -1577,7 +1577,7 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
   const T* trow = reinterpret_cast<const T*>(a.target) + q.tr * a.tstride;
   const T* drow = reinterpret_cast<const T*>(a.draft) + q.dr * a.dstride;
   const float u = a.unif[q.off + q.kb];
-  const int y = sample_from_parts<T>(trow, drow, a.V, resid, q.mst, q.msd, q.rho0, u, ws + (int64_t)b * S, S, sd,
+  const int y = sample_from_parts<T, BD>(trow, drow, a.V, resid, q.mst, q.msd, q.rho0, u, ws + (int64_t)b * S, S, sd,
                                      si, s_sc, &s_y);
   if (t == 0) {
     a.n_acc[b] = nacc;
@@ -1604,7 +1604,7 @@ __global__ __launch_bounds__(kPartBD) void k_draft_parts(const T* __restrict__ l
   const float mst = stats[r].max_logit * kLog2e;
   double sum[kSubPerWG][4] = {};
   const int64_t u_first = (int64_t)sl0 * kSliceUnits;
-  if (u_first < nu) parts_group<T, false>(row, row, g, true, u_first, mst, 0.f, 0.f, sum);
+  if (u_first < nu) parts_wave<T, false, kSubPerWG>(row, row, g, true, u_first, threadIdx.x, mst, 0.f, 0.f, sum);
   double w_[kSubPerWG];
 #pragma unroll
   for (int k = 0; k < kSubPerWG; ++k) w_[k] = wave_all_d(sum[k][0], OpSumD());
@@ -1633,7 +1633,7 @@ __global__ __launch_bounds__(kSampleBD) void k_draft_pick(const T* __restrict__ 
   __shared__ int s_y;
   const int64_t r = blockIdx.x;
   const T* row = logits + r * stride;
-  const int y = sample_from_parts<T>(row, row, V, false, stats[r].max_logit * kLog2e, 0.f, 0.f, unif[r], ws + r * S,
+  const int y = sample_from_parts<T, kSampleBD>(row, row, V, false, stats[r].max_logit * kLog2e, 0.f, 0.f, unif[r], ws + r * S,
                                      S, sd, si, s_sc, &s_y);
   if (threadIdx.x == 0) out[r] = y;
 }
