@@ -437,10 +437,14 @@ __device__ __forceinline__ cmsd_row_stats row_stats_record(float m, float z2, do
 
 // One drafter row -> its stats record (and, with VAR, its logit variance), by one
 // workgroup of BD threads.
+#ifndef CMSD_KEEP_MAX_ROUND
+#define CMSD_KEEP_MAX_ROUND 1
+#endif
 template <typename T, int BD, bool VAR>
 __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, const ConfArgs& a,
                                          cmsd_row_stats* __restrict__ out, float* __restrict__ var_out) {
   using E = Elem<T>;
+  constexpr bool KEEP = CMSD_KEEP_MAX_ROUND && BD == 64;
   constexpr int VEC = E::VEC, U = E::U, N = VEC * U;
   constexpr int ND = VAR ? 5 : 2;  // fp64 sums of the epilogue: A, T (+ count, S1, S2)
   __shared__ double sd[(VAR ? 3 : 1) * (BD / 64)];
@@ -457,6 +461,11 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
 
     ConfState s;
     if (t < g.head) conf_one<VAR>(s, E::load(row + t), 0);
+    // KEEP: the vectors of the round that set this thread's maximum stay in registers,
+    // so the epilogue finds the max index without reading that round again
+    uint4 keep[KEEP ? U : 1];
+#pragma unroll
+    for (int u = 0; u < (KEEP ? U : 1); ++u) keep[u] = make_uint4(0u, 0u, 0u, 0u);
 
     // full rounds, next round's loads issued before the current one is consumed
     stream_rounds<U, BD, CMSD_STREAM_DEPTH>(vp, nr, t, [] {}, [&](const uint4 (&raw)[U], int64_t k) {
@@ -464,6 +473,16 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
 #pragma unroll
       for (int u = 0; u < U; ++u) E::unpack(raw[u], f + u * VEC);
       conf_chunk<N, false, VAR>(s, f, 0xffffffffu, int(k + 1));
+      if (KEEP) {
+        const bool up = s.gid == int(k + 1);
+#pragma unroll
+        for (int u = 0; u < (KEEP ? U : 1); ++u) {
+          keep[u].x = up ? raw[u].x : keep[u].x;
+          keep[u].y = up ? raw[u].y : keep[u].y;
+          keep[u].z = up ? raw[u].z : keep[u].z;
+          keep[u].w = up ? raw[u].w : keep[u].w;
+        }
+      }
     });
     // partial round
     const int64_t rb = nr * per_round;
@@ -496,7 +515,23 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
     const bool is_max = s.t1 == m;
     int64_t idx = INT64_MAX;
     float other = -INFINITY;
-    if (is_max) rescan_chunk<T, BD>(row, g, nr, s.gid, m, idx, other);
+    if (is_max) {
+      if (KEEP && s.gid >= 1 && s.gid <= nr) {
+#pragma unroll
+        for (int u = 0; u < (KEEP ? U : 1); ++u) {
+          float fv[VEC];
+          E::unpack(keep[u], fv);
+          const int64_t j = (int64_t)(s.gid - 1) * U * BD + (int64_t)u * BD + t;
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            if (idx == INT64_MAX && fv[e] == m) idx = g.head + j * VEC + e;
+            else other = fmaxf(other, fv[e]);
+          }
+        }
+      } else {
+        rescan_chunk<T, BD>(row, g, nr, s.gid, m, idx, other);
+      }
+    }
     const float contrib = is_max ? s.t2 : s.t1;
     const int idx32 = idx == INT64_MAX ? INT32_MAX : int(idx);
 
