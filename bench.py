@@ -117,6 +117,9 @@ def main() -> int:
     ap.add_argument("--event-every", type=int, default=4, metavar="N",
                     help="bracket the roofline kernel with HIP events in every N-th timed step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--capacity-rows", action="store_true",
+                    help="ragged workload: pass verify all B*(k_max+1) allocated target rows instead of "
+                         "the sum(k_b+1) rows the verifier scored")
     ap.add_argument("--no-rotate", action="store_true",
                     help="reuse one copy of the logits in every step (by default small workloads rotate "
                          "copies totalling more than 512 MiB)")
@@ -180,6 +183,10 @@ def main() -> int:
             lpg.draft_len(main)
             a[1] = W.pack_device(a[1], lpg.k, lpg.off, K)
             a[3] = W.pack_device(a[3], lpg.k, lpg.off, K)
+            if not args.capacity_rows:
+                # the verifier scored exactly sum(k_b + 1) rows: hand verify that many
+                rt = int(lpg.off[bg].item())
+                a[1], a[3] = a[1][:rt], a[3][:rt]
         groups.append((lpg, a, main if G == 1 else torch.cuda.Stream(dev)))
     # successive steps read different copies of the logits, together more than 512 MiB
     # (twice the 256 MB last-level cache), so no step finds rows a recent one left there

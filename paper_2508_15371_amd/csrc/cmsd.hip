@@ -898,21 +898,35 @@ __device__ __forceinline__ void target_row(const VerifyArgs& a, int64_t r) {
       count = has_draft && a.mode != CMSD_MODE_STANDARD && a.beta > 0;
       return;
     }
-    // sequence owning row r: number of offsets[1..B] that are <= r
-    int cnt = 0;
-    for (int j = 1 + t; j <= a.B; j += BD) cnt += a.off[j] <= r ? 1 : 0;
+    // sequence owning row r, from one scan of the offsets: b = #{j in 1..B : off[j] <= r},
+    // and (for non-decreasing offsets) off[b] = the largest offset <= r and off[b+1] =
+    // the smallest offset[1..B] > r, so no second round trip fetches them
+    int cnt = 0, lo = INT32_MIN, hi = INT32_MAX;
+    for (int j = t; j <= a.B; j += BD) {
+      const int o = a.off[j];
+      if (o <= r) {
+        cnt += j >= 1 ? 1 : 0;
+        lo = o > lo ? o : lo;
+      } else if (j >= 1) {
+        hi = o < hi ? o : hi;
+      }
+    }
     b = block_all_i<BD>(cnt, OpSumI(), si);
     b = b < a.B ? b : a.B - 1;
-    const int64_t off_b = a.off[b], off_b1 = a.off[b + 1];
+    const int64_t off_b = block_all_i<BD>(lo, OpMaxI(), si), off_b1 = block_all_i<BD>(hi, OpMinI(), si);
+    i = off_b >= 0 ? int(r - off_b) : 0;  // r - off[b] (no offset <= r: the layout check fails)
+    // the draft length and, for a position inside the k_max drafts, its id and drafter
+    // stats in one round trip (all in bounds whatever the layout check finds)
+    const bool in_k = off_b >= 0 && i < a.k_max;
+    const int64_t drow = (int64_t)b * a.k_max + (in_k ? i : 0);
     const int kb = a.klen[b];
+    const int y = in_k ? a.drafted[drow] : -1;
+    const cmsd_row_stats ds = in_k ? a.dstats[drow] : cmsd_row_stats{};
     layout = kb >= 0 && kb <= a.k_max && off_b >= 0 && off_b <= r && r < off_b1 && off_b1 == off_b + kb + 1 &&
              off_b1 <= a.target_rows;
     valid = layout;
-    i = int(r - off_b);
     has_draft = valid && i < kb;
     if (has_draft) {
-      const int64_t drow = (int64_t)b * a.k_max + i;
-      const int y = a.drafted[drow];
       yd = y;
       if (y < 0 || (int64_t)y >= a.V) {
         valid = false;
@@ -920,7 +934,6 @@ __device__ __forceinline__ void target_row(const VerifyArgs& a, int64_t r) {
       } else {
         gz = E::load(trow + y);
         zd = E::load(reinterpret_cast<const T*>(a.draft) + drow * a.dstride + y);
-        const cmsd_row_stats ds = a.dstats[drow];
         cm = ds.conf;
         dm = ds.max_logit;
         dA = ds.sum_exp;
