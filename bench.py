@@ -31,10 +31,10 @@ PEAK_HBM_GBS = 8000.0   # MI355X HBM3E
 # runs (FETCH_SIZE, WRITE_SIZE) scaled by what the same counters read for a 1 GiB
 # device copy (x2.0 and x1.0).  Valid only for the kernel source they were
 # taken on (sha256 prefix of the .hip file); otherwise "traffic" is reported null.
-TRAFFIC = {"kernel_sha256_16": "0de29425dec8dcab",
+TRAFFIC = {"kernel_sha256_16": "77f91c046ed92004",
            "k_row_pass_c4": 2170.13e6 + 0.270e6, "k_confidence_c4": 1052.89e6 + 0.131e6,
-           "k_confidence_c5": 524.63e6 + 0.262e6, "k_row_pass_c3": 113.90e6 + 0.035e6,
-           "k_row_pass_c2": 9.06e6 + 0.004e6, "k_row_pass_v152k": 331.58e6 + 0.035e6,
+           "k_confidence_c5": 524.63e6 + 0.262e6, "k_row_pass_c3": 113.86e6 + 0.035e6,
+           "k_row_pass_c2": 9.07e6 + 0.004e6, "k_row_pass_v152k": 331.59e6 + 0.035e6,
            "profile": "profiles/<workload>_cm_logit_pass.md"}
 
 
