@@ -27,6 +27,11 @@
 //   k_draft_parts / k_draft_pick   the same slice machinery for one softmax sample
 //                   per drafter row.
 //
+// Compile-time tuning knobs (defaults are the measured best on gfx950): CMSD_STREAM_DEPTH
+// (row-pass rounds of loads in flight), CMSD_KEEP_MAX_ROUND (64-thread drafter rows keep
+// their max round in registers), CMSD_SLICE_UNITS and CMSD_SUB_PER_WG (final-token slice
+// size and slices per one-wave workgroup).
+//
 // Numerics: exponentials are evaluated as 2^(z*log2e - m*log2e) with one FMA and
 // v_exp_f32; per-thread partial sums are fp32 over 32-element chunks, the
 // cross-thread combines and every decision-side formula are fp64.  Reductions have
