@@ -1870,9 +1870,9 @@ cmsd_status cmsd_draft_sample(const void* logits, int32_t dtype, int64_t n_rows,
 }
 
 size_t cmsd_verify_workspace_bytes(int32_t batch, int32_t k_max, int64_t vocab) {
+  static_assert(sizeof(RowSlot) == 32 && sizeof(SlicePart) == 32, "workspace record sizes");
   if (batch <= 0 || k_max < 1 || k_max > 4096 || vocab < 2 || vocab > INT32_MAX) return 0;
   return (size_t)batch * ((size_t)verify_slices(vocab, 4) * sizeof(SlicePart) + (size_t)(k_max + 1) * sizeof(RowSlot));
-  static_assert(sizeof(RowSlot) == 32 && sizeof(SlicePart) == 32, "workspace record sizes");
 }
 
 cmsd_status cmsd_confidence(const void* logits, int32_t dtype, int64_t n_rows, int64_t vocab, int64_t row_stride,
