@@ -257,3 +257,54 @@ def test_row_events_time_the_row_pass(cm):
     assert 0.0 < ms < 100.0, ms
     for k in ref:
         assert torch.equal(out[k].view(torch.int32), ref[k].view(torch.int32)), k
+
+
+class _DeviceRows:
+    """Rows of a device bf16 matrix, fetched one at a time as stored bits."""
+
+    def __init__(self, t):
+        self.t = t
+
+    def __getitem__(self, r):
+        return self.t[r].view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def test_large_batch_past_int32_elements(cm):
+    # 1000 sequences of 16 drafts at V = 128256: 16000 drafter rows (2.05e9 logits) and
+    # 17000 target rows (2.18e9), so element offsets pass 2^31 in both arrays; the
+    # inputs come from torch's seeded generator on the device; sampled sequences at
+    # the start, middle and end are checked against the oracle, and the three
+    # separate calls must give the same bits
+    from paper_2508_15371_amd import pipeline
+    B, K, V = 1000, 16, 128256
+    dev = torch.device("cuda:0")
+    print(f"[logit pass large] B={B} K={K} V={V}", flush=True)
+    g = torch.Generator(device=dev).manual_seed(1234)
+    sig = torch.exp(torch.empty(B * K, 1, device=dev).uniform_(math.log(0.3), math.log(10.0), generator=g))
+    draft = torch.empty(B * K, V, dtype=torch.bfloat16, device=dev)
+    target = torch.empty(B * (K + 1), V, dtype=torch.bfloat16, device=dev)
+    drafted = torch.empty(B * K, dtype=torch.int32, device=dev)
+    for c0 in range(0, B, 100):               # 100 sequences at a time
+        c1 = c0 + 100
+        z = torch.randn((c1 - c0) * K, V, device=dev, generator=g) * sig[c0 * K:c1 * K]
+        draft[c0 * K:c1 * K] = z.to(torch.bfloat16)
+        zd = draft[c0 * K:c1 * K].float()
+        gum = -torch.log(-torch.log(torch.rand(zd.shape, device=dev, generator=g).clamp_(1e-12, 1.0 - 1e-7)))
+        drafted[c0 * K:c1 * K] = torch.argmax(zd + gum, dim=1).to(torch.int32)
+        t3 = target[c0 * (K + 1):c1 * (K + 1)].view(c1 - c0, K + 1, V)
+        t3[:, :K] = (zd + 0.5 * torch.randn(zd.shape, device=dev, generator=g)).view(c1 - c0, K, V).to(torch.bfloat16)
+        t3[:, K] = (2.0 * torch.randn(c1 - c0, V, device=dev, generator=g)).to(torch.bfloat16)
+        del z, zd, gum
+    unif = (torch.randint(0, 1 << 24, (B * (K + 1),), device=dev, generator=g).float() * 2.0 ** -24).contiguous()
+    out, P = _pass(cm, draft, target, drafted, unif, B, K, O.MODE_CM)
+    t = Hn.Tally()
+    n_acc, _ = _check(t, B, K, V, "bf16", _DeviceRows(draft), _DeviceRows(target), drafted.view(B, K).cpu().numpy(),
+                      unif.view(B, K + 1).cpu().numpy(), out, P, O.MODE_CM, False, [0, 1, 499, 998, 999])
+    print(f"[logit pass large] checked={t.checked} exceptions={t.exceptions} mean n_acc={n_acc.mean():.3f}", flush=True)
+    t.assert_ok()
+    lp = pipeline.LogitPass(B, K, V, dev, pipeline.Params(mode=O.MODE_CM))
+    lp.run(draft, target, drafted, unif)
+    torch.cuda.synchronize()
+    for k, ref in {"draft_stats": lp.stats, "draft_len": lp.k, "target_stats": lp.tstats, "n_accepted": lp.n_acc,
+                   "next_token": lp.next_tok}.items():
+        assert torch.equal(out[k].view(torch.int32), ref.view(torch.int32)), k
