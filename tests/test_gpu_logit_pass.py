@@ -308,3 +308,38 @@ def test_large_batch_past_int32_elements(cm):
     for k, ref in {"draft_stats": lp.stats, "draft_len": lp.k, "target_stats": lp.tstats, "n_accepted": lp.n_acc,
                    "next_token": lp.next_tok}.items():
         assert torch.equal(out[k].view(torch.int32), ref.view(torch.int32)), k
+
+
+@pytest.mark.parametrize("mode", [O.MODE_CM, O.MODE_GREEDY])
+def test_graph_capture_replays_match_eager(cm, mode):
+    # one cmsd_logit_pass call allocates and synchronises nothing, so it can be captured
+    # in a HIP graph: every replay (with eager work in between) matches the eager run
+    from paper_2508_15371_amd import pipeline
+    cfg = W.CONFIGS["c3"]
+    d = Hn.workload("c3")
+    args = (d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"])
+    ref = pipeline.LogitPass(cfg.B, cfg.k_max, cfg.V, "cuda:0", pipeline.Params(mode=mode))
+    ref.logit_pass(*args)
+    torch.cuda.synchronize()
+    fields = ("stats", "k", "tstats", "n_acc", "next_tok")
+    want = {f: getattr(ref, f).clone() for f in fields}
+    lp = pipeline.LogitPass(cfg.B, cfg.k_max, cfg.V, "cuda:0", pipeline.Params(mode=mode))
+    lp.logit_pass(*args)                           # warm-up outside the capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        lp.logit_pass(*args)
+    junk = torch.zeros(1 << 20, device="cuda:0")
+    for rep in range(4):
+        lp.stats.fill_(float("nan"))
+        lp.tstats.fill_(float("nan"))
+        lp.k.fill_(-7)
+        lp.n_acc.fill_(-7)
+        lp.next_tok.fill_(-7)
+        junk.add_(1.0)                             # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for f in fields:
+            a, b = getattr(lp, f), want[f]
+            assert torch.equal(a.view(torch.int32), b.view(torch.int32)), (rep, f)
