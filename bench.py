@@ -32,10 +32,10 @@ PEAK_HBM_GBS = 8000.0   # MI355X HBM3E
 # device copy (x2.0 and x1.0).  Valid only for the kernel code they were taken on
 # (kernel_code_hash(): sha256 prefix of the .hip file's code without comments);
 # otherwise "traffic" is reported null.
-TRAFFIC = {"kernel_code_sha256_16": "ef78fb7779f2d0b2",
+TRAFFIC = {"kernel_code_sha256_16": "be3b1d2f74103a92",
            "k_row_pass_c4": 2170.13e6 + 0.270e6, "k_confidence_c4": 1052.89e6 + 0.131e6,
-           "k_confidence_c5": 524.63e6 + 0.262e6, "k_row_pass_c3": 113.86e6 + 0.035e6,
-           "k_row_pass_c2": 9.07e6 + 0.004e6, "k_row_pass_v152k": 331.59e6 + 0.035e6,
+           "k_confidence_c5": 524.63e6 + 0.262e6, "k_row_pass_c3": 113.88e6 + 0.035e6,
+           "k_row_pass_c2": 9.07e6 + 0.004e6, "k_row_pass_v152k": 331.58e6 + 0.035e6,
            "profile": "profiles/<workload>_cm_logit_pass.md"}
 
 
@@ -208,12 +208,6 @@ def main() -> int:
     torch.cuda.synchronize()
     R_d = cfg.draft_rows
     R_t = sum(int(lpg.off[bg].item()) for lpg, _, _ in groups) if cfg.ragged else cfg.dense_target_rows
-    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        for lpg, a, st in groups:
-            lpg.run(*a, st)
-    torch.cuda.synchronize()
-
     # one cmsd_logit_pass call per step on dense workloads (one stream), else the three calls
     use_pass = args.path == "pass" or (args.path == "auto" and not cfg.ragged)
     if use_pass and (cfg.ragged or G != 1):
