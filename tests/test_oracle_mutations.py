@@ -32,6 +32,17 @@ MUTATIONS = [
     ("q = np.maximum(0.0, p_t - p_d)", "q = np.maximum(0.0, p_d - p_t)", "residual sign"),
     ("t = z_t_rows[k_b]", "t = z_t_rows[k_b - 1]", "bonus row index"),
     ("hit = np.nonzero(c > x)[0]", "hit = np.nonzero(c >= x)[0]", ">= vs > in the inverse CDF"),
+    ("top1 = int(np.argmax(z))  ", "top1 = int(z.size - 1 - np.argmax(z[::-1]))  ", "highest instead of lowest max index"),
+    ("p1_minus_p2 = float(p[top1]) - p2", "p1_minus_p2 = float(p[top1]) + p2", "softmax-margin sign"),
+    ("off[1:] = np.cumsum(k.astype(np.int64) + 1)", "off[1:] = np.cumsum(k.astype(np.int64))",
+     "offsets without the final row"),
+    ("gap = rs_t.m - zy if", "gap = zy - rs_t.m if", "gap sign"),
+    ("exact = y == int(np.argmax(z_t))", "exact = y == int(np.argmax(z_t)) or y == 0", "GREEDY exact-match test"),
+    ("            return i\n", "            return i + 1\n", "prefix keeps the first rejected draft"),
+    ("p_d = np.exp(z_d - rs_d.m) / rs_d.A", "p_d = np.exp(z_d - rs_d.m) / rs_t.A",
+     "residual with the target's normaliser on the drafter row"),
+    ("return int(np.argmax(z_t_rows[min(n_acc, k_b)]))", "return int(np.argmax(z_t_rows[k_b]))",
+     "GREEDY final token from the bonus row after a rejection"),
 ]
 
 
@@ -52,19 +63,43 @@ def _run_pins(cwd):
                           cwd=cwd, capture_output=True, text=True, timeout=900)
 
 
-def test_unmodified_copy_passes(tmp_path):
-    _scratch_copy(str(tmp_path))
-    r = _run_pins(str(tmp_path))
-    assert r.returncode == 0, r.stdout[-3000:]
+def _mutated_run(base, idx):
+    """Run the pins against a scratch copy of the oracle carrying mutation idx
+    (idx = -1: the unmodified oracle); returns (returncode, output tail)."""
+    d = os.path.join(base, f"m{idx}")
+    _scratch_copy(d)
+    if idx >= 0:
+        orig, mutant, what = MUTATIONS[idx]
+        path = os.path.join(d, "oracle", "cmsd_oracle.py")
+        src = open(path).read()
+        if src.count(orig) != 1:
+            return -1, f"the oracle no longer contains the line for: {what}"
+        with open(path, "w") as f:
+            f.write(src.replace(orig, mutant))
+    r = _run_pins(d)
+    return r.returncode, r.stdout[-3000:]
 
 
-@pytest.mark.parametrize("orig,mutant,what", MUTATIONS, ids=[m[2] for m in MUTATIONS])
-def test_planted_mistake_fails_a_pin(tmp_path, orig, mutant, what):
-    _scratch_copy(str(tmp_path))
-    path = os.path.join(str(tmp_path), "oracle", "cmsd_oracle.py")
-    src = open(path).read()
-    assert src.count(orig) == 1, f"the oracle no longer contains the line for: {what}"
-    with open(path, "w") as f:
-        f.write(src.replace(orig, mutant))
-    r = _run_pins(str(tmp_path))
-    assert r.returncode == 1, f"no pin caught: {what}\n{r.stdout[-3000:]}"
+@pytest.fixture(scope="module")
+def runs(tmp_path_factory):
+    """Every mutated copy (and the unmodified one) runs the pins, in parallel."""
+    from concurrent.futures import ThreadPoolExecutor
+    base = str(tmp_path_factory.mktemp("oracle_mutations"))
+    try:
+        ncpu = len(os.sched_getaffinity(0))
+    except AttributeError:
+        ncpu = os.cpu_count() or 1
+    idx = list(range(-1, len(MUTATIONS)))
+    with ThreadPoolExecutor(max(1, min(8, ncpu))) as ex:
+        return dict(zip(idx, ex.map(lambda i: _mutated_run(base, i), idx)))
+
+
+def test_unmodified_copy_passes(runs):
+    rc, out = runs[-1]
+    assert rc == 0, out
+
+
+@pytest.mark.parametrize("i", range(len(MUTATIONS)), ids=[m[2] for m in MUTATIONS])
+def test_planted_mistake_fails_a_pin(runs, i):
+    rc, out = runs[i]
+    assert rc == 1, f"no pin caught: {MUTATIONS[i][2]}\n{out}"
