@@ -343,3 +343,31 @@ def test_graph_capture_replays_match_eager(cm, mode):
         for f in fields:
             a, b = getattr(lp, f), want[f]
             assert torch.equal(a.view(torch.int32), b.view(torch.int32)), (rep, f)
+
+
+@pytest.mark.parametrize("mode,kw", [
+    (O.MODE_CM, dict(gamma=-1.0)),                               # the prose's direction: confident -> lenient
+    (O.MODE_CM, dict(gamma=3.0, tau_base=0.0)),
+    (O.MODE_CM, dict(top_beta=1, tau_base=2.0, gamma=0.0)),
+    (O.MODE_CM, dict(top_beta=10, tau_base=0.5)),
+    (O.MODE_CM, dict(top_beta=0)),                               # gate off: standard speculative sampling
+    (O.MODE_CM, dict(alpha=0.3, k_min=2)),
+    (O.MODE_CM, dict(lambdas=(1.0, 0.0, 0.0), beta_margin=0.25)),
+    (O.MODE_GREEDY, dict(top_beta=1, tau_base=0.0, gamma=-0.5)),
+    (O.MODE_GREEDY, dict(top_beta=5, tau_base=1.0, gamma=2.0)),
+], ids=["gamma-1", "gamma3-tau0", "beta1-tau2", "beta10", "beta0", "alpha0.3-kmin2", "entropy-only",
+        "greedy-beta1", "greedy-beta5"])
+@pytest.mark.parametrize("adaptive", [False, True])
+def test_parameter_settings(cm, mode, kw, adaptive):
+    # the gate, threshold, draft-length and confidence parameters away from their
+    # defaults, on c3 (odd V), 16 sequences against the oracle
+    cfg = W.CONFIGS["c3"]
+    d = Hn.workload("c3")
+    out, P = _pass(cm, d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"], cfg.B, cfg.k_max, mode,
+                   adaptive, **kw)
+    t = Hn.Tally()
+    n_acc, k = _check(t, cfg.B, cfg.k_max, cfg.V, cfg.dtype, d["draft"], d["target"], d["drafted"], d["uniforms"],
+                      out, P, mode, adaptive, _seqs(cfg.B, 16, 77), stats_rows=False)
+    print(f"[logit pass params] {kw} mode={mode} adaptive={adaptive}: checked={t.checked} exceptions={t.exceptions} "
+          f"mean n_acc={n_acc.mean():.3f} mean k={k.mean():.3f}", flush=True)
+    t.assert_ok()
