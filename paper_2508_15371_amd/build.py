@@ -33,8 +33,25 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libcmsd.so)")
 
 
+NATIVE_SRC = os.path.join(ROOT, "tests", "native", "logit_pass_native.cpp")
+NATIVE_BIN = os.path.join(ROOT, "tests", "native", "logit_pass_native")
+
+
+def build_native(verbose: bool = False) -> str:
+    """Compile the native (C++, no Python) test consumer of libcmsd.so; returns its path."""
+    cmd = [hipcc(), "-O2", "-std=c++17", "-I", INC, "-o", NATIVE_BIN, NATIVE_SRC, "-L", PKG, "-lcmsd",
+           f"-Wl,-rpath,{PKG}", "-Wl,-rpath,$ORIGIN/../../paper_2508_15371_amd"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed ({r.returncode}):\n{r.stderr}")
+    return NATIVE_BIN
+
+
 def build(verbose: bool = False) -> str:
-    """Compile libcmsd.so; returns its path.  Always recompiles."""
+    """Compile libcmsd.so, then the native test consumer; returns the library's
+    path.  Always recompiles."""
     tmp = LIB + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", *FLAGS, "-I", INC, "-o", tmp, SRC]
     if verbose:
@@ -46,6 +63,7 @@ def build(verbose: bool = False) -> str:
     if verbose and err:
         print(err, file=sys.stderr)
     os.replace(tmp, LIB)
+    build_native(verbose)
     return LIB
 
 
