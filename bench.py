@@ -111,6 +111,43 @@ def _traffic(kernel: str, workload: str):
     return TRAFFIC[key]
 
 
+def extras(cmsd, groups, sets, n_sets, stream, cfg, steps) -> dict:
+    """Per-call time of the calls around the step that it does not run: the drafting
+    sampler (an exact softmax sample per drafter row, from the row stats) and the
+    confidence pass with the logit-variance moment, each over all drafter rows."""
+    import torch
+    dev = torch.device("cuda:0")
+    n = max(3, steps // 4)
+    out = {}
+    for name in ("cmsd_draft_sample", "cmsd_confidence_var"):
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(n)]
+        for i, e in enumerate(ev):
+            for gi, (lpg, _, _) in enumerate(groups):
+                draft = sets[gi][i % n_sets][0]
+                rows = draft.shape[0]
+                if name == "cmsd_draft_sample":
+                    if not hasattr(lpg, "_xs"):
+                        ws = torch.empty((cmsd.cmsd_draft_sample_workspace_bytes(rows, cfg.V) + 7) // 8,
+                                         dtype=torch.float64, device=dev)
+                        lpg._xs = (torch.rand(rows, device=dev), torch.empty(rows, dtype=torch.int32, device=dev), ws)
+                    u, drafted, ws = lpg._xs
+                    if gi == 0:
+                        e[0].record(stream)
+                    cmsd.cmsd_draft_sample(draft, lpg.stats, u, drafted=drafted, workspace=ws, stream=stream)
+                else:
+                    if not hasattr(lpg, "_xv"):
+                        lpg._xv = torch.empty(rows, dtype=torch.float32, device=dev)
+                    if gi == 0:
+                        e[0].record(stream)
+                    cmsd.cmsd_confidence_var(draft, lpg.stats, lpg._xv, stream=stream)
+            e[1].record(stream)
+        torch.cuda.synchronize()
+        t = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) * 1e-3
+        nbytes = cfg.draft_rows * cfg.V * cfg.elem_bytes
+        out[name] = {"ms": t * 1e3, "logit_gbps": nbytes / t / 1e9, "rows": cfg.draft_rows}
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -135,6 +172,9 @@ def main() -> int:
     ap.add_argument("--no-rotate", action="store_true",
                     help="reuse one copy of the logits in every step (by default small workloads rotate "
                          "copies totalling more than 512 MiB)")
+    ap.add_argument("--extras", action="store_true",
+                    help="also time the drafting sampler (cmsd_draft_sample) and cmsd_confidence_var on the "
+                         "drafter rows, after the timed region (reported under 'extras')")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run device-to-device copies of MIB MiB (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -315,6 +355,8 @@ def main() -> int:
                            "mean_draft_len": float(k_all.mean()), "streams": G,
                            "path": "cmsd_logit_pass" if use_pass else "three calls", "input_copies": n_sets},
     }
+    if args.extras:
+        result["extras"] = extras(cmsd, groups, sets, n_sets, main, cfg, args.steps)
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(cfg.name, args.seed, mode)
