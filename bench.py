@@ -9,8 +9,15 @@ the draft lengths, it is cmsd_confidence + cmsd_draft_len + cmsd_verify (--path 
 forces the separate calls everywhere).  Prints one JSON line.  Default workload: B=256
 sequences, k_max=16, V=128256, bf16 (the largest configuration; inputs 2.17 GB).
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4] [--mode cm|standard]
-                  [--path auto|pass|calls] [--no-cpu-baseline]
+Inputs are resident in HBM before timing; workloads smaller than 512 MiB rotate copies of
+their logits between steps (``--no-rotate`` reuses one).  HIP events around the roofline
+kernel in every 4th timed step give its achieved bandwidth; after the timed region the
+bench times each of the three calls separately and, with ``--extras``, the drafting
+sampler and the logit-variance pass; the CPU oracle runs last on the host.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4|c5|c3|c2|v152k]
+                  [--mode cm|standard] [--path auto|pass|calls] [--streams G] [--event-every N]
+                  [--capacity-rows] [--no-rotate] [--extras] [--no-cpu-baseline] [--copy-probe MIB]
 """
 from __future__ import annotations
 
