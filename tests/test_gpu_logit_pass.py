@@ -371,3 +371,60 @@ def test_parameter_settings(cm, mode, kw, adaptive):
     print(f"[logit pass params] {kw} mode={mode} adaptive={adaptive}: checked={t.checked} exceptions={t.exceptions} "
           f"mean n_acc={n_acc.mean():.3f} mean k={k.mean():.3f}", flush=True)
     t.assert_ok()
+
+
+def test_boundary_uniforms(cm):
+    # u = 0 and u = 1 - 2^-24, the ends of the uniform grid, with outcomes fixed by
+    # construction: target rows 0..K-1 equal the drafter rows except tokens j < k
+    # raised by 2 and 1, so p_t > p_d exactly there (the residual lives on {j, k}) and
+    # p_t < p_d elsewhere; the final rows mask everything outside [lo, hi]
+    B, K, V = 4, 2, 4099
+    g = np.random.default_rng(2024)
+    zd = g.normal(0, 1, (B * K, V)).astype(np.float32)
+    zt = np.zeros((B * (K + 1), V), dtype=np.float32)
+    boost = {}
+    for b in range(B):
+        for i in range(K):
+            j, k = sorted(g.choice(V, 2, replace=False).tolist())
+            boost[(b, i)] = (j, k)
+            row = zd[b * K + i].copy()
+            row[j] += 2.0
+            row[k] += 1.0
+            zt[b * (K + 1) + i] = row
+        fin = np.full(V, -np.inf, dtype=np.float32)
+        lo, hi = 100 + b, V - 50 - b
+        fin[lo:hi + 1] = g.normal(0, 1, hi - lo + 1).astype(np.float32)
+        fin[hi] = 3.0                                       # a large final mass at the last live token
+        zt[b * (K + 1) + K] = fin
+        boost[(b, "final")] = (lo, hi)
+    top = 1.0 - 2.0 ** -24
+    # sequence 0: boosted drafts (ratio > 1) pass even at u = 1 - 2^-24; bonus with u = 0
+    # sequence 1: an unboosted draft (ratio < 1) fails at u = 1 - 2^-24; residual with u = 0
+    # sequence 2: the same rejection; residual with u = 1 - 2^-24
+    # sequence 3: drafts accepted at u = 0 (p_t > 0); bonus with u = 1 - 2^-24
+    dr = np.zeros((B, K), dtype=np.int32)
+    un = np.zeros((B, K + 1), dtype=np.float32)
+    dr[0] = [boost[(0, 0)][0], boost[(0, 1)][1]]
+    un[0] = [top, top, 0.0]
+    for b in (1, 2):
+        j, k = boost[(b, 0)]
+        dr[b] = [(j + k) // 2 if (j + k) // 2 not in (j, k) else (k + 1) % V, 0]
+        un[b] = [top, 0.5, 0.0 if b == 1 else top]
+    dr[3] = [7, 11]
+    un[3] = [0.0, 0.0, top]
+    dev = torch.device("cuda:0")
+    out, P = _pass(cm, Hn.to_device(zd, "f32", dev), Hn.to_device(zt, "f32", dev), torch.from_numpy(dr.reshape(-1)).to(dev),
+                   torch.from_numpy(un.reshape(-1)).to(dev), B, K, O.MODE_STANDARD)
+    n_acc = out["n_accepted"].cpu().tolist()
+    nxt = out["next_token"].cpu().tolist()
+    assert n_acc == [2, 0, 0, 2], n_acc
+    assert nxt[0] == boost[(0, "final")][0]                 # u = 0: the first live token of the bonus row
+    assert nxt[1] == boost[(1, 0)][0]                        # u = 0: the first residual token j
+    assert nxt[2] == boost[(2, 0)][1]                        # u = 1 - 2^-24: the last residual token k
+    assert nxt[3] == boost[(3, "final")][1]                 # u = 1 - 2^-24: the last live token (large mass)
+    # and the oracle agrees on every one
+    for b in range(B):
+        res = O.verify_sequence([zt[b * (K + 1) + i].astype(np.float64) for i in range(K + 1)],
+                                [zd[b * K + i].astype(np.float64) for i in range(K)], dr[b],
+                                [float(u) for u in un[b]], [0.5] * K, K, O.MODE_STANDARD, 3, 0.1, 1.0)
+        assert (res["n_acc"], res["next"]) == (n_acc[b], nxt[b]), b
