@@ -12,12 +12,15 @@ sequences, k_max=16, V=128256, bf16 (the largest configuration; inputs 2.17 GB).
 Inputs are resident in HBM before timing; workloads smaller than 512 MiB rotate copies of
 their logits between steps (``--no-rotate`` reuses one).  HIP events around the roofline
 kernel in every 4th timed step give its achieved bandwidth; after the timed region the
-bench times each of the three calls separately and, with ``--extras``, the drafting
-sampler and the logit-variance pass; the CPU oracle runs last on the host.
+bench times each of the three calls separately, then a bare read of the roofline
+kernel's rows in its grid shape (``read_ceiling``: what one launch of those bytes can
+reach) and, with ``--extras``, the drafting sampler and the logit-variance pass; the CPU
+oracle runs last on the host.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4|c5|c3|c2|v152k]
                   [--mode cm|standard] [--path auto|pass|calls] [--streams G] [--event-every N]
-                  [--capacity-rows] [--no-rotate] [--extras] [--no-cpu-baseline] [--copy-probe MIB]
+                  [--capacity-rows] [--no-rotate] [--extras] [--no-read-ceiling] [--no-cpu-baseline]
+                  [--copy-probe MIB]
 """
 from __future__ import annotations
 
@@ -39,10 +42,10 @@ PEAK_HBM_GBS = 8000.0   # MI355X HBM3E
 # device copy (x2.0 and x1.0).  Valid only for the kernel code they were taken on
 # (kernel_code_hash(): sha256 prefix of the .hip file's code without comments);
 # otherwise "traffic" is reported null.
-TRAFFIC = {"kernel_code_sha256_16": "be3b1d2f74103a92",
-           "k_row_pass_c4": 2170.13e6 + 0.270e6, "k_confidence_c4": 1052.89e6 + 0.131e6,
-           "k_confidence_c5": 524.63e6 + 0.262e6, "k_row_pass_c3": 113.88e6 + 0.035e6,
-           "k_row_pass_c2": 9.07e6 + 0.004e6, "k_row_pass_v152k": 331.58e6 + 0.035e6,
+TRAFFIC = {"kernel_code_sha256_16": "f50fa2d918555a25",
+           "k_row_pass_c4": 2170.55e6 + 0.270e6, "k_confidence_c4": 1052.91e6 + 0.131e6,
+           "k_confidence_c5": 524.68e6 + 0.262e6, "k_row_pass_c3": 112.77e6 + 0.035e6,
+           "k_row_pass_c2": 9.12e6 + 0.004e6, "k_row_pass_v152k": 331.72e6 + 0.035e6,
            "profile": "profiles/<workload>_cm_logit_pass.md"}
 
 
@@ -155,6 +158,55 @@ def extras(cmsd, groups, sets, n_sets, stream, cfg, steps) -> dict:
     return out
 
 
+def read_ceiling(sets, n_sets, cfg, R_t, use_pass, stream, steps, t_roof) -> dict:
+    """Bare-read ceiling of the roofline kernel's launch: the same rows (drafter rows,
+    then the target rows on the joint pass), the same one-workgroup-per-row grid and
+    the same nontemporal 16-byte loads, nothing reduced, timed with HIP events around
+    each launch like the roofline kernel.  Reports every workgroup size / loads-in-flight
+    shape and the roofline kernel's time over the fastest bare read."""
+    import ctypes as C
+    import torch
+    from paper_2508_15371_amd import build as B
+    if not os.path.exists(B.PROBE_LIB):
+        return {"error": f"{B.PROBE_LIB} is not built"}
+    lib = C.CDLL(B.PROBE_LIB)
+    i64, vp = C.c_int64, C.c_void_p
+    lib.cmsd_probe_read_rows.argtypes = [vp, i64, i64, vp, i64, i64, i64, C.c_int, C.c_int, vp, vp]
+    lib.cmsd_probe_read_rows.restype = C.c_int
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda:0")
+    s = cfg.elem_bytes
+    row_bytes = cfg.V * s
+    rows_b = R_t if use_pass else 0
+    n = max(20, steps // 4)
+
+    def launch(i, bd, unroll):
+        a = sets[0][i % n_sets]
+        draft, target = a[0], a[1]
+        rc = lib.cmsd_probe_read_rows(draft.data_ptr(), draft.shape[0], draft.stride(0) * s,
+                                      target.data_ptr(), rows_b, target.stride(0) * s, row_bytes,
+                                      bd, unroll, sink.data_ptr(), stream.cuda_stream)
+        if rc != 0:
+            raise RuntimeError(f"cmsd_probe_read_rows: status {rc}")
+
+    shapes = {}
+    nbytes = (cfg.draft_rows + rows_b) * row_bytes
+    for bd in (64, 128, 256):
+        for unroll in (4, 8):
+            for i in range(10):
+                launch(i, bd, unroll)
+            ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(n)]
+            for i, e in enumerate(ev):
+                e[0].record(stream)
+                launch(i, bd, unroll)
+                e[1].record(stream)
+            torch.cuda.synchronize()
+            t = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) * 1e-3
+            shapes[f"bd{bd}_u{unroll}"] = {"us": t * 1e6, "gbps": nbytes / t / 1e9}
+    best = min(shapes, key=lambda k: shapes[k]["us"])
+    return {"kernel": "k_read_rows", "bytes": nbytes, "launches": n, "by_shape": shapes, "best": best,
+            "best_gbps": shapes[best]["gbps"], "roofline_kernel_time_over_read": t_roof / (shapes[best]["us"] * 1e-6)}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -182,6 +234,9 @@ def main() -> int:
     ap.add_argument("--extras", action="store_true",
                     help="also time the drafting sampler (cmsd_draft_sample) and cmsd_confidence_var on the "
                          "drafter rows, after the timed region (reported under 'extras')")
+    ap.add_argument("--no-read-ceiling", action="store_true",
+                    help="skip the bare-read ceiling (a read of the roofline kernel's rows in its grid "
+                         "shape, timed after the timed region)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run device-to-device copies of MIB MiB (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -362,6 +417,8 @@ def main() -> int:
                            "mean_draft_len": float(k_all.mean()), "streams": G,
                            "path": "cmsd_logit_pass" if use_pass else "three calls", "input_copies": n_sets},
     }
+    if not args.no_read_ceiling and G == 1:
+        result["read_ceiling"] = read_ceiling(sets, n_sets, cfg, R_t, use_pass, main, args.steps, t_roof)
     if args.extras:
         result["extras"] = extras(cmsd, groups, sets, n_sets, main, cfg, args.steps)
     if not args.no_cpu_baseline:

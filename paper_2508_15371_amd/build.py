@@ -49,9 +49,27 @@ def build_native(verbose: bool = False) -> str:
     return NATIVE_BIN
 
 
+PROBE_SRC = os.path.join(PKG, "csrc", "read_probe.hip")
+PROBE_LIB = os.path.join(PKG, "libcmsd_readprobe.so")
+
+
+def build_probe(verbose: bool = False) -> str:
+    """Compile the benchmark's read-ceiling probe (a bare read of the same rows in the
+    same grid shape as the joint row pass); returns its path."""
+    tmp = PROBE_LIB + ".tmp"
+    cmd = [hipcc(), f"--offload-arch={ARCH}", *FLAGS, "-o", tmp, PROBE_SRC]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed ({r.returncode}):\n{r.stderr}")
+    os.replace(tmp, PROBE_LIB)
+    return PROBE_LIB
+
+
 def build(verbose: bool = False) -> str:
-    """Compile libcmsd.so, then the native test consumer; returns the library's
-    path.  Always recompiles."""
+    """Compile libcmsd.so, then the native test consumer and the benchmark's read
+    probe; returns the library's path.  Always recompiles."""
     tmp = LIB + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", *FLAGS, "-I", INC, "-o", tmp, SRC]
     if verbose:
@@ -64,6 +82,7 @@ def build(verbose: bool = False) -> str:
         print(err, file=sys.stderr)
     os.replace(tmp, LIB)
     build_native(verbose)
+    build_probe(verbose)
     return LIB
 
 

@@ -20,3 +20,23 @@ def test_cpu_baseline_worker_counts_rows():
     rows, secs = bench._cpu_baseline_worker(("tiny", 0, 0, 1))
     assert rows == 4 + 4 + 1          # k_max drafter rows and k_max + 1 target rows of one sequence
     assert secs > 0.0
+
+
+def test_read_probe_library_checks_its_arguments():
+    # the bench's bare-read probe: loads, exports its entry point, and rejects bad
+    # arguments on the host before any launch (no GPU needed for these calls)
+    import ctypes as C
+    from paper_2508_15371_amd import build as B
+    lib = C.CDLL(B.PROBE_LIB)
+    f = lib.cmsd_probe_read_rows
+    i64, vp = C.c_int64, C.c_void_p
+    f.argtypes = [vp, i64, i64, vp, i64, i64, i64, C.c_int, C.c_int, vp, vp]
+    f.restype = C.c_int
+    fake = C.c_void_p(4096)
+    assert f(fake, 4, 100, fake, 4, 100, 100, 96, 4, fake, None) == 1        # workgroup size
+    assert f(fake, 4, 100, fake, 4, 100, 100, 256, 3, fake, None) == 1       # loads in flight
+    assert f(fake, 4, 64, fake, 4, 100, 100, 256, 4, fake, None) == 1        # stride below the row
+    assert f(None, 4, 100, fake, 0, 100, 100, 256, 4, fake, None) == 1       # rows without a base
+    assert f(fake, 4, 100, fake, 4, 100, 100, 256, 4, None, None) == 1       # no sink
+    assert f(fake, -1, 100, fake, 4, 100, 100, 256, 4, fake, None) == 1      # negative count
+    assert f(None, 0, 0, None, 0, 0, 100, 256, 4, fake, None) == 0           # nothing to read: no launch
