@@ -244,24 +244,45 @@ __device__ __forceinline__ void block_sum_n(double (&v)[N], double* lds) {
 // Streams the nr full rounds of a row: round k is U vectors per thread at
 // vp[(k*U + u)*BD + t].  DEPTH rounds of loads are kept in flight in a ring of
 // registers (fully unrolled, so each slot is consumed and then refilled in place:
-// no register copies).  prep() runs once the first loads are issued (work that
-// must precede the first round overlaps their latency); consume(raw[U], k) is
-// called in round order.
+// no register copies).  The main loop covers the rounds whose refills all exist, so
+// no load there sits behind a branch: the number of loads in flight is the same on
+// every path, and the wait before a round covers that round only while the later
+// rounds stay in flight.  The last rounds (fewer than 2*DEPTH) follow with guarded
+// refills; the first DEPTH are always requested.  prep() runs once the first loads
+// are issued (work that must precede the first round overlaps their latency);
+// consume(raw[U], k) is called in round order.
 #ifndef CMSD_STREAM_DEPTH
 #define CMSD_STREAM_DEPTH 2
 #endif
 template <int U, int BD, int DEPTH, typename P, typename F>
 __device__ __forceinline__ void stream_rounds(const uint4* vp, int64_t nr, int t, P&& prep, F&& consume) {
+  if (nr <= 0) {
+    prep();
+    return;
+  }
+  // the first DEPTH rounds, issued unconditionally (a row of fewer rounds reads vp[0],
+  // the same 16 bytes for every lane, in their place)
   uint4 buf[DEPTH][U];
 #pragma unroll
   for (int d = 0; d < DEPTH; ++d) {
-    if (d < nr) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) buf[d][u] = ld_stream(vp + ((int64_t)d * U + u) * BD + t);
-    }
+    for (int u = 0; u < U; ++u) buf[d][u] = ld_stream(vp + (d < nr ? ((int64_t)d * U + u) * BD + t : 0));
+    __builtin_amdgcn_sched_barrier(0);  // rounds leave in order, as the loop refills them
   }
   prep();
-  for (int64_t k0 = 0; k0 < nr; k0 += DEPTH) {
+  int64_t k0 = 0;
+  for (; k0 + 2 * DEPTH <= nr; k0 += DEPTH) {
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) {
+      const int64_t k = k0 + d;
+      consume(buf[d], k);
+      const int64_t kn = k + DEPTH;
+#pragma unroll
+      for (int u = 0; u < U; ++u) buf[d][u] = ld_stream(vp + (kn * U + u) * BD + t);
+      __builtin_amdgcn_sched_barrier(0);  // the refill leaves before the next round is consumed
+    }
+  }
+  for (; k0 < nr; k0 += DEPTH) {
 #pragma unroll
     for (int d = 0; d < DEPTH; ++d) {
       const int64_t k = k0 + d;
@@ -465,7 +486,6 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
     const int64_t nr = g.nvec / per_round;
 
     ConfState s;
-    if (t < g.head) conf_one<VAR>(s, E::load(row + t), 0);
     // KEEP: the vectors of the round that set this thread's maximum stay in registers,
     // so the epilogue finds the max index without reading that round again
     uint4 keep[KEEP ? U : 1];
@@ -473,7 +493,10 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
     for (int u = 0; u < (KEEP ? U : 1); ++u) keep[u] = make_uint4(0u, 0u, 0u, 0u);
 
     // full rounds, next round's loads issued before the current one is consumed
-    stream_rounds<U, BD, CMSD_STREAM_DEPTH>(vp, nr, t, [] {}, [&](const uint4 (&raw)[U], int64_t k) {
+    // the head elements are loaded and folded in once the first rounds are requested
+    stream_rounds<U, BD, CMSD_STREAM_DEPTH>(vp, nr, t, [&] {
+      if (t < g.head) conf_one<VAR>(s, E::load(row + t), 0);
+    }, [&](const uint4 (&raw)[U], int64_t k) {
       float f[N];
 #pragma unroll
       for (int u = 0; u < U; ++u) E::unpack(raw[u], f + u * VEC);
@@ -799,12 +822,14 @@ __device__ __forceinline__ void target_stream(const T* row, const Geom& g, const
   const uint4* vp = reinterpret_cast<const uint4*>(row + g.head);
   const int64_t per_round = (int64_t)U * BD;
   const int64_t nr = g.nvec / per_round;
-  const float head = t < g.head ? E::load(row + t) : -INFINITY;
   stream_rounds<U, BD, CMSD_STREAM_DEPTH>(
       vp, nr, t,
       [&] {
+        // the head element is requested with the rounds, before prep() waits for
+        // its own loads (every lane loads, lanes past the head element 0)
+        const float hv = E::load(row + (t < g.head ? t : 0));
         prep();
-        float f[1] = {head};
+        float f[1] = {t < g.head ? hv : -INFINITY};
         target_chunk<1, true>(s, f, t < g.head ? 1u : 0u, 0, count, gz, beta, wcnt);
       },
       [&](const uint4 (&raw)[U], int64_t k) {
