@@ -82,6 +82,32 @@ def test_each_row_block(cm, monkeypatch, block, dtype, V):
     t.assert_ok()
 
 
+@pytest.mark.parametrize("block", [64, 128, 256])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_rounds_across_the_ring(cm, monkeypatch, block, dtype):
+    # a row streams in rounds of 32 elements per thread, two rounds in flight: rows of
+    # 1..9 full rounds (plus a partial round, a tail and an unaligned head) take the
+    # ring's main loop zero to three times and leave 2 or 3 rounds to its last part
+    monkeypatch.setenv("CMSD_ROW_BLOCK", str(block))
+    lam = (0.2, 0.5, 0.3)
+    lam32 = tuple(Hn.f32(x) for x in lam)
+    for nr in range(1, 10):
+        V = 32 * block * nr + 37
+        g = np.random.default_rng(nr * 1000 + block)
+        rows = _invariant_rows(V, g)[:4] + [g.normal(0, 2, V)]
+        stored = _store(rows, dtype)
+        buf = np.zeros((stored.shape[0], V + 3), dtype=stored.dtype)
+        buf[:, 3:] = stored                     # rows start 3 elements into their stride
+        tdev = Hn.to_device(buf, dtype, torch.device("cuda:0"))[:, 3:]
+        st = cm.cmsd_confidence(tdev, lambdas=lam, beta_margin=0.7)
+        torch.cuda.synchronize()
+        gs = Hn.stats_np(st)
+        t = Hn.Tally()
+        for r in range(stored.shape[0]):
+            Hn.check_row_stats(t, gs, r, Hn.decode(stored[r], dtype), V, lam32, Hn.f32(0.7))
+        t.assert_ok()
+
+
 def _sample_rows(cfg, k):
     n = cfg.draft_rows
     if n <= k:

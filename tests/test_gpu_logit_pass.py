@@ -159,6 +159,19 @@ def test_shapes(cm, dtype, V, K, B, pad):
         _run_case(cm, zd, zt, dr, u, B, K, V, dtype, mode=mode, adaptive=bool(mode == O.MODE_CM), pad=pad)
 
 
+@pytest.mark.parametrize("block", [64, 128, 256])
+def test_rounds_across_the_ring(cm, monkeypatch, block):
+    # drafter and target rows of 1..9 full 32-element-per-thread rounds (plus a partial
+    # round and a tail), unaligned starts: every way through the streaming ring's main
+    # loop and its last rounds, for every workgroup size
+    monkeypatch.setenv("CMSD_ROW_BLOCK", str(block))
+    for nr in (1, 2, 3, 4, 5, 6, 9):
+        V = 32 * block * nr + 37
+        g = np.random.default_rng(nr * 100 + block)
+        zd, zt, dr, u = _case(g, 2, 3, V, "bf16")
+        _run_case(cm, zd, zt, dr, u, 2, 3, V, "bf16", mode=O.MODE_CM, adaptive=True, pad=1)
+
+
 def test_masked_logits(cm):
     # -inf entries: flags bit 0, entropy over the finite entries, final tokens never masked
     V, K, B = 3001, 4, 4
