@@ -241,7 +241,7 @@ def main() -> int:
                     help="only run device-to-device copies of MIB MiB (calibrates HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); the path shards by "
+        print(f"bench.py: the benchmark runs on one GPU only (asked for --gpus {args.gpus}); the path shards by "
               f"sequence across GPUs with no exchange, so the whole-job figure is N times the one-GPU value",
               file=sys.stderr)
         return 2
