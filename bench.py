@@ -17,8 +17,8 @@ kernel's rows in its grid shape (``read_ceiling``: what one launch of those byte
 reach) and, with ``--extras``, the drafting sampler and the logit-variance pass; the CPU
 oracle runs last on the host.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4|c5|c3|c2|v152k]
-                  [--mode cm|standard] [--path auto|pass|calls] [--streams G] [--event-every N]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4|c5|c3|c2|v152k|tiny]
+                  [--mode cm|standard] [--path auto|pass|fused|calls] [--streams G] [--event-every N]
                   [--capacity-rows] [--no-rotate] [--extras] [--no-read-ceiling] [--no-cpu-baseline]
                   [--copy-probe MIB]
 """
@@ -214,12 +214,12 @@ def main() -> int:
     # ~3 % slower), so the default warms up for 100 steps and times 500 (~0.2 s on c4)
     ap.add_argument("--steps", type=int, default=500)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--workload", default="c4", choices=["c2", "c3", "c4", "c5", "v152k"])
+    ap.add_argument("--workload", default="c4", choices=["tiny", "c2", "c3", "c4", "c5", "v152k"])
     ap.add_argument("--mode", default="cm", choices=["cm", "standard"])
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--path", default="auto", choices=["auto", "pass", "calls"],
-                    help="one cmsd_logit_pass call per step (dense layouts; auto: dense workloads) "
-                         "or the three separate calls")
+    ap.add_argument("--path", default="auto", choices=["auto", "pass", "fused", "calls"],
+                    help="one cmsd_logit_pass call per step (dense layouts; auto: dense workloads), one "
+                         "cmsd_logit_pass_fused call (one launch, for small batches), or the three separate calls")
     ap.add_argument("--streams", type=int, default=1, metavar="G",
                     help="split the batch into G sequence groups, each on its own stream")
     ap.add_argument("--event-every", type=int, default=4, metavar="N",
@@ -311,13 +311,22 @@ def main() -> int:
     R_d = cfg.draft_rows
     R_t = sum(int(lpg.off[bg].item()) for lpg, _, _ in groups) if cfg.ragged else cfg.dense_target_rows
     # one cmsd_logit_pass call per step on dense workloads (one stream), else the three calls
+    use_fused = args.path == "fused"
     use_pass = args.path == "pass" or (args.path == "auto" and not cfg.ragged)
-    if use_pass and (cfg.ragged or G != 1):
-        print("bench.py: --path pass needs a dense workload and one stream", file=sys.stderr)
+    if (use_pass or use_fused) and (cfg.ragged or G != 1):
+        print(f"bench.py: --path {args.path} needs a dense workload and one stream", file=sys.stderr)
         return 2
-    rk = "k_row_pass" if use_pass else "k_confidence"
+    rk = "k_fused_pass" if use_fused else ("k_row_pass" if use_pass else "k_confidence")
 
     def step(lpg, a, st, e=None):
+        if use_fused:
+            # the whole step is the one launch: the events bracket it
+            if e is not None:
+                e[0].record(st)
+            lpg.logit_pass_fused(a[0], a[1], a[2], a[3], st)
+            if e is not None:
+                e[1].record(st)
+            return
         if use_pass:
             lpg.logit_pass(a[0], a[1], a[2], a[3], st, row_events=e)
             return
@@ -386,10 +395,14 @@ def main() -> int:
     # reads one group's drafter rows (the whole batch when G = 1) and writes their records
     if use_pass:
         launch_bytes = R_d * (cfg.V * s + 32) + R_t * (cfg.V * s + 64) + cfg.B * cfg.k_max * 8
+    elif use_fused:
+        launch_bytes = None     # the whole step: its algorithmic bytes (below)
     else:
         launch_bytes = (R_d // G) * (cfg.V * s + 32)
     verify_bytes = R_t * cfg.V * s + rej * cfg.V * s + R_t * 32 + cfg.B * cfg.k_max * 8
     step_bytes = conf_bytes + cfg.B * cfg.k_max * 32 + verify_bytes
+    if launch_bytes is None:
+        launch_bytes = step_bytes
 
     result = {
         "metric": "logit rows/sec and achieved HBM GB/s (confidence+verify), V=32000-152064",
@@ -415,9 +428,10 @@ def main() -> int:
                      "traffic": _traffic(rk, cfg.name) if G == 1 else None},
         "workload_stats": {"mean_n_acc": float(n_acc.mean()), "rejecting_sequences": rej,
                            "mean_draft_len": float(k_all.mean()), "streams": G,
-                           "path": "cmsd_logit_pass" if use_pass else "three calls", "input_copies": n_sets},
+                           "path": ("cmsd_logit_pass_fused" if use_fused else "cmsd_logit_pass" if use_pass
+                                    else "three calls"), "input_copies": n_sets},
     }
-    if not args.no_read_ceiling and G == 1:
+    if not args.no_read_ceiling and G == 1 and not use_fused:
         result["read_ceiling"] = read_ceiling(sets, n_sets, cfg, R_t, use_pass, main, args.steps, t_roof)
     if args.extras:
         result["extras"] = extras(cmsd, groups, sets, n_sets, main, cfg, args.steps)

@@ -14,7 +14,8 @@
  *                    the residual (or bonus) distribution     (Sec. III.A, III.B(c))
  *
  * cmsd_logit_pass does all three in one call (four launches, two in GREEDY mode)
- * for a dense target layout.
+ * for a dense target layout; cmsd_logit_pass_fused does it in one launch, for small
+ * batches.
  *
  * Conventions shared by every call
  *   - All array pointers are DEVICE pointers (hipMalloc / torch CUDA tensors);
@@ -280,6 +281,43 @@ cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, cons
                             int32_t* next_token, void* workspace, size_t workspace_bytes,
                             void* const* row_events, void* stream);
 
+/*
+ * cmsd_logit_pass_fused - cmsd_logit_pass in a single launch, for small batches
+ * (Sec. III.B(1) to (c), Sec. III.A, as cmsd_logit_pass; the paper's small-batch
+ * latency, Fig. 2, is what it is for).  Every drafter and target row is one
+ * 256-thread workgroup; the last row of a sequence to finish (an atomic count per
+ * sequence, each row's results published behind a device fence) makes the draft
+ * length and the accept tests and samples the final token in the same launch.  The
+ * fences serialise across the chip (tens of ns per row), so this pays for launches of
+ * up to a few hundred rows (batch*(2*k_max+1)); larger batches are faster with
+ * cmsd_logit_pass.  Arguments, outputs and errors are cmsd_logit_pass's (without
+ * row_events), except the workspace:
+ *   workspace       device scratch of at least
+ *                   cmsd_logit_pass_fused_workspace_bytes(batch, k_max, vocab) bytes,
+ *                   8-byte aligned, owned by the caller.  Its last 4*batch bytes
+ *                   (ending at workspace_bytes rounded down to a multiple of 4) hold
+ *                   one int32 counter per sequence: they must be zero before the first
+ *                   call with this workspace (zero the whole buffer once when
+ *                   allocating it), and every call leaves them zero, so one workspace
+ *                   serves calls of any batch it fits.  Calls sharing a workspace must
+ *                   be ordered (same stream); after another call (cmsd_verify,
+ *                   cmsd_logit_pass) has used it, zero it again.
+ * The outputs are bit-identical to cmsd_logit_pass's when that call's row kernels
+ * run with 256 threads (as it chooses for fewer than 16 rows per compute unit).
+ */
+cmsd_status cmsd_logit_pass_fused(const void* draft_logits, int64_t draft_stride, const void* target_logits,
+                                  int64_t target_stride, const int32_t* drafted, const float* uniforms,
+                                  int32_t dtype, int32_t batch, int32_t k_max, int64_t vocab,
+                                  const cmsd_conf_params* conf, const cmsd_draft_params* draft,
+                                  const cmsd_verify_params* verify, int32_t adaptive, cmsd_row_stats* draft_stats,
+                                  int32_t* draft_len, cmsd_target_stats* target_stats, int32_t* n_accepted,
+                                  int32_t* next_token, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace of cmsd_logit_pass_fused: cmsd_verify_workspace_bytes(batch, k_max, vocab)
+ * plus 4 bytes per sequence (rounded up to 8) for the counters; 0 for batch <= 0 or
+ * an invalid k_max (outside [1, 63]) / vocab. */
+size_t cmsd_logit_pass_fused_workspace_bytes(int32_t batch, int32_t k_max, int64_t vocab);
+
 /* Workspace cmsd_verify needs for `batch` sequences of up to `k_max` drafts over
  * `vocab`: per sequence, one 32-byte record per vocabulary slice (256 16-byte
  * vectors of a row) and one 32-byte record per target row position (k_max + 1);
@@ -313,7 +351,7 @@ size_t cmsd_draft_sample_workspace_bytes(int64_t n_rows, int64_t vocab);
 /* Human-readable name of a status code (static string). */
 const char* cmsd_status_string(cmsd_status s);
 
-/* Library ABI version, (major << 16) | minor: 1.3 (1.2 plus cmsd_logit_pass). */
+/* Library ABI version, (major << 16) | minor: 1.4 (1.3 plus cmsd_logit_pass_fused). */
 int32_t cmsd_version(void);
 
 #ifdef __cplusplus

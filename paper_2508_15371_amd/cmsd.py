@@ -69,6 +69,12 @@ def _load() -> C.CDLL:
                                     C.POINTER(DraftParams), C.POINTER(VerifyParams), i32, vp, vp, vp, vp, vp, vp,
                                     C.c_size_t, C.POINTER(vp), vp]
     lib.cmsd_logit_pass.restype = C.c_int
+    lib.cmsd_logit_pass_fused.argtypes = [vp, i64, vp, i64, vp, vp, i32, i32, i32, i64, C.POINTER(ConfParams),
+                                          C.POINTER(DraftParams), C.POINTER(VerifyParams), i32, vp, vp, vp, vp, vp,
+                                          vp, C.c_size_t, vp]
+    lib.cmsd_logit_pass_fused.restype = C.c_int
+    lib.cmsd_logit_pass_fused_workspace_bytes.argtypes = [i32, i32, i64]
+    lib.cmsd_logit_pass_fused_workspace_bytes.restype = C.c_size_t
     lib.cmsd_status_string.argtypes = [C.c_int]
     lib.cmsd_status_string.restype = C.c_char_p
     lib.cmsd_version.argtypes = []
@@ -211,6 +217,17 @@ def verify_workspace(batch: int, k_max: int, vocab: int, device) -> torch.Tensor
     return torch.empty((n + 7) // 8, dtype=torch.float64, device=device)
 
 
+def cmsd_logit_pass_fused_workspace_bytes(batch: int, k_max: int, vocab: int) -> int:
+    return int(_lib.cmsd_logit_pass_fused_workspace_bytes(int(batch), int(k_max), int(vocab)))
+
+
+def fused_workspace(batch: int, k_max: int, vocab: int, device) -> torch.Tensor:
+    """A zero-filled device workspace for cmsd_logit_pass_fused (its per-sequence
+    counters must start at zero; every call leaves them zero).  Allocate once, reuse."""
+    n = max(8, cmsd_logit_pass_fused_workspace_bytes(batch, k_max, vocab))
+    return torch.zeros((n + 7) // 8, dtype=torch.float64, device=device)
+
+
 def cmsd_verify(draft_logits: torch.Tensor, draft_stats: torch.Tensor, target_logits: torch.Tensor,
                 target_offsets: torch.Tensor, draft_len: torch.Tensor, drafted: torch.Tensor,
                 uniforms: torch.Tensor, *, batch: int, k_max: int, mode: int = CMSD_MODE_CM, top_beta: int = 3,
@@ -289,20 +306,9 @@ def cmsd_draft_sample(logits: torch.Tensor, stats: torch.Tensor, uniforms: torch
     return drafted
 
 
-def cmsd_logit_pass(draft_logits: torch.Tensor, target_logits: torch.Tensor, drafted: torch.Tensor,
-                    uniforms: torch.Tensor | None, *, batch: int, k_max: int, lambdas=(1 / 3, 1 / 3, 1 / 3),
-                    beta_margin: float = 1.0, k_min: int = 1, alpha: float = 1.0, mode: int = CMSD_MODE_CM,
-                    top_beta: int = 3, tau_base: float = 0.1, gamma: float = 1.0, adaptive: bool = False,
-                    draft_stats: torch.Tensor | None = None, draft_len: torch.Tensor | None = None,
-                    target_stats: torch.Tensor | None = None, n_accepted: torch.Tensor | None = None,
-                    next_token: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
-                    row_events=None, stream=None) -> dict:
-    """Confidence, draft length and verification of a dense draft in one call.
-    ``draft_logits`` [batch*k_max, V], ``target_logits`` [batch*(k_max+1), V] (same
-    dtype), ``drafted`` int32 [batch*k_max], ``uniforms`` float32 [batch*(k_max+1)]
-    (None in GREEDY mode).  ``row_events``: optional pair of recorded-once
-    ``torch.cuda.Event`` objects, recorded again around the row-pass kernel.  Returns
-    the output tensors by name."""
+def _pass_args(draft_logits, target_logits, drafted, uniforms, batch, k_max, lambdas, beta_margin, k_min, alpha,
+               mode, top_beta, tau_base, gamma, outs, workspace, make_workspace):
+    """Checks and completes the arguments of the single-call passes."""
     drows, V, dst = _rows(draft_logits, "draft_logits")
     trows, V2, tst = _rows(target_logits, "target_logits")
     if V2 != V or target_logits.dtype != draft_logits.dtype:
@@ -315,8 +321,7 @@ def cmsd_logit_pass(draft_logits: torch.Tensor, target_logits: torch.Tensor, dra
     if draft_logits.device != dev:
         raise ValueError("draft and target logits must be on one device")
     nt = batch * (k_max + 1)
-    out = {"draft_stats": draft_stats, "draft_len": draft_len, "target_stats": target_stats,
-           "n_accepted": n_accepted, "next_token": next_token}
+    out = dict(outs)
     shapes = {"draft_stats": ((batch * k_max, 8), torch.float32), "draft_len": ((batch,), torch.int32),
               "target_stats": ((nt, 8), torch.float32), "n_accepted": ((batch,), torch.int32),
               "next_token": ((batch,), torch.int32)}
@@ -334,7 +339,7 @@ def cmsd_logit_pass(draft_logits: torch.Tensor, target_logits: torch.Tensor, dra
             continue
         _buf(t, name, dt, n, dev)
     if workspace is None:
-        workspace = verify_workspace(batch, k_max, V, dev)
+        workspace = make_workspace(batch, k_max, V, dev)
     if workspace.dtype != torch.float64 or not workspace.is_contiguous() or workspace.device != dev:
         raise ValueError(f"workspace must be a contiguous float64 tensor on {dev}")
     out["workspace"] = workspace
@@ -342,10 +347,59 @@ def cmsd_logit_pass(draft_logits: torch.Tensor, target_logits: torch.Tensor, dra
     dp = DraftParams(int(k_min), int(k_max), float(alpha))
     vp_ = VerifyParams(int(mode), int(top_beta), float(tau_base), float(gamma))
     _on_device(target_logits, "target_logits")
+    return out, dst, tst, V, cp, dp, vp_
+
+
+def cmsd_logit_pass(draft_logits: torch.Tensor, target_logits: torch.Tensor, drafted: torch.Tensor,
+                    uniforms: torch.Tensor | None, *, batch: int, k_max: int, lambdas=(1 / 3, 1 / 3, 1 / 3),
+                    beta_margin: float = 1.0, k_min: int = 1, alpha: float = 1.0, mode: int = CMSD_MODE_CM,
+                    top_beta: int = 3, tau_base: float = 0.1, gamma: float = 1.0, adaptive: bool = False,
+                    draft_stats: torch.Tensor | None = None, draft_len: torch.Tensor | None = None,
+                    target_stats: torch.Tensor | None = None, n_accepted: torch.Tensor | None = None,
+                    next_token: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                    row_events=None, stream=None) -> dict:
+    """Confidence, draft length and verification of a dense draft in one call.
+    ``draft_logits`` [batch*k_max, V], ``target_logits`` [batch*(k_max+1), V] (same
+    dtype), ``drafted`` int32 [batch*k_max], ``uniforms`` float32 [batch*(k_max+1)]
+    (None in GREEDY mode).  ``row_events``: optional pair of recorded-once
+    ``torch.cuda.Event`` objects, recorded again around the row-pass kernel.  Returns
+    the output tensors by name."""
+    outs = {"draft_stats": draft_stats, "draft_len": draft_len, "target_stats": target_stats,
+            "n_accepted": n_accepted, "next_token": next_token}
+    out, dst, tst, V, cp, dp, vp_ = _pass_args(draft_logits, target_logits, drafted, uniforms, batch, k_max, lambdas,
+                                               beta_margin, k_min, alpha, mode, top_beta, tau_base, gamma, outs,
+                                               workspace, verify_workspace)
+    ws = out["workspace"]
     _check("cmsd_logit_pass", _lib.cmsd_logit_pass(
         _ptr(draft_logits), dst, _ptr(target_logits), tst, _ptr(drafted), _ptr(uniforms),
         _dtype_code(target_logits), int(batch), int(k_max), V, C.byref(cp), C.byref(dp), C.byref(vp_),
         1 if adaptive else 0, _ptr(out["draft_stats"]), _ptr(out["draft_len"]), _ptr(out["target_stats"]),
-        _ptr(out["n_accepted"]), _ptr(out["next_token"]), _ptr(workspace),
-        workspace.numel() * workspace.element_size(), _events(row_events), _stream(stream)))
+        _ptr(out["n_accepted"]), _ptr(out["next_token"]), _ptr(ws),
+        ws.numel() * ws.element_size(), _events(row_events), _stream(stream)))
+    return out
+
+
+def cmsd_logit_pass_fused(draft_logits: torch.Tensor, target_logits: torch.Tensor, drafted: torch.Tensor,
+                          uniforms: torch.Tensor | None, *, batch: int, k_max: int, lambdas=(1 / 3, 1 / 3, 1 / 3),
+                          beta_margin: float = 1.0, k_min: int = 1, alpha: float = 1.0, mode: int = CMSD_MODE_CM,
+                          top_beta: int = 3, tau_base: float = 0.1, gamma: float = 1.0, adaptive: bool = False,
+                          draft_stats: torch.Tensor | None = None, draft_len: torch.Tensor | None = None,
+                          target_stats: torch.Tensor | None = None, n_accepted: torch.Tensor | None = None,
+                          next_token: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                          stream=None) -> dict:
+    """cmsd_logit_pass in one launch, for small batches (a few hundred rows).  Same
+    arguments and outputs; ``workspace`` must come from ``fused_workspace`` (or be
+    zero-filled once before its first use) and is reused across calls."""
+    outs = {"draft_stats": draft_stats, "draft_len": draft_len, "target_stats": target_stats,
+            "n_accepted": n_accepted, "next_token": next_token}
+    out, dst, tst, V, cp, dp, vp_ = _pass_args(draft_logits, target_logits, drafted, uniforms, batch, k_max, lambdas,
+                                               beta_margin, k_min, alpha, mode, top_beta, tau_base, gamma, outs,
+                                               workspace, fused_workspace)
+    ws = out["workspace"]
+    _check("cmsd_logit_pass_fused", _lib.cmsd_logit_pass_fused(
+        _ptr(draft_logits), dst, _ptr(target_logits), tst, _ptr(drafted), _ptr(uniforms),
+        _dtype_code(target_logits), int(batch), int(k_max), V, C.byref(cp), C.byref(dp), C.byref(vp_),
+        1 if adaptive else 0, _ptr(out["draft_stats"]), _ptr(out["draft_len"]), _ptr(out["target_stats"]),
+        _ptr(out["n_accepted"]), _ptr(out["next_token"]), _ptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
     return out

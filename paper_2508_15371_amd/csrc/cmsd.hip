@@ -1667,6 +1667,101 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
 // One exact softmax sample per drafter row (the draws a sampled draft needs):
 // vocabulary-slice partials of e = 2^(z log2e - m log2e), then the same slice scan
 // and exact in-slice locate as the final token, with u one uniform per row.
+// ----------------------------------------------------------------------------- fused pass (small batches)
+// The whole dense logit pass in one launch.  The grid is k_row_pass's (drafter rows,
+// then target rows, one 256-thread workgroup each).  Every row workgroup publishes its
+// record behind a device fence and counts itself into its sequence's counter; the
+// workgroup that completes the count (2 k_max + 1 rows) fences again, makes the
+// sequence's decisions (seq_info_pass, as k_pass_decide), computes the final row's
+// slice partials one wave per slice (parts_wave, as k_final_parts) and samples from
+// them (sample_from_parts, as k_final_sample), then sets the counter back to zero.
+// The arithmetic is the four-launch pass's, so the outputs are bit-identical to it.
+// The fences serialise chip-wide (about 35-50 ns per workgroup), which is why this
+// path is for launches of a few hundred rows, where it saves three dependent launches.
+constexpr int kFusedBD = 256;
+#ifndef CMSD_FUSED_SUB
+#define CMSD_FUSED_SUB 2
+#endif
+constexpr int kFusedSub = CMSD_FUSED_SUB;  // slices per wave and step in the final-token part
+
+template <typename T>
+__device__ __forceinline__ void fused_tail(const VerifyArgs& a, int b, int S, SlicePart* __restrict__ ws) {
+  constexpr int BD = kFusedBD, NW = BD / 64;
+  __shared__ SeqInfo s_q;
+  __shared__ double sd[2 * NW];
+  __shared__ int si[NW];
+  __shared__ double s_sc[3];
+  __shared__ int s_y;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const SeqInfo q = seq_info_pass(a, b, &s_q);
+  if (q.nacc < 0 || a.mode == CMSD_MODE_GREEDY) {
+    if (t == 0) {
+      a.n_acc[b] = q.nacc < 0 ? -1 : q.nacc;
+      a.next_tok[b] = q.nacc < 0 ? -1 : q.top1;
+    }
+    return;
+  }
+  const bool resid = q.nacc < q.kb;
+  const T* trow = reinterpret_cast<const T*>(a.target) + q.tr * a.tstride;
+  const T* drow = reinterpret_cast<const T*>(a.draft) + q.dr * a.dstride;
+  const bool same_phase = ((reinterpret_cast<uintptr_t>(trow) ^ reinterpret_cast<uintptr_t>(drow)) & 15u) == 0;
+  const Geom g = row_geom(trow, a.V);
+  const int64_t nu = g.nvec + 2;
+  SlicePart* P = ws + (int64_t)b * S;
+  // kFusedSub consecutive slices per wave and step, all their loads issued first
+  for (int sl = w * kFusedSub; sl < S; sl += NW * kFusedSub) {
+    double sum[kFusedSub][4] = {};
+    const int64_t u_first = (int64_t)sl * kSliceUnits;
+    if (u_first < nu) {
+      if (resid)
+        parts_wave<T, true, kFusedSub>(trow, drow, g, same_phase, u_first, lane, q.mst, q.msd, q.rho0, sum);
+      else
+        parts_wave<T, false, kFusedSub>(trow, trow, g, true, u_first, lane, q.mst, 0.f, 0.f, sum);
+    }
+#pragma unroll
+    for (int k = 0; k < kFusedSub; ++k) {
+      double r[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) r[j] = wave_all_d(sum[k][j], OpSumD());
+      if (lane == 0 && sl + k < S) P[sl + k] = SlicePart{r[0], r[1], r[2], r[3]};
+    }
+  }
+  __syncthreads();  // the partials of every slice, written by this workgroup
+  const float u = a.unif[q.off + q.kb];
+  const int y = sample_from_parts<T, BD>(trow, drow, a.V, resid, q.mst, q.msd, q.rho0, u, P, S, sd, si, s_sc, &s_y);
+  if (t == 0) {
+    a.n_acc[b] = q.nacc;
+    a.next_tok[b] = y;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kFusedBD) void k_fused_pass(VerifyArgs a, int S, SlicePart* __restrict__ ws,
+                                                         int32_t* __restrict__ cnt) {
+  __shared__ int s_last;
+  const int64_t nd = (int64_t)a.B * a.k_max;
+  const int64_t r = blockIdx.x;
+  int b;
+  if (r < nd) {
+    conf_row<T, kFusedBD, false>(reinterpret_cast<const T*>(a.draft) + r * a.dstride, a.V, a.ca, a.dstats_out + r,
+                                 nullptr);
+    b = int(r / a.k_max);
+  } else {
+    target_row<T, kFusedBD, true>(a, r - nd);
+    b = int((r - nd) / (a.k_max + 1));
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();  // this row's record is visible before it is counted
+    s_last = atomicAdd(cnt + b, 1) == 2 * a.k_max;
+  }
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();  // every other row of the sequence was counted after its record
+  if (threadIdx.x == 0) cnt[b] = 0;
+  fused_tail<T>(a, b, S, ws);
+}
+
 template <typename T>
 __global__ __launch_bounds__(kPartBD) void k_draft_parts(const T* __restrict__ logits, int64_t stride, int64_t V,
                                                          const cmsd_row_stats* __restrict__ stats, int S, int SW,
@@ -1839,6 +1934,64 @@ cmsd_status confidence_impl(const void* logits, int32_t dtype, int64_t n_rows, i
   return launched();
 }
 
+// Checks the arguments of the single-call pass and fills its kernel arguments (the
+// row slots sit after the per-dtype-independent slice records of the workspace).
+cmsd_status pass_setup(const void* draft_logits, int64_t draft_stride, const void* target_logits,
+                       int64_t target_stride, const int32_t* drafted, const float* uniforms, int32_t dtype,
+                       int32_t batch, int32_t k_max, int64_t vocab, const cmsd_conf_params* conf,
+                       const cmsd_draft_params* draft, const cmsd_verify_params* verify, int32_t adaptive,
+                       cmsd_row_stats* draft_stats, int32_t* draft_len, cmsd_target_stats* target_stats,
+                       int32_t* n_accepted, int32_t* next_token, void* workspace, size_t workspace_bytes,
+                       size_t workspace_need, VerifyArgs& a) {
+  if (dtype != CMSD_F32 && dtype != CMSD_BF16) return CMSD_ERR_DTYPE;
+  if (!conf || !draft || !verify) return CMSD_ERR_ARG;
+  if (batch < 0 || k_max < 1 || k_max > 63 || vocab < 2 || vocab > INT32_MAX) return CMSD_ERR_ARG;
+  if (adaptive != 0 && adaptive != 1) return CMSD_ERR_ARG;
+  if (!conf_args(conf, vocab, a.ca) || !draft_params_ok(draft) || draft->k_max != k_max || !verify_params_ok(verify))
+    return CMSD_ERR_ARG;
+  if (draft_stride < vocab || target_stride < vocab) return CMSD_ERR_ARG;
+  if (batch == 0) return CMSD_OK;
+  const size_t es = dtype == CMSD_F32 ? 4 : 2;
+  const int64_t drows = (int64_t)batch * k_max, trows = (int64_t)batch * (k_max + 1);
+  if (drows + trows > INT32_MAX || draft_stride > INT64_MAX / drows || target_stride > INT64_MAX / trows)
+    return CMSD_ERR_ARG;
+  if ((int64_t)batch * verify_slices(vocab, 4) > INT32_MAX) return CMSD_ERR_ARG;
+  if (!draft_logits || !target_logits || !drafted || (!uniforms && verify->mode != CMSD_MODE_GREEDY) ||
+      !draft_stats || !draft_len || !target_stats || !n_accepted || !next_token || !workspace)
+    return CMSD_ERR_ARG;
+  if (workspace_need == 0 || workspace_bytes < workspace_need || !aligned(workspace, 8)) return CMSD_ERR_ARG;
+  if (!aligned(draft_logits, es) || !aligned(target_logits, es) || !aligned(drafted, 4) || !aligned(uniforms, 4) ||
+      !aligned(draft_stats, 4) || !aligned(draft_len, 4) || !aligned(target_stats, 4) || !aligned(n_accepted, 4) ||
+      !aligned(next_token, 4))
+    return CMSD_ERR_ARG;
+  a.draft = draft_logits;
+  a.dstride = draft_stride;
+  a.dstats = draft_stats;
+  a.dstats_out = draft_stats;
+  a.target = target_logits;
+  a.tstride = target_stride;
+  a.target_rows = trows;
+  a.drafted = drafted;
+  a.unif = uniforms;
+  a.B = batch;
+  a.k_max = k_max;
+  a.V = vocab;
+  a.mode = verify->mode;
+  a.beta = verify->top_beta;
+  a.tau_base = verify->tau_base;
+  a.gamma = verify->gamma;
+  a.tstats = target_stats;
+  a.n_acc = n_accepted;
+  a.next_tok = next_token;
+  a.klen_out = draft_len;
+  a.k_min = draft->k_min;
+  a.alpha = draft->alpha;
+  a.adaptive = adaptive;
+  static_assert(sizeof(PassSlot) == sizeof(RowSlot), "the pass uses the verify workspace layout");
+  a.pslots = reinterpret_cast<PassSlot*>(static_cast<SlicePart*>(workspace) + (size_t)batch * verify_slices(vocab, 4));
+  return CMSD_OK;
+}
+
 }  // namespace
 
 // ----------------------------------------------------------------------------- C ABI
@@ -1854,7 +2007,7 @@ const char* cmsd_status_string(cmsd_status s) {
   return "unknown status";
 }
 
-int32_t cmsd_version(void) { return (1 << 16) | 3; }
+int32_t cmsd_version(void) { return (1 << 16) | 4; }
 
 size_t cmsd_draft_sample_workspace_bytes(int64_t n_rows, int64_t vocab) {
   if (n_rows <= 0 || n_rows > INT32_MAX || vocab < 2 || vocab > INT32_MAX) return 0;
@@ -1997,58 +2150,19 @@ cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, cons
                             cmsd_row_stats* draft_stats, int32_t* draft_len, cmsd_target_stats* target_stats,
                             int32_t* n_accepted, int32_t* next_token, void* workspace, size_t workspace_bytes,
                             void* const* row_events, void* stream) {
-  if (dtype != CMSD_F32 && dtype != CMSD_BF16) return CMSD_ERR_DTYPE;
-  if (!conf || !draft || !verify) return CMSD_ERR_ARG;
   if (row_events && (!row_events[0] || !row_events[1])) return CMSD_ERR_ARG;
-  if (batch < 0 || k_max < 1 || k_max > 63 || vocab < 2 || vocab > INT32_MAX) return CMSD_ERR_ARG;
-  if (adaptive != 0 && adaptive != 1) return CMSD_ERR_ARG;
   VerifyArgs a{};
-  if (!conf_args(conf, vocab, a.ca) || !draft_params_ok(draft) || draft->k_max != k_max || !verify_params_ok(verify))
-    return CMSD_ERR_ARG;
-  if (draft_stride < vocab || target_stride < vocab) return CMSD_ERR_ARG;
-  if (batch == 0) return CMSD_OK;
+  const cmsd_status e = pass_setup(draft_logits, draft_stride, target_logits, target_stride, drafted, uniforms, dtype,
+                                   batch, k_max, vocab, conf, draft, verify, adaptive, draft_stats, draft_len,
+                                   target_stats, n_accepted, next_token, workspace, workspace_bytes,
+                                   cmsd_verify_workspace_bytes(batch, k_max, vocab), a);
+  if (e != CMSD_OK || batch == 0) return e;
   const size_t es = dtype == CMSD_F32 ? 4 : 2;
   const int64_t drows = (int64_t)batch * k_max, trows = (int64_t)batch * (k_max + 1);
-  if (drows + trows > INT32_MAX || draft_stride > INT64_MAX / drows || target_stride > INT64_MAX / trows)
-    return CMSD_ERR_ARG;
-  if ((int64_t)batch * verify_slices(vocab, 4) > INT32_MAX) return CMSD_ERR_ARG;
-  if (!draft_logits || !target_logits || !drafted || (!uniforms && verify->mode != CMSD_MODE_GREEDY) ||
-      !draft_stats || !draft_len || !target_stats || !n_accepted || !next_token || !workspace)
-    return CMSD_ERR_ARG;
-  if (workspace_bytes < cmsd_verify_workspace_bytes(batch, k_max, vocab) || !aligned(workspace, 8)) return CMSD_ERR_ARG;
-  if (!aligned(draft_logits, es) || !aligned(target_logits, es) || !aligned(drafted, 4) || !aligned(uniforms, 4) ||
-      !aligned(draft_stats, 4) || !aligned(draft_len, 4) || !aligned(target_stats, 4) || !aligned(n_accepted, 4) ||
-      !aligned(next_token, 4))
-    return CMSD_ERR_ARG;
-  a.draft = draft_logits;
-  a.dstride = draft_stride;
-  a.dstats = draft_stats;
-  a.dstats_out = draft_stats;
-  a.target = target_logits;
-  a.tstride = target_stride;
-  a.target_rows = trows;
-  a.drafted = drafted;
-  a.unif = uniforms;
-  a.B = batch;
-  a.k_max = k_max;
-  a.V = vocab;
-  a.mode = verify->mode;
-  a.beta = verify->top_beta;
-  a.tau_base = verify->tau_base;
-  a.gamma = verify->gamma;
-  a.tstats = target_stats;
-  a.n_acc = n_accepted;
-  a.next_tok = next_token;
-  a.klen_out = draft_len;
-  a.k_min = draft->k_min;
-  a.alpha = draft->alpha;
-  a.adaptive = adaptive;
   const hipStream_t st = as_stream(stream);
   const int S = verify_slices(vocab, (int)es);
   const int SW = (S + kSubPerWG - 1) / kSubPerWG;
   SlicePart* ws = static_cast<SlicePart*>(workspace);
-  a.pslots = reinterpret_cast<PassSlot*>(ws + (size_t)batch * verify_slices(vocab, 4));
-  static_assert(sizeof(PassSlot) == sizeof(RowSlot), "the pass uses the verify workspace layout");
   const unsigned gp = (unsigned)((int64_t)batch * SW);
   const int bd = row_block(drows + trows, vocab * (int64_t)es);
   if (row_events && hipEventRecord(static_cast<hipEvent_t>(row_events[0]), st) != hipSuccess) return CMSD_ERR_LAUNCH;
@@ -2066,6 +2180,40 @@ cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, cons
     hipLaunchKernelGGL((k_final_parts<Bf16, true>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
     hipLaunchKernelGGL((k_final_sample<Bf16, true>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   }
+  return launched();
+}
+
+size_t cmsd_logit_pass_fused_workspace_bytes(int32_t batch, int32_t k_max, int64_t vocab) {
+  const size_t v = cmsd_verify_workspace_bytes(batch, k_max, vocab);
+  if (v == 0 || k_max > 63) return 0;
+  return v + (((size_t)batch * sizeof(int32_t) + 7u) & ~(size_t)7u);
+}
+
+cmsd_status cmsd_logit_pass_fused(const void* draft_logits, int64_t draft_stride, const void* target_logits,
+                                  int64_t target_stride, const int32_t* drafted, const float* uniforms,
+                                  int32_t dtype, int32_t batch, int32_t k_max, int64_t vocab,
+                                  const cmsd_conf_params* conf, const cmsd_draft_params* draft,
+                                  const cmsd_verify_params* verify, int32_t adaptive, cmsd_row_stats* draft_stats,
+                                  int32_t* draft_len, cmsd_target_stats* target_stats, int32_t* n_accepted,
+                                  int32_t* next_token, void* workspace, size_t workspace_bytes, void* stream) {
+  VerifyArgs a{};
+  const cmsd_status e = pass_setup(draft_logits, draft_stride, target_logits, target_stride, drafted, uniforms, dtype,
+                                   batch, k_max, vocab, conf, draft, verify, adaptive, draft_stats, draft_len,
+                                   target_stats, n_accepted, next_token, workspace, workspace_bytes,
+                                   cmsd_logit_pass_fused_workspace_bytes(batch, k_max, vocab), a);
+  if (e != CMSD_OK || batch == 0) return e;
+  const int es = dtype == CMSD_F32 ? 4 : 2;
+  const int64_t rows = (int64_t)batch * (2 * k_max + 1);
+  const int S = verify_slices(vocab, es);
+  SlicePart* ws = static_cast<SlicePart*>(workspace);
+  // the counters end the workspace (its size rounded down to 4 bytes): calls of any
+  // batch that fits share them, clear of the slice records and row slots at its start
+  int32_t* cnt = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + (workspace_bytes & ~(size_t)3)) - batch;
+  const hipStream_t st = as_stream(stream);
+  if (dtype == CMSD_F32)
+    hipLaunchKernelGGL((k_fused_pass<float>), dim3((unsigned)rows), dim3(kFusedBD), 0, st, a, S, ws, cnt);
+  else
+    hipLaunchKernelGGL((k_fused_pass<Bf16>), dim3((unsigned)rows), dim3(kFusedBD), 0, st, a, S, ws, cnt);
   return launched();
 }
 

@@ -108,3 +108,19 @@ class LogitPass:
                              draft_stats=self.stats, draft_len=self.k, target_stats=self.tstats,
                              n_accepted=self.n_acc, next_token=self.next_tok, workspace=self.ws,
                              row_events=row_events, stream=stream)
+
+    def logit_pass_fused(self, draft, target, drafted, uniforms, stream=None, adaptive=False) -> None:
+        """The same iteration as one cmsd_logit_pass_fused call: a single launch, for
+        small batches (dense target layout only).  Its zero-filled workspace is
+        allocated on first use and kept."""
+        if not self.dense:
+            raise ValueError("cmsd_logit_pass_fused takes the dense target layout; this LogitPass is packed")
+        if getattr(self, "fws", None) is None:
+            self.fws = cmsd.fused_workspace(self.B, self.k_max, self.V, self.stats.device)
+        p = self.p
+        cmsd.cmsd_logit_pass_fused(draft, target, drafted, uniforms, batch=self.B, k_max=self.k_max,
+                                   lambdas=p.lambdas, beta_margin=p.beta_margin, k_min=p.k_min, alpha=p.alpha,
+                                   mode=p.mode, top_beta=p.top_beta, tau_base=p.tau_base, gamma=p.gamma,
+                                   adaptive=adaptive, draft_stats=self.stats, draft_len=self.k,
+                                   target_stats=self.tstats, n_accepted=self.n_acc, next_token=self.next_tok,
+                                   workspace=self.fws, stream=stream)

@@ -15,11 +15,12 @@ def test_exports_every_declared_symbol():
     assert set(syms) >= {"cmsd_confidence", "cmsd_confidence_var", "cmsd_draft_len", "cmsd_verify",
                          "cmsd_verify_workspace_bytes",
                          "cmsd_draft_sample", "cmsd_draft_sample_workspace_bytes", "cmsd_status_string",
-                         "cmsd_version", "cmsd_logit_pass"}
+                         "cmsd_version", "cmsd_logit_pass", "cmsd_logit_pass_fused",
+                         "cmsd_logit_pass_fused_workspace_bytes"}
     lib = cm.lib()
     for s in syms:
         assert hasattr(lib, s), s
-    assert lib.cmsd_version() == (1 << 16) | 3
+    assert lib.cmsd_version() == (1 << 16) | 4
     assert lib.cmsd_status_string(0) == b"ok"
     assert lib.cmsd_status_string(1) == b"invalid argument"
 
@@ -171,3 +172,43 @@ def _lpass(**kw):
 ])
 def test_logit_pass_argument_errors(kw, want):
     assert _lpass(**kw) == want
+
+
+def _fpass(**kw):
+    a = dict(dl=P, ds=1024, tl=P, ts=1024, dr=P, u=P, dtype=cm.CMSD_BF16, B=4, K=8, V=1024,
+             cp=cm.ConfParams(0.25, 0.25, 0.5, 1.0), dp=cm.DraftParams(1, 8, 1.0), vp=cm.VerifyParams(1, 3, 0.1, 1.0),
+             ad=0, dst=P, kl=P, tst=P, na=P, nt=P, ws=P, wsb=1 << 20)
+    a.update(kw)
+    ref = lambda x: C.byref(x) if x is not None else None  # noqa: E731
+    return cm.lib().cmsd_logit_pass_fused(a["dl"], a["ds"], a["tl"], a["ts"], a["dr"], a["u"], a["dtype"], a["B"],
+                                          a["K"], a["V"], ref(a["cp"]), ref(a["dp"]), ref(a["vp"]), a["ad"], a["dst"],
+                                          a["kl"], a["tst"], a["na"], a["nt"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(dtype=3), cm.CMSD_ERR_DTYPE),
+    (dict(cp=None), cm.CMSD_ERR_ARG),
+    (dict(dp=cm.DraftParams(1, 7, 1.0)), cm.CMSD_ERR_ARG),
+    (dict(K=64, dp=cm.DraftParams(1, 64, 1.0)), cm.CMSD_ERR_ARG),
+    (dict(V=1), cm.CMSD_ERR_ARG),
+    (dict(ws=None), cm.CMSD_ERR_ARG),
+    (dict(ws=P + 4), cm.CMSD_ERR_ARG),
+    (dict(u=None), cm.CMSD_ERR_ARG),
+    (dict(nt=None), cm.CMSD_ERR_ARG),
+    (dict(B=-1), cm.CMSD_ERR_ARG),
+    (dict(B=0, dl=None, tl=None, dr=None, ws=None, wsb=0), cm.CMSD_OK),
+])
+def test_logit_pass_fused_argument_errors(kw, want):
+    assert _fpass(**kw) == want
+
+
+def test_logit_pass_fused_workspace():
+    f = cm.lib().cmsd_logit_pass_fused_workspace_bytes
+    v = cm.lib().cmsd_verify_workspace_bytes
+    # the verify workspace, then one 4-byte counter per sequence (rounded up to 8 bytes)
+    assert f(8, 8, 32000) == v(8, 8, 32000) + 32
+    assert f(3, 8, 32000) == v(3, 8, 32000) + 16
+    assert f(0, 8, 32000) == 0 and f(4, 64, 32000) == 0 and f(4, 8, 1) == 0
+    # exactly the verify workspace is one counter area too small
+    assert _fpass(wsb=v(4, 8, 1024)) == cm.CMSD_ERR_ARG
+    assert _fpass(wsb=f(4, 8, 1024) - 1) == cm.CMSD_ERR_ARG

@@ -23,7 +23,7 @@ int main(void) {
   cmsd_row_stats st;
   float x = 0.f;
   int32_t k = 0, off = 0;
-  if (cmsd_version() != ((1 << 16) | 3)) bad |= 1;
+  if (cmsd_version() != ((1 << 16) | 4)) bad |= 1;
   if (strcmp(cmsd_status_string(CMSD_OK), "ok") != 0) bad |= 2;
   if (cmsd_verify_workspace_bytes(0, 8, 1000) != 0) bad |= 4;
   if (cmsd_verify_workspace_bytes(4, 8, 1000) == 0) bad |= 8;
@@ -37,6 +37,9 @@ int main(void) {
   if (cmsd_verify(&x, 100, &st, &x, 100, 9, &off, &k, &k, &x, CMSD_F32, 1, 8, 100, &vp, NULL, &k, &k,
                   &x, 1, NULL) != CMSD_ERR_ARG) bad |= 256;
   if (cmsd_draft_sample_workspace_bytes(3, 1) != 0) bad |= 512;
+  if (cmsd_logit_pass_fused_workspace_bytes(4, 8, 1000) != cmsd_verify_workspace_bytes(4, 8, 1000) + 16) bad |= 1024;
+  if (cmsd_logit_pass_fused(&x, 100, &x, 100, &k, &x, 9, 1, 8, 100, &cp, &dp, &vp, 0, &st, &k, NULL, &k, &k, &x,
+                            1 << 20, NULL) != CMSD_ERR_DTYPE) bad |= 2048;
   printf("bad=%d\n", bad);
   return bad;
 }
