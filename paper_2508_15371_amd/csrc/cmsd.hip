@@ -24,6 +24,9 @@
 //                   grid.
 //   k_pass_decide   cmsd_logit_pass, one wave per sequence: draft length, accept
 //                   tests and first rejection, written once for the final kernels.
+//   k_fused_pass    cmsd_logit_pass_fused, one launch for small batches: the row pass,
+//                   then the last row workgroup of each sequence (atomic count behind
+//                   a device fence) decides and samples with the same functions.
 //   k_draft_parts / k_draft_pick   the same slice machinery for one softmax sample
 //                   per drafter row.
 //
