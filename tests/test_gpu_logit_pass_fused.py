@@ -61,7 +61,7 @@ def _counters(ws, B):
 
 @pytest.mark.parametrize("adaptive", [False, True])
 @pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY])
-@pytest.mark.parametrize("name", ["tiny", "c2"])
+@pytest.mark.parametrize("name", ["tiny", "b1", "c2"])
 def test_fused_equals_logit_pass_and_oracle(cm, name, mode, adaptive):
     print(f"[fused parity] start {name} mode={mode} adaptive={adaptive}", flush=True)
     cfg = W.CONFIGS[name]

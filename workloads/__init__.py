@@ -104,6 +104,8 @@ CONFIGS = {
     "c5": Config("c5", 4, 512, 16, 32000, "bf16", ragged=True),
     # sweep point at the top of the metric's vocabulary range, with c2's row recipe
     "v152k": Config("v152k", 5, 64, 8, 152064, "bf16", style="c2"),
+    # one sequence (single-stream decoding latency), with c2's row recipe
+    "b1": Config("b1", 6, 1, 8, 32000, "bf16", style="c2"),
 }
 
 
