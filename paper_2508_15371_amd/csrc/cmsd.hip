@@ -31,7 +31,8 @@
 //                   per drafter row.
 //
 // Compile-time tuning knobs (defaults are the measured best on gfx950): CMSD_STREAM_DEPTH
-// (row-pass rounds of loads in flight), CMSD_KEEP_MAX_ROUND (64-thread drafter rows keep
+// and CMSD_DEEP_DEPTH (row-pass rounds of loads in flight for short and long launches),
+// CMSD_KEEP_MAX_ROUND (64-thread drafter rows keep
 // their max round in registers), CMSD_SLICE_UNITS and CMSD_SUB_PER_WG (final-token slice
 // size and slices per one-wave workgroup).
 //
@@ -469,7 +470,7 @@ __device__ __forceinline__ cmsd_row_stats row_stats_record(float m, float z2, do
 #ifndef CMSD_KEEP_MAX_ROUND
 #define CMSD_KEEP_MAX_ROUND 1
 #endif
-template <typename T, int BD, bool VAR>
+template <typename T, int BD, bool VAR, int DEPTH = CMSD_STREAM_DEPTH>
 __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, const ConfArgs& a,
                                          cmsd_row_stats* __restrict__ out, float* __restrict__ var_out) {
   using E = Elem<T>;
@@ -497,7 +498,7 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
 
     // full rounds, next round's loads issued before the current one is consumed
     // the head elements are loaded and folded in once the first rounds are requested
-    stream_rounds<U, BD, CMSD_STREAM_DEPTH>(vp, nr, t, [&] {
+    stream_rounds<U, BD, DEPTH>(vp, nr, t, [&] {
       if (t < g.head) conf_one<VAR>(s, E::load(row + t), 0);
     }, [&](const uint4 (&raw)[U], int64_t k) {
       float f[N];
@@ -677,12 +678,12 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
   }
 }
 
-template <typename T, int BD, bool VAR>
+template <typename T, int BD, bool VAR, int DEPTH>
 __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits, int64_t n_rows, int64_t V,
                                                    int64_t stride, ConfArgs a, cmsd_row_stats* __restrict__ out,
                                                    float* __restrict__ var_out) {
   for (int64_t r = blockIdx.x; r < n_rows; r += gridDim.x)
-    conf_row<T, BD, VAR>(logits + r * stride, V, a, out + r, VAR ? var_out + r : nullptr);
+    conf_row<T, BD, VAR, DEPTH>(logits + r * stride, V, a, out + r, VAR ? var_out + r : nullptr);
 }
 
 // ----------------------------------------------------------------------------- K2 draft length
@@ -816,7 +817,7 @@ __device__ __forceinline__ void target_chunk(TargetState& s, const float* f, uin
 
 // The target row pass.  prep() resolves the drafted token (and with it `count` and
 // `gz`) while the first rounds of the row are already in flight.
-template <typename T, int BD, typename P>
+template <typename T, int BD, int DEPTH, typename P>
 __device__ __forceinline__ void target_stream(const T* row, const Geom& g, const bool& count, const float& gz,
                                               int beta, TargetState& s, int& wcnt, P&& prep) {
   using E = Elem<T>;
@@ -825,7 +826,7 @@ __device__ __forceinline__ void target_stream(const T* row, const Geom& g, const
   const uint4* vp = reinterpret_cast<const uint4*>(row + g.head);
   const int64_t per_round = (int64_t)U * BD;
   const int64_t nr = g.nvec / per_round;
-  stream_rounds<U, BD, CMSD_STREAM_DEPTH>(
+  stream_rounds<U, BD, DEPTH>(
       vp, nr, t,
       [&] {
         // the head element is requested with the rounds, before prep() waits for
@@ -891,7 +892,7 @@ __device__ __forceinline__ int accept_test(int mode, int beta, float tau_base, f
 // One target row.  PASS = false: a packed row of cmsd_verify (sequence found from the
 // offsets, accept test made here).  PASS = true: dense row r = b*(k_max+1) + i of the
 // single-call pass, whose accept test waits for the drafter stats (PassSlot).
-template <typename T, int BD, bool PASS>
+template <typename T, int BD, bool PASS, int DEPTH = CMSD_STREAM_DEPTH>
 __device__ __forceinline__ void target_row(const VerifyArgs& a, int64_t r) {
   using E = Elem<T>;
   __shared__ double sd[BD / 64];
@@ -976,7 +977,7 @@ __device__ __forceinline__ void target_row(const VerifyArgs& a, int64_t r) {
   };
   TargetState s;
   int wcnt = 0;
-  target_stream<T, BD>(trow, g, count, gz, a.beta, s, wcnt, prep);
+  target_stream<T, BD, DEPTH>(trow, g, count, gz, a.beta, s, wcnt, prep);
 
   const float m = block_all_f<BD>(s.t1, OpMax(), sf);
   const float ms_row = m * kLog2e;
@@ -1039,14 +1040,15 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
 
 // The row pass of cmsd_logit_pass: drafter rows (stats) and dense target rows in one
 // grid, drafter rows first; the two kinds of row do not depend on each other.
-template <typename T, int BD>
+template <typename T, int BD, int DEPTH>
 __global__ __launch_bounds__(BD) void k_row_pass(VerifyArgs a) {
   const int64_t nd = (int64_t)a.B * a.k_max;
   const int64_t r = blockIdx.x;
   if (r < nd)
-    conf_row<T, BD, false>(reinterpret_cast<const T*>(a.draft) + r * a.dstride, a.V, a.ca, a.dstats_out + r, nullptr);
+    conf_row<T, BD, false, DEPTH>(reinterpret_cast<const T*>(a.draft) + r * a.dstride, a.V, a.ca, a.dstats_out + r,
+                                  nullptr);
   else
-    target_row<T, BD, true>(a, r - nd);
+    target_row<T, BD, true, DEPTH>(a, r - nd);
 }
 
 // ----------------------------------------------------------------------------- K4 final token
@@ -1849,16 +1851,42 @@ int row_block(int64_t n_rows, int64_t row_bytes) {
   return 256;
 }
 
+// Rounds in flight per thread for a streaming-row launch.  Long launches (several
+// generations of workgroups: at least 16 rows per compute unit for the joint row pass,
+// 32 for the confidence pass alone, as c4's row pass and c5's 8192 drafter rows) stream
+// better with three rounds in flight; shorter ones keep two, whose smaller register
+// count lets more of their rows run at once.  The depth only schedules loads: the
+// arithmetic, and so every result, is the same.  CMSD_RING_DEPTH (2 or 3) in the
+// environment forces it.
+#ifndef CMSD_DEEP_DEPTH
+#define CMSD_DEEP_DEPTH 3
+#endif
+bool deep_ring(int64_t n_rows, int rows_per_cu) {
+  if (const char* e = getenv("CMSD_RING_DEPTH")) return atoi(e) == 3;
+  return n_rows >= rows_per_cu * (int64_t)device_cus();
+}
+
+template <typename T, bool VAR, int DEPTH>
+void launch_confidence_d(int bd, const T* logits, int64_t n_rows, int64_t V, int64_t stride, const ConfArgs& a,
+                         cmsd_row_stats* out, float* var, hipStream_t st) {
+  const dim3 grid((unsigned)n_rows);
+  if (bd == 64)
+    hipLaunchKernelGGL((k_confidence<T, 64, VAR, DEPTH>), grid, dim3(64), 0, st, logits, n_rows, V, stride, a, out,
+                       var);
+  else if (bd == 128)
+    hipLaunchKernelGGL((k_confidence<T, 128, VAR, DEPTH>), grid, dim3(128), 0, st, logits, n_rows, V, stride, a, out,
+                       var);
+  else
+    hipLaunchKernelGGL((k_confidence<T, 256, VAR, DEPTH>), grid, dim3(256), 0, st, logits, n_rows, V, stride, a, out,
+                       var);
+}
 template <typename T, bool VAR>
 void launch_confidence(int bd, const T* logits, int64_t n_rows, int64_t V, int64_t stride, const ConfArgs& a,
                        cmsd_row_stats* out, float* var, hipStream_t st) {
-  const dim3 grid((unsigned)n_rows);
-  if (bd == 64)
-    hipLaunchKernelGGL((k_confidence<T, 64, VAR>), grid, dim3(64), 0, st, logits, n_rows, V, stride, a, out, var);
-  else if (bd == 128)
-    hipLaunchKernelGGL((k_confidence<T, 128, VAR>), grid, dim3(128), 0, st, logits, n_rows, V, stride, a, out, var);
+  if (deep_ring(n_rows, 32))
+    launch_confidence_d<T, VAR, CMSD_DEEP_DEPTH>(bd, logits, n_rows, V, stride, a, out, var, st);
   else
-    hipLaunchKernelGGL((k_confidence<T, 256, VAR>), grid, dim3(256), 0, st, logits, n_rows, V, stride, a, out, var);
+    launch_confidence_d<T, VAR, CMSD_STREAM_DEPTH>(bd, logits, n_rows, V, stride, a, out, var, st);
 }
 
 template <typename T>
@@ -1872,15 +1900,22 @@ void launch_target_rows(int bd, const VerifyArgs& a, hipStream_t st) {
     hipLaunchKernelGGL((k_target_rows<T, 256>), grid, dim3(256), 0, st, a);
 }
 
-template <typename T>
-void launch_row_pass(int bd, const VerifyArgs& a, int64_t rows, hipStream_t st) {
+template <typename T, int DEPTH>
+void launch_row_pass_d(int bd, const VerifyArgs& a, int64_t rows, hipStream_t st) {
   const dim3 grid((unsigned)rows);
   if (bd == 64)
-    hipLaunchKernelGGL((k_row_pass<T, 64>), grid, dim3(64), 0, st, a);
+    hipLaunchKernelGGL((k_row_pass<T, 64, DEPTH>), grid, dim3(64), 0, st, a);
   else if (bd == 128)
-    hipLaunchKernelGGL((k_row_pass<T, 128>), grid, dim3(128), 0, st, a);
+    hipLaunchKernelGGL((k_row_pass<T, 128, DEPTH>), grid, dim3(128), 0, st, a);
   else
-    hipLaunchKernelGGL((k_row_pass<T, 256>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((k_row_pass<T, 256, DEPTH>), grid, dim3(256), 0, st, a);
+}
+template <typename T>
+void launch_row_pass(int bd, const VerifyArgs& a, int64_t rows, hipStream_t st) {
+  if (deep_ring(rows, 16))
+    launch_row_pass_d<T, CMSD_DEEP_DEPTH>(bd, a, rows, st);
+  else
+    launch_row_pass_d<T, CMSD_STREAM_DEPTH>(bd, a, rows, st);
 }
 
 // Number of vocabulary slices of the final-token pass: units are 16-byte vectors
