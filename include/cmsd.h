@@ -20,7 +20,8 @@
  * Conventions shared by every call
  *   - All array pointers are DEVICE pointers (hipMalloc / torch CUDA tensors);
  *     params structs are HOST pointers read during the call.  The caller owns
- *     every buffer; the library keeps no state and allocates no memory.
+ *     every buffer and the library allocates no memory.  Its only state is the
+ *     row-kernel shape override of cmsd_set_row_shape.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Calls
  *     only enqueue work and return; results are ready when the stream is.
  *   - Argument errors are detected on the host before anything is enqueued and
@@ -267,9 +268,15 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
  *                   k_max, vocab) bytes, 8-byte aligned, owned by the caller, as for
  *                   cmsd_verify (calls sharing it must be ordered).
  *   workspace_bytes its size.
+ *   row_events      NULL, or a host array of two hipEvent_t (created by the caller):
+ *                   the row-pass launch is made with hipExtLaunchKernel, which stamps
+ *                   them with that kernel's own start and end, so the caller can time
+ *                   the bandwidth-bound row pass alone on its stream.  Results do not
+ *                   depend on it.
  * The arithmetic is the separate calls': the outputs are bit-identical to theirs
  * whenever the row kernels run with the same workgroup size (chosen from the number
- * of rows in the launch), else equal up to the rounding of the reduction order.
+ * of rows in the launch and their length, or forced by cmsd_set_row_shape), else
+ * equal up to the rounding of the reduction order.
  * Errors: CMSD_ERR_ARG, CMSD_ERR_DTYPE, CMSD_ERR_LAUNCH.
  */
 cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, const void* target_logits,
@@ -299,11 +306,16 @@ cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, cons
  *                   one int32 counter per sequence: they must be zero before the first
  *                   call with this workspace (zero the whole buffer once when
  *                   allocating it), and every call leaves them zero, so one workspace
- *                   serves calls of any batch it fits.  Calls sharing a workspace must
- *                   be ordered (same stream); after another call (cmsd_verify,
- *                   cmsd_logit_pass) has used it, zero it again.
+ *                   serves repeated calls of one (batch, k_max, vocab).  A call of
+ *                   another shape lays its records over other bytes, which may hold
+ *                   the counters of a former shape: zero the workspace again before
+ *                   changing batch, k_max or vocab (or keep one workspace per shape),
+ *                   and after another call (cmsd_verify, cmsd_logit_pass) has used it.
+ *                   Calls sharing a workspace must be ordered (same stream).
  * The outputs are bit-identical to cmsd_logit_pass's when that call's row kernels
- * run with 256 threads (as it chooses for fewer than 16 rows per compute unit).
+ * run with 256 threads: it chooses 256 for rows over 128 KiB and for launches of
+ * fewer than 8 rows per compute unit (batch*(2*k_max+1) < 2048 on 256 compute
+ * units); cmsd_set_row_shape(256, 0) forces it.
  */
 cmsd_status cmsd_logit_pass_fused(const void* draft_logits, int64_t draft_stride, const void* target_logits,
                                   int64_t target_stride, const int32_t* drafted, const float* uniforms,
@@ -317,6 +329,20 @@ cmsd_status cmsd_logit_pass_fused(const void* draft_logits, int64_t draft_stride
  * plus 4 bytes per sequence (rounded up to 8) for the counters; 0 for batch <= 0 or
  * an invalid k_max (outside [1, 63]) / vocab. */
 size_t cmsd_logit_pass_fused_workspace_bytes(int32_t batch, int32_t k_max, int64_t vocab);
+
+/*
+ * cmsd_set_row_shape - launch shape of the streaming row kernels (one workgroup per
+ * logit row: cmsd_confidence, cmsd_confidence_var, cmsd_verify's target rows, the row
+ * pass of cmsd_logit_pass), for tuning and for tests that
+ * cover every shape.  Process-wide; applies to launches made after it returns.
+ *   threads     0 (chosen per launch from its rows and row length), 64, 128 or 256.
+ *   ring_depth  0 (chosen per launch), 2 or 3: rounds of 16-byte loads kept in flight
+ *               per thread.  It schedules loads only: results are identical.
+ * The workgroup size fixes the reduction order, so outputs are bit-identical across
+ * calls with the same size and equal up to rounding otherwise.  cmsd_logit_pass_fused
+ * always uses 256 threads.  Errors: CMSD_ERR_ARG for any other value.
+ */
+cmsd_status cmsd_set_row_shape(int32_t threads, int32_t ring_depth);
 
 /* Workspace cmsd_verify needs for `batch` sequences of up to `k_max` drafts over
  * `vocab`: per sequence, one 32-byte record per vocabulary slice (256 16-byte
@@ -351,7 +377,7 @@ size_t cmsd_draft_sample_workspace_bytes(int64_t n_rows, int64_t vocab);
 /* Human-readable name of a status code (static string). */
 const char* cmsd_status_string(cmsd_status s);
 
-/* Library ABI version, (major << 16) | minor: 1.4 (1.3 plus cmsd_logit_pass_fused). */
+/* Library ABI version, (major << 16) | minor: 1.5 (1.4 plus cmsd_set_row_shape). */
 int32_t cmsd_version(void);
 
 #ifdef __cplusplus

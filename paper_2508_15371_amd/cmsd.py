@@ -73,6 +73,8 @@ def _load() -> C.CDLL:
                                           C.POINTER(DraftParams), C.POINTER(VerifyParams), i32, vp, vp, vp, vp, vp,
                                           vp, C.c_size_t, vp]
     lib.cmsd_logit_pass_fused.restype = C.c_int
+    lib.cmsd_set_row_shape.argtypes = [i32, i32]
+    lib.cmsd_set_row_shape.restype = C.c_int
     lib.cmsd_logit_pass_fused_workspace_bytes.argtypes = [i32, i32, i64]
     lib.cmsd_logit_pass_fused_workspace_bytes.restype = C.c_size_t
     lib.cmsd_status_string.argtypes = [C.c_int]
@@ -136,6 +138,12 @@ def _buf(t: torch.Tensor, name: str, dtype: torch.dtype, min_elems: int, device:
         raise ValueError(f"{name} has {t.numel()} elements; {min_elems} are needed")
     if t.device != device:
         raise ValueError(f"{name} must be on {device}, not {t.device}")
+
+
+def cmsd_set_row_shape(threads: int = 0, ring_depth: int = 0) -> None:
+    """Force the row kernels' workgroup size (64/128/256) and loads-in-flight depth
+    (2/3); 0 restores the per-launch choice.  Process-wide."""
+    _check("cmsd_set_row_shape", _lib.cmsd_set_row_shape(int(threads), int(ring_depth)))
 
 
 def _events(evs):
@@ -362,8 +370,8 @@ def cmsd_logit_pass(draft_logits: torch.Tensor, target_logits: torch.Tensor, dra
     ``draft_logits`` [batch*k_max, V], ``target_logits`` [batch*(k_max+1), V] (same
     dtype), ``drafted`` int32 [batch*k_max], ``uniforms`` float32 [batch*(k_max+1)]
     (None in GREEDY mode).  ``row_events``: optional pair of recorded-once
-    ``torch.cuda.Event`` objects, recorded again around the row-pass kernel.  Returns
-    the output tensors by name."""
+    ``torch.cuda.Event`` objects that the row-pass launch stamps with its own start and
+    end.  Returns the output tensors by name."""
     outs = {"draft_stats": draft_stats, "draft_len": draft_len, "target_stats": target_stats,
             "n_accepted": n_accepted, "next_token": next_token}
     out, dst, tst, V, cp, dp, vp_ = _pass_args(draft_logits, target_logits, drafted, uniforms, batch, k_max, lambdas,
@@ -403,3 +411,4 @@ def cmsd_logit_pass_fused(draft_logits: torch.Tensor, target_logits: torch.Tenso
         _ptr(out["n_accepted"]), _ptr(out["next_token"]), _ptr(ws),
         ws.numel() * ws.element_size(), _stream(stream)))
     return out
+

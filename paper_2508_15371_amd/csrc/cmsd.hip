@@ -40,10 +40,13 @@
 // v_exp_f32; per-thread partial sums are fp32 over 32-element chunks, the
 // cross-thread combines and every decision-side formula are fp64.  Reductions have
 // a fixed order, so results are bit-reproducible run to run.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
+
+#include <atomic>
 
 #include "cmsd.h"
 
@@ -1822,12 +1825,16 @@ bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) %
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 cmsd_status launched() { return hipGetLastError() == hipSuccess ? CMSD_OK : CMSD_ERR_LAUNCH; }
 
+// Launch-shape overrides of the row kernels, set by cmsd_set_row_shape (0 = chosen
+// per launch).  Process-wide; read once per launch.
+std::atomic<int> g_row_block{0};
+std::atomic<int> g_ring_depth{0};
+
 // Workgroup size of the row kernels (one workgroup per logit row).  A row pays a
 // fixed cost (pipeline fill, epilogue reductions, the argmax rescan) besides its
 // streaming time, so short rows go to narrower groups, each streaming its row for
 // longer, as long as the launch still fills every SIMD with 4 waves; long rows and
-// short launches use 256 threads.  CMSD_ROW_BLOCK (64, 128 or 256) in the
-// environment overrides the choice.
+// short launches use 256 threads.  cmsd_set_row_shape overrides the choice.
 int device_cus() {
   static int cache[64] = {0};
   int dev = 0;
@@ -1839,10 +1846,7 @@ int device_cus() {
   return n;
 }
 int row_block(int64_t n_rows, int64_t row_bytes) {
-  if (const char* e = getenv("CMSD_ROW_BLOCK")) {
-    const int v = atoi(e);
-    if (v == 64 || v == 128 || v == 256) return v;
-  }
+  if (const int v = g_row_block.load(std::memory_order_relaxed)) return v;
   const int64_t waves = 16 * (int64_t)device_cus();  // 4 waves on each of 4 SIMDs per CU
   if (row_bytes <= (int64_t)128 << 10) {
     if (n_rows >= waves) return 64;
@@ -1856,13 +1860,12 @@ int row_block(int64_t n_rows, int64_t row_bytes) {
 // 32 for the confidence pass alone, as c4's row pass and c5's 8192 drafter rows) stream
 // better with three rounds in flight; shorter ones keep two, whose smaller register
 // count lets more of their rows run at once.  The depth only schedules loads: the
-// arithmetic, and so every result, is the same.  CMSD_RING_DEPTH (2 or 3) in the
-// environment forces it.
+// arithmetic, and so every result, is the same.  cmsd_set_row_shape forces it.
 #ifndef CMSD_DEEP_DEPTH
 #define CMSD_DEEP_DEPTH 3
 #endif
 bool deep_ring(int64_t n_rows, int rows_per_cu) {
-  if (const char* e = getenv("CMSD_RING_DEPTH")) return atoi(e) == 3;
+  if (const int d = g_ring_depth.load(std::memory_order_relaxed)) return d == 3;
   return n_rows >= rows_per_cu * (int64_t)device_cus();
 }
 
@@ -1900,22 +1903,31 @@ void launch_target_rows(int bd, const VerifyArgs& a, hipStream_t st) {
     hipLaunchKernelGGL((k_target_rows<T, 256>), grid, dim3(256), 0, st, a);
 }
 
-template <typename T, int DEPTH>
-void launch_row_pass_d(int bd, const VerifyArgs& a, int64_t rows, hipStream_t st) {
-  const dim3 grid((unsigned)rows);
-  if (bd == 64)
-    hipLaunchKernelGGL((k_row_pass<T, 64, DEPTH>), grid, dim3(64), 0, st, a);
-  else if (bd == 128)
-    hipLaunchKernelGGL((k_row_pass<T, 128, DEPTH>), grid, dim3(128), 0, st, a);
+// The joint row pass.  With events, the launch goes through hipExtLaunchKernel, which
+// stamps them with the kernel's own start and end (the caller times the launch alone).
+template <typename K>
+void launch_rows(K kernel, int64_t rows, int bd, const VerifyArgs& a, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+  const dim3 grid((unsigned)rows), block((unsigned)bd);
+  if (e0)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, st, e0, e1, 0, a);
   else
-    hipLaunchKernelGGL((k_row_pass<T, 256, DEPTH>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL(kernel, grid, block, 0, st, a);
+}
+template <typename T, int DEPTH>
+void launch_row_pass_d(int bd, const VerifyArgs& a, int64_t rows, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+  if (bd == 64)
+    launch_rows(k_row_pass<T, 64, DEPTH>, rows, bd, a, st, e0, e1);
+  else if (bd == 128)
+    launch_rows(k_row_pass<T, 128, DEPTH>, rows, bd, a, st, e0, e1);
+  else
+    launch_rows(k_row_pass<T, 256, DEPTH>, rows, bd, a, st, e0, e1);
 }
 template <typename T>
-void launch_row_pass(int bd, const VerifyArgs& a, int64_t rows, hipStream_t st) {
+void launch_row_pass(int bd, const VerifyArgs& a, int64_t rows, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
   if (deep_ring(rows, 16))
-    launch_row_pass_d<T, CMSD_DEEP_DEPTH>(bd, a, rows, st);
+    launch_row_pass_d<T, CMSD_DEEP_DEPTH>(bd, a, rows, st, e0, e1);
   else
-    launch_row_pass_d<T, CMSD_STREAM_DEPTH>(bd, a, rows, st);
+    launch_row_pass_d<T, CMSD_STREAM_DEPTH>(bd, a, rows, st, e0, e1);
 }
 
 // Number of vocabulary slices of the final-token pass: units are 16-byte vectors
@@ -1972,15 +1984,14 @@ cmsd_status confidence_impl(const void* logits, int32_t dtype, int64_t n_rows, i
   return launched();
 }
 
-// Checks the arguments of the single-call pass and fills its kernel arguments (the
-// row slots sit after the per-dtype-independent slice records of the workspace).
+// Checks the arguments of the single-call pass (all but its workspace) and fills its
+// kernel arguments; bind_pass_workspace completes them.
 cmsd_status pass_setup(const void* draft_logits, int64_t draft_stride, const void* target_logits,
                        int64_t target_stride, const int32_t* drafted, const float* uniforms, int32_t dtype,
                        int32_t batch, int32_t k_max, int64_t vocab, const cmsd_conf_params* conf,
                        const cmsd_draft_params* draft, const cmsd_verify_params* verify, int32_t adaptive,
                        cmsd_row_stats* draft_stats, int32_t* draft_len, cmsd_target_stats* target_stats,
-                       int32_t* n_accepted, int32_t* next_token, void* workspace, size_t workspace_bytes,
-                       size_t workspace_need, VerifyArgs& a) {
+                       int32_t* n_accepted, int32_t* next_token, VerifyArgs& a) {
   if (dtype != CMSD_F32 && dtype != CMSD_BF16) return CMSD_ERR_DTYPE;
   if (!conf || !draft || !verify) return CMSD_ERR_ARG;
   if (batch < 0 || k_max < 1 || k_max > 63 || vocab < 2 || vocab > INT32_MAX) return CMSD_ERR_ARG;
@@ -1995,9 +2006,8 @@ cmsd_status pass_setup(const void* draft_logits, int64_t draft_stride, const voi
     return CMSD_ERR_ARG;
   if ((int64_t)batch * verify_slices(vocab, 4) > INT32_MAX) return CMSD_ERR_ARG;
   if (!draft_logits || !target_logits || !drafted || (!uniforms && verify->mode != CMSD_MODE_GREEDY) ||
-      !draft_stats || !draft_len || !target_stats || !n_accepted || !next_token || !workspace)
+      !draft_stats || !draft_len || !target_stats || !n_accepted || !next_token)
     return CMSD_ERR_ARG;
-  if (workspace_need == 0 || workspace_bytes < workspace_need || !aligned(workspace, 8)) return CMSD_ERR_ARG;
   if (!aligned(draft_logits, es) || !aligned(target_logits, es) || !aligned(drafted, 4) || !aligned(uniforms, 4) ||
       !aligned(draft_stats, 4) || !aligned(draft_len, 4) || !aligned(target_stats, 4) || !aligned(n_accepted, 4) ||
       !aligned(next_token, 4))
@@ -2025,9 +2035,45 @@ cmsd_status pass_setup(const void* draft_logits, int64_t draft_stride, const voi
   a.k_min = draft->k_min;
   a.alpha = draft->alpha;
   a.adaptive = adaptive;
-  static_assert(sizeof(PassSlot) == sizeof(RowSlot), "the pass uses the verify workspace layout");
-  a.pslots = reinterpret_cast<PassSlot*>(static_cast<SlicePart*>(workspace) + (size_t)batch * verify_slices(vocab, 4));
   return CMSD_OK;
+}
+
+// The caller's workspace of the single-call pass: per sequence, slice records first
+// (sized for fp32, the dtype with most slices), then the row slots.
+cmsd_status bind_pass_workspace(VerifyArgs& a, void* workspace, size_t workspace_bytes, size_t workspace_need) {
+  if (!workspace || workspace_need == 0 || workspace_bytes < workspace_need || !aligned(workspace, 8))
+    return CMSD_ERR_ARG;
+  static_assert(sizeof(PassSlot) == sizeof(RowSlot), "the pass uses the verify workspace layout");
+  a.pslots = reinterpret_cast<PassSlot*>(static_cast<SlicePart*>(workspace) + (size_t)a.B * verify_slices(a.V, 4));
+  return CMSD_OK;
+}
+
+// The launches of cmsd_logit_pass on a bound workspace: the joint row pass (bracketed
+// by the caller's events, if any), the per-sequence decisions, then the final-token
+// pair (not in GREEDY mode, whose final token is the row's top token).
+cmsd_status enqueue_logit_pass(const VerifyArgs& a, int32_t dtype, void* workspace, hipEvent_t e0, hipEvent_t e1,
+                               hipStream_t st) {
+  const int es = dtype == CMSD_F32 ? 4 : 2;
+  const int64_t drows = (int64_t)a.B * a.k_max, trows = (int64_t)a.B * (a.k_max + 1);
+  const int S = verify_slices(a.V, es);
+  const int SW = (S + kSubPerWG - 1) / kSubPerWG;
+  SlicePart* ws = static_cast<SlicePart*>(workspace);
+  const unsigned gp = (unsigned)((int64_t)a.B * SW);
+  const int bd = row_block(drows + trows, a.V * (int64_t)es);
+  if (dtype == CMSD_F32)
+    launch_row_pass<float>(bd, a, drows + trows, st, e0, e1);
+  else
+    launch_row_pass<Bf16>(bd, a, drows + trows, st, e0, e1);
+  hipLaunchKernelGGL(k_pass_decide, dim3((unsigned)a.B), dim3(64), 0, st, a);
+  if (a.mode == CMSD_MODE_GREEDY) return launched();
+  if (dtype == CMSD_F32) {
+    hipLaunchKernelGGL((k_final_parts<float, true>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
+    hipLaunchKernelGGL((k_final_sample<float, true>), dim3((unsigned)a.B), dim3(kSampleBD), 0, st, a, S, ws);
+  } else {
+    hipLaunchKernelGGL((k_final_parts<Bf16, true>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
+    hipLaunchKernelGGL((k_final_sample<Bf16, true>), dim3((unsigned)a.B), dim3(kSampleBD), 0, st, a, S, ws);
+  }
+  return launched();
 }
 
 }  // namespace
@@ -2045,7 +2091,7 @@ const char* cmsd_status_string(cmsd_status s) {
   return "unknown status";
 }
 
-int32_t cmsd_version(void) { return (1 << 16) | 4; }
+int32_t cmsd_version(void) { return (1 << 16) | 5; }
 
 size_t cmsd_draft_sample_workspace_bytes(int64_t n_rows, int64_t vocab) {
   if (n_rows <= 0 || n_rows > INT32_MAX || vocab < 2 || vocab > INT32_MAX) return 0;
@@ -2190,35 +2236,22 @@ cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, cons
                             void* const* row_events, void* stream) {
   if (row_events && (!row_events[0] || !row_events[1])) return CMSD_ERR_ARG;
   VerifyArgs a{};
-  const cmsd_status e = pass_setup(draft_logits, draft_stride, target_logits, target_stride, drafted, uniforms, dtype,
-                                   batch, k_max, vocab, conf, draft, verify, adaptive, draft_stats, draft_len,
-                                   target_stats, n_accepted, next_token, workspace, workspace_bytes,
-                                   cmsd_verify_workspace_bytes(batch, k_max, vocab), a);
+  cmsd_status e = pass_setup(draft_logits, draft_stride, target_logits, target_stride, drafted, uniforms, dtype,
+                             batch, k_max, vocab, conf, draft, verify, adaptive, draft_stats, draft_len, target_stats,
+                             n_accepted, next_token, a);
   if (e != CMSD_OK || batch == 0) return e;
-  const size_t es = dtype == CMSD_F32 ? 4 : 2;
-  const int64_t drows = (int64_t)batch * k_max, trows = (int64_t)batch * (k_max + 1);
-  const hipStream_t st = as_stream(stream);
-  const int S = verify_slices(vocab, (int)es);
-  const int SW = (S + kSubPerWG - 1) / kSubPerWG;
-  SlicePart* ws = static_cast<SlicePart*>(workspace);
-  const unsigned gp = (unsigned)((int64_t)batch * SW);
-  const int bd = row_block(drows + trows, vocab * (int64_t)es);
-  if (row_events && hipEventRecord(static_cast<hipEvent_t>(row_events[0]), st) != hipSuccess) return CMSD_ERR_LAUNCH;
-  if (dtype == CMSD_F32)
-    launch_row_pass<float>(bd, a, drows + trows, st);
-  else
-    launch_row_pass<Bf16>(bd, a, drows + trows, st);
-  if (row_events && hipEventRecord(static_cast<hipEvent_t>(row_events[1]), st) != hipSuccess) return CMSD_ERR_LAUNCH;
-  hipLaunchKernelGGL(k_pass_decide, dim3((unsigned)batch), dim3(64), 0, st, a);
-  if (a.mode == CMSD_MODE_GREEDY) return launched();  // the final token is the row's top token
-  if (dtype == CMSD_F32) {
-    hipLaunchKernelGGL((k_final_parts<float, true>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
-    hipLaunchKernelGGL((k_final_sample<float, true>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
-  } else {
-    hipLaunchKernelGGL((k_final_parts<Bf16, true>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
-    hipLaunchKernelGGL((k_final_sample<Bf16, true>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
-  }
-  return launched();
+  e = bind_pass_workspace(a, workspace, workspace_bytes, cmsd_verify_workspace_bytes(batch, k_max, vocab));
+  if (e != CMSD_OK) return e;
+  return enqueue_logit_pass(a, dtype, workspace, row_events ? static_cast<hipEvent_t>(row_events[0]) : nullptr,
+                            row_events ? static_cast<hipEvent_t>(row_events[1]) : nullptr, as_stream(stream));
+}
+
+cmsd_status cmsd_set_row_shape(int32_t threads, int32_t ring_depth) {
+  if (threads != 0 && threads != 64 && threads != 128 && threads != 256) return CMSD_ERR_ARG;
+  if (ring_depth != 0 && ring_depth != 2 && ring_depth != 3) return CMSD_ERR_ARG;
+  g_row_block.store(threads, std::memory_order_relaxed);
+  g_ring_depth.store(ring_depth, std::memory_order_relaxed);
+  return CMSD_OK;
 }
 
 size_t cmsd_logit_pass_fused_workspace_bytes(int32_t batch, int32_t k_max, int64_t vocab) {
@@ -2235,11 +2268,12 @@ cmsd_status cmsd_logit_pass_fused(const void* draft_logits, int64_t draft_stride
                                   int32_t* draft_len, cmsd_target_stats* target_stats, int32_t* n_accepted,
                                   int32_t* next_token, void* workspace, size_t workspace_bytes, void* stream) {
   VerifyArgs a{};
-  const cmsd_status e = pass_setup(draft_logits, draft_stride, target_logits, target_stride, drafted, uniforms, dtype,
-                                   batch, k_max, vocab, conf, draft, verify, adaptive, draft_stats, draft_len,
-                                   target_stats, n_accepted, next_token, workspace, workspace_bytes,
-                                   cmsd_logit_pass_fused_workspace_bytes(batch, k_max, vocab), a);
+  cmsd_status e = pass_setup(draft_logits, draft_stride, target_logits, target_stride, drafted, uniforms, dtype,
+                             batch, k_max, vocab, conf, draft, verify, adaptive, draft_stats, draft_len, target_stats,
+                             n_accepted, next_token, a);
   if (e != CMSD_OK || batch == 0) return e;
+  e = bind_pass_workspace(a, workspace, workspace_bytes, cmsd_logit_pass_fused_workspace_bytes(batch, k_max, vocab));
+  if (e != CMSD_OK) return e;
   const int es = dtype == CMSD_F32 ? 4 : 2;
   const int64_t rows = (int64_t)batch * (2 * k_max + 1);
   const int S = verify_slices(vocab, es);

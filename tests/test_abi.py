@@ -16,13 +16,26 @@ def test_exports_every_declared_symbol():
                          "cmsd_verify_workspace_bytes",
                          "cmsd_draft_sample", "cmsd_draft_sample_workspace_bytes", "cmsd_status_string",
                          "cmsd_version", "cmsd_logit_pass", "cmsd_logit_pass_fused",
-                         "cmsd_logit_pass_fused_workspace_bytes"}
+                         "cmsd_logit_pass_fused_workspace_bytes", "cmsd_set_row_shape"}
     lib = cm.lib()
     for s in syms:
         assert hasattr(lib, s), s
-    assert lib.cmsd_version() == (1 << 16) | 4
+    assert lib.cmsd_version() == (1 << 16) | 5
     assert lib.cmsd_status_string(0) == b"ok"
     assert lib.cmsd_status_string(1) == b"invalid argument"
+
+
+@pytest.mark.parametrize("threads,depth,want", [
+    (0, 0, cm.CMSD_OK), (64, 2, cm.CMSD_OK), (128, 3, cm.CMSD_OK), (256, 0, cm.CMSD_OK),
+    (32, 0, cm.CMSD_ERR_ARG), (512, 0, cm.CMSD_ERR_ARG), (-64, 0, cm.CMSD_ERR_ARG),
+    (0, 1, cm.CMSD_ERR_ARG), (0, 4, cm.CMSD_ERR_ARG), (64, -2, cm.CMSD_ERR_ARG),
+])
+def test_set_row_shape(threads, depth, want):
+    lib = cm.lib()
+    try:
+        assert lib.cmsd_set_row_shape(threads, depth) == want
+    finally:
+        assert lib.cmsd_set_row_shape(0, 0) == cm.CMSD_OK
 
 
 def _conf(**kw):
@@ -212,3 +225,4 @@ def test_logit_pass_fused_workspace():
     # exactly the verify workspace is one counter area too small
     assert _fpass(wsb=v(4, 8, 1024)) == cm.CMSD_ERR_ARG
     assert _fpass(wsb=f(4, 8, 1024) - 1) == cm.CMSD_ERR_ARG
+

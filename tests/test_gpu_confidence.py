@@ -66,9 +66,9 @@ def test_invariant_rows(cm, dtype, V, pad):
 @pytest.mark.parametrize("block", [64, 128, 256])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("V", [9, 1025, 50257])
-def test_each_row_block(cm, monkeypatch, block, dtype, V):
-    # every workgroup size the library may pick for a launch (forced by CMSD_ROW_BLOCK)
-    monkeypatch.setenv("CMSD_ROW_BLOCK", str(block))
+def test_each_row_block(cm, row_shape, block, dtype, V):
+    # every workgroup size the library may pick for a launch (forced by cmsd_set_row_shape)
+    row_shape(block)
     g = np.random.default_rng(V + block)
     stored = _store(_invariant_rows(V, g), dtype)
     tdev = Hn.to_device(stored, dtype, torch.device("cuda:0"))
@@ -82,13 +82,15 @@ def test_each_row_block(cm, monkeypatch, block, dtype, V):
     t.assert_ok()
 
 
+@pytest.mark.parametrize("depth", [2, 3])
 @pytest.mark.parametrize("block", [64, 128, 256])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_rounds_across_the_ring(cm, monkeypatch, block, dtype):
-    # a row streams in rounds of 32 elements per thread, two rounds in flight: rows of
-    # 1..9 full rounds (plus a partial round, a tail and an unaligned head) take the
-    # ring's main loop zero to three times and leave 2 or 3 rounds to its last part
-    monkeypatch.setenv("CMSD_ROW_BLOCK", str(block))
+def test_rounds_across_the_ring(cm, row_shape, block, dtype, depth):
+    # a row streams in rounds of 32 elements per thread with `depth` rounds of loads in
+    # flight: rows of 1..9 full rounds (plus a partial round, a tail and an unaligned
+    # head) take the ring's main loop zero or more times and leave depth..2*depth-1
+    # rounds (or the whole row) to its guarded last part
+    row_shape(block, depth)
     lam = (0.2, 0.5, 0.3)
     lam32 = tuple(Hn.f32(x) for x in lam)
     for nr in range(1, 10):
@@ -181,8 +183,8 @@ def test_logit_variance_rows(cm, dtype, V, pad):
 
 
 @pytest.mark.parametrize("block", [64, 128, 256])
-def test_logit_variance_each_row_block(cm, monkeypatch, block):
-    monkeypatch.setenv("CMSD_ROW_BLOCK", str(block))
+def test_logit_variance_each_row_block(cm, row_shape, block):
+    row_shape(block)
     g = np.random.default_rng(block)
     V = 20011
     stored = _store(_invariant_rows(V, g), "bf16")

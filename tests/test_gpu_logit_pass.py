@@ -159,12 +159,13 @@ def test_shapes(cm, dtype, V, K, B, pad):
         _run_case(cm, zd, zt, dr, u, B, K, V, dtype, mode=mode, adaptive=bool(mode == O.MODE_CM), pad=pad)
 
 
+@pytest.mark.parametrize("depth", [2, 3])
 @pytest.mark.parametrize("block", [64, 128, 256])
-def test_rounds_across_the_ring(cm, monkeypatch, block):
+def test_rounds_across_the_ring(cm, row_shape, block, depth):
     # drafter and target rows of 1..9 full 32-element-per-thread rounds (plus a partial
     # round and a tail), unaligned starts: every way through the streaming ring's main
-    # loop and its last rounds, for every workgroup size
-    monkeypatch.setenv("CMSD_ROW_BLOCK", str(block))
+    # loop and its last rounds, for every workgroup size and ring depth
+    row_shape(block, depth)
     for nr in (1, 2, 3, 4, 5, 6, 9):
         V = 32 * block * nr + 37
         g = np.random.default_rng(nr * 100 + block)
@@ -247,8 +248,8 @@ def test_empty_batch(cm):
 
 
 def test_row_events_time_the_row_pass(cm):
-    # events handed to the call bracket the row-pass kernel on the call's stream and
-    # leave the outputs unchanged
+    # events handed to the call are stamped with the row-pass kernel's start and end on
+    # the call's stream, and leave the outputs unchanged
     cfg = W.CONFIGS["c2"]
     d = Hn.workload("c2")
     ref, _ = _pass(cm, d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"], cfg.B, cfg.k_max, O.MODE_CM)

@@ -17,10 +17,10 @@ FIELDS = ("draft_stats", "draft_len", "target_stats", "n_accepted", "next_token"
 
 
 @pytest.fixture(autouse=True)
-def _row_block_256(monkeypatch):
+def _row_block_256(row_shape):
     # the fused pass runs its rows with 256 threads; the four-launch pass it is compared
     # with bit for bit must too, also when a run forces another size for every launch
-    monkeypatch.setenv("CMSD_ROW_BLOCK", "256")
+    row_shape(256)
 
 
 @pytest.fixture(scope="module")

@@ -167,9 +167,9 @@ def test_ragged_lengths_small_vocab(mods, dtype, V, mode):
 @pytest.mark.parametrize("block", [64, 128, 256])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY])
-def test_each_row_block(mods, monkeypatch, block, dtype, mode):
+def test_each_row_block(mods, row_shape, block, dtype, mode):
     # every workgroup size the library may pick for the target-row pass
-    monkeypatch.setenv("CMSD_ROW_BLOCK", str(block))
+    row_shape(block)
     g = np.random.default_rng(block + 7 * mode)
     B, K, V = 5, 4, 9001
     zd, zt_pad, drafted, unif_pad = _small_case(g, B, K, V, dtype)

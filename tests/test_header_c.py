@@ -23,7 +23,7 @@ int main(void) {
   cmsd_row_stats st;
   float x = 0.f;
   int32_t k = 0, off = 0;
-  if (cmsd_version() != ((1 << 16) | 4)) bad |= 1;
+  if (cmsd_version() != ((1 << 16) | 5)) bad |= 1;
   if (strcmp(cmsd_status_string(CMSD_OK), "ok") != 0) bad |= 2;
   if (cmsd_verify_workspace_bytes(0, 8, 1000) != 0) bad |= 4;
   if (cmsd_verify_workspace_bytes(4, 8, 1000) == 0) bad |= 8;
@@ -40,6 +40,7 @@ int main(void) {
   if (cmsd_logit_pass_fused_workspace_bytes(4, 8, 1000) != cmsd_verify_workspace_bytes(4, 8, 1000) + 16) bad |= 1024;
   if (cmsd_logit_pass_fused(&x, 100, &x, 100, &k, &x, 9, 1, 8, 100, &cp, &dp, &vp, 0, &st, &k, NULL, &k, &k, &x,
                             1 << 20, NULL) != CMSD_ERR_DTYPE) bad |= 2048;
+  if (cmsd_set_row_shape(48, 0) != CMSD_ERR_ARG || cmsd_set_row_shape(0, 0) != CMSD_OK) bad |= 16384;
   printf("bad=%d\n", bad);
   return bad;
 }
