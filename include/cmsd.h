@@ -21,7 +21,8 @@
  *   - All array pointers are DEVICE pointers (hipMalloc / torch CUDA tensors);
  *     params structs are HOST pointers read during the call.  The caller owns
  *     every buffer and the library allocates no memory.  Its only state is the
- *     row-kernel shape override of cmsd_set_row_shape.
+ *     row-kernel shape override of cmsd_set_row_shape and, per device, the static
+ *     scratch array of cmsd_logit_pass_noalloc.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Calls
  *     only enqueue work and return; results are ready when the stream is.
  *   - Argument errors are detected on the host before anything is enqueued and
@@ -53,8 +54,15 @@ typedef enum {
   CMSD_OK = 0,
   CMSD_ERR_ARG = 1,    /* invalid size, pointer or parameter            */
   CMSD_ERR_DTYPE = 2,  /* unknown logit dtype                            */
-  CMSD_ERR_LAUNCH = 3  /* the HIP runtime refused a launch               */
+  CMSD_ERR_LAUNCH = 3, /* the HIP runtime refused a launch               */
+  CMSD_ERR_SIZE = 4    /* the problem exceeds CMSD_STATIC_SCRATCH_BYTES
+                          (cmsd_logit_pass_noalloc only)                  */
 } cmsd_status;
+
+/* Size of the static per-device scratch array that cmsd_logit_pass_noalloc uses in
+ * place of a caller workspace: 16 MiB, i.e. cmsd_verify_workspace_bytes(batch,
+ * k_max, vocab) up to 16 MiB (e.g. batch 1024 at k_max 16, vocab 128256). */
+#define CMSD_STATIC_SCRATCH_BYTES (16u << 20)
 
 typedef enum { CMSD_F32 = 0, CMSD_BF16 = 1 } cmsd_dtype;
 
@@ -331,9 +339,38 @@ cmsd_status cmsd_logit_pass_fused(const void* draft_logits, int64_t draft_stride
 size_t cmsd_logit_pass_fused_workspace_bytes(int32_t batch, int32_t k_max, int64_t vocab);
 
 /*
+ * cmsd_logit_pass_noalloc - cmsd_logit_pass without a caller workspace, for callers
+ * that cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  It calls no hipMalloc or hipFree and no
+ * allocating routine.  Its workspace is a static array of CMSD_STATIC_SCRATCH_BYTES
+ * in the library, one per device, held from the first call on that device until the
+ * process ends; its device address is looked up once per device (with that device
+ * current) and kept.
+ *
+ * Arguments, outputs and results are those of cmsd_logit_pass without workspace,
+ * workspace_bytes and row_events: the same kernels on the same workgroup sizes, so
+ * the outputs are bit-identical to cmsd_logit_pass's.  Nothing in the scratch needs
+ * to start at zero; it keeps the last call's contents.
+ * Limits and errors: as cmsd_logit_pass, plus CMSD_ERR_SIZE (nothing enqueued) when
+ * cmsd_verify_workspace_bytes(batch, k_max, vocab) > CMSD_STATIC_SCRATCH_BYTES, and
+ * CMSD_ERR_LAUNCH if the scratch address cannot be obtained.
+ * Every call on one device shares that device's scratch: calls that can overlap on
+ * one GPU (concurrent streams, several host threads) race and give wrong results;
+ * order them on one stream.
+ */
+cmsd_status cmsd_logit_pass_noalloc(const void* draft_logits, int64_t draft_stride, const void* target_logits,
+                                    int64_t target_stride, const int32_t* drafted, const float* uniforms,
+                                    int32_t dtype, int32_t batch, int32_t k_max, int64_t vocab,
+                                    const cmsd_conf_params* conf, const cmsd_draft_params* draft,
+                                    const cmsd_verify_params* verify, int32_t adaptive,
+                                    cmsd_row_stats* draft_stats, int32_t* draft_len,
+                                    cmsd_target_stats* target_stats, int32_t* n_accepted,
+                                    int32_t* next_token, void* stream);
+
+/*
  * cmsd_set_row_shape - launch shape of the streaming row kernels (one workgroup per
  * logit row: cmsd_confidence, cmsd_confidence_var, cmsd_verify's target rows, the row
- * pass of cmsd_logit_pass), for tuning and for tests that
+ * pass of cmsd_logit_pass / cmsd_logit_pass_noalloc), for tuning and for tests that
  * cover every shape.  Process-wide; applies to launches made after it returns.
  *   threads     0 (chosen per launch from its rows and row length), 64, 128 or 256.
  *   ring_depth  0 (chosen per launch), 2 or 3: rounds of 16-byte loads kept in flight
@@ -377,7 +414,8 @@ size_t cmsd_draft_sample_workspace_bytes(int64_t n_rows, int64_t vocab);
 /* Human-readable name of a status code (static string). */
 const char* cmsd_status_string(cmsd_status s);
 
-/* Library ABI version, (major << 16) | minor: 1.5 (1.4 plus cmsd_set_row_shape). */
+/* Library ABI version, (major << 16) | minor: 1.5 (1.4 plus cmsd_logit_pass_noalloc,
+ * cmsd_set_row_shape and CMSD_ERR_SIZE). */
 int32_t cmsd_version(void);
 
 #ifdef __cplusplus

@@ -18,7 +18,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libcmsd.so")
 HEADER = os.path.join(os.path.dirname(_HERE), "include", "cmsd.h")
 
-CMSD_OK, CMSD_ERR_ARG, CMSD_ERR_DTYPE, CMSD_ERR_LAUNCH = 0, 1, 2, 3
+CMSD_OK, CMSD_ERR_ARG, CMSD_ERR_DTYPE, CMSD_ERR_LAUNCH, CMSD_ERR_SIZE = 0, 1, 2, 3, 4
+CMSD_STATIC_SCRATCH_BYTES = 16 << 20     # include/cmsd.h
 CMSD_F32, CMSD_BF16 = 0, 1
 CMSD_MODE_STANDARD, CMSD_MODE_CM, CMSD_MODE_GREEDY = 0, 1, 2
 
@@ -73,6 +74,10 @@ def _load() -> C.CDLL:
                                           C.POINTER(DraftParams), C.POINTER(VerifyParams), i32, vp, vp, vp, vp, vp,
                                           vp, C.c_size_t, vp]
     lib.cmsd_logit_pass_fused.restype = C.c_int
+    lib.cmsd_logit_pass_noalloc.argtypes = [vp, i64, vp, i64, vp, vp, i32, i32, i32, i64, C.POINTER(ConfParams),
+                                            C.POINTER(DraftParams), C.POINTER(VerifyParams), i32, vp, vp, vp, vp,
+                                            vp, vp]
+    lib.cmsd_logit_pass_noalloc.restype = C.c_int
     lib.cmsd_set_row_shape.argtypes = [i32, i32]
     lib.cmsd_set_row_shape.restype = C.c_int
     lib.cmsd_logit_pass_fused_workspace_bytes.argtypes = [i32, i32, i64]
@@ -314,6 +319,9 @@ def cmsd_draft_sample(logits: torch.Tensor, stats: torch.Tensor, uniforms: torch
     return drafted
 
 
+_NO_WORKSPACE = object()     # marker: the call takes no workspace (cmsd_logit_pass_noalloc)
+
+
 def _pass_args(draft_logits, target_logits, drafted, uniforms, batch, k_max, lambdas, beta_margin, k_min, alpha,
                mode, top_beta, tau_base, gamma, outs, workspace, make_workspace):
     """Checks and completes the arguments of the single-call passes."""
@@ -346,9 +354,12 @@ def _pass_args(draft_logits, target_logits, drafted, uniforms, batch, k_max, lam
         if t is None and name == "uniforms":
             continue
         _buf(t, name, dt, n, dev)
-    if workspace is None:
+    if workspace is _NO_WORKSPACE:
+        pass
+    elif workspace is None:
         workspace = make_workspace(batch, k_max, V, dev)
-    if workspace.dtype != torch.float64 or not workspace.is_contiguous() or workspace.device != dev:
+    if workspace is not _NO_WORKSPACE and (workspace.dtype != torch.float64 or not workspace.is_contiguous()
+                                           or workspace.device != dev):
         raise ValueError(f"workspace must be a contiguous float64 tensor on {dev}")
     out["workspace"] = workspace
     cp = ConfParams(float(lambdas[0]), float(lambdas[1]), float(lambdas[2]), float(beta_margin))
@@ -412,3 +423,26 @@ def cmsd_logit_pass_fused(draft_logits: torch.Tensor, target_logits: torch.Tenso
         ws.numel() * ws.element_size(), _stream(stream)))
     return out
 
+
+def cmsd_logit_pass_noalloc(draft_logits: torch.Tensor, target_logits: torch.Tensor, drafted: torch.Tensor,
+                            uniforms: torch.Tensor | None, *, batch: int, k_max: int, lambdas=(1 / 3, 1 / 3, 1 / 3),
+                            beta_margin: float = 1.0, k_min: int = 1, alpha: float = 1.0, mode: int = CMSD_MODE_CM,
+                            top_beta: int = 3, tau_base: float = 0.1, gamma: float = 1.0, adaptive: bool = False,
+                            draft_stats: torch.Tensor | None = None, draft_len: torch.Tensor | None = None,
+                            target_stats: torch.Tensor | None = None, n_accepted: torch.Tensor | None = None,
+                            next_token: torch.Tensor | None = None, stream=None) -> dict:
+    """cmsd_logit_pass on the library's static scratch instead of a workspace (the
+    call allocates no device memory; pass preallocated outputs to allocate nothing
+    here either).  Same arguments and outputs, without ``workspace``/``row_events``."""
+    outs = {"draft_stats": draft_stats, "draft_len": draft_len, "target_stats": target_stats,
+            "n_accepted": n_accepted, "next_token": next_token}
+    out, dst, tst, V, cp, dp, vp_ = _pass_args(draft_logits, target_logits, drafted, uniforms, batch, k_max, lambdas,
+                                               beta_margin, k_min, alpha, mode, top_beta, tau_base, gamma, outs,
+                                               _NO_WORKSPACE, None)
+    del out["workspace"]
+    _check("cmsd_logit_pass_noalloc", _lib.cmsd_logit_pass_noalloc(
+        _ptr(draft_logits), dst, _ptr(target_logits), tst, _ptr(drafted), _ptr(uniforms),
+        _dtype_code(target_logits), int(batch), int(k_max), V, C.byref(cp), C.byref(dp), C.byref(vp_),
+        1 if adaptive else 0, _ptr(out["draft_stats"]), _ptr(out["draft_len"]), _ptr(out["target_stats"]),
+        _ptr(out["n_accepted"]), _ptr(out["next_token"]), _stream(stream)))
+    return out

@@ -47,6 +47,7 @@
 #include <stdlib.h>
 
 #include <atomic>
+#include <mutex>
 
 #include "cmsd.h"
 
@@ -2076,6 +2077,38 @@ cmsd_status enqueue_logit_pass(const VerifyArgs& a, int32_t dtype, void* workspa
   return launched();
 }
 
+// ----------------------------------------------------------------------------- static scratch
+// The workspace of cmsd_logit_pass_noalloc: one array per device, held from the
+// library's first use on that device until the process ends.  Host code never passes
+// the array's name to a kernel (on the host it names a stand-in, not device memory):
+// its device address is looked up once per device with hipGetSymbolAddress, with that
+// device current, and kept.  Every no-allocation call on a device shares its array.
+static __device__ __align__(256) unsigned char scratch[CMSD_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// Device address of the current device's scratch array; nullptr on a HIP error.
+void* scratch_ptr() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  void* p = g_scratch[dev].load(std::memory_order_acquire);
+  if (p) return p;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  p = g_scratch[dev].load(std::memory_order_relaxed);
+  if (!p) {
+    void* q = nullptr;
+    if (hipGetSymbolAddress(&q, HIP_SYMBOL(scratch)) != hipSuccess || !q) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    p = q;
+    g_scratch[dev].store(p, std::memory_order_release);
+  }
+  return p;
+}
+
 }  // namespace
 
 // ----------------------------------------------------------------------------- C ABI
@@ -2087,6 +2120,7 @@ const char* cmsd_status_string(cmsd_status s) {
     case CMSD_ERR_ARG: return "invalid argument";
     case CMSD_ERR_DTYPE: return "unknown logit dtype";
     case CMSD_ERR_LAUNCH: return "kernel launch failed";
+    case CMSD_ERR_SIZE: return "problem larger than the static scratch";
   }
   return "unknown status";
 }
@@ -2244,6 +2278,27 @@ cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, cons
   if (e != CMSD_OK) return e;
   return enqueue_logit_pass(a, dtype, workspace, row_events ? static_cast<hipEvent_t>(row_events[0]) : nullptr,
                             row_events ? static_cast<hipEvent_t>(row_events[1]) : nullptr, as_stream(stream));
+}
+
+cmsd_status cmsd_logit_pass_noalloc(const void* draft_logits, int64_t draft_stride, const void* target_logits,
+                                    int64_t target_stride, const int32_t* drafted, const float* uniforms,
+                                    int32_t dtype, int32_t batch, int32_t k_max, int64_t vocab,
+                                    const cmsd_conf_params* conf, const cmsd_draft_params* draft,
+                                    const cmsd_verify_params* verify, int32_t adaptive, cmsd_row_stats* draft_stats,
+                                    int32_t* draft_len, cmsd_target_stats* target_stats, int32_t* n_accepted,
+                                    int32_t* next_token, void* stream) {
+  VerifyArgs a{};
+  cmsd_status e = pass_setup(draft_logits, draft_stride, target_logits, target_stride, drafted, uniforms, dtype,
+                             batch, k_max, vocab, conf, draft, verify, adaptive, draft_stats, draft_len, target_stats,
+                             n_accepted, next_token, a);
+  if (e != CMSD_OK || batch == 0) return e;
+  const size_t need = cmsd_verify_workspace_bytes(batch, k_max, vocab);
+  if (need > (size_t)CMSD_STATIC_SCRATCH_BYTES) return CMSD_ERR_SIZE;
+  void* ws = scratch_ptr();
+  if (!ws) return CMSD_ERR_LAUNCH;
+  e = bind_pass_workspace(a, ws, (size_t)CMSD_STATIC_SCRATCH_BYTES, need);
+  if (e != CMSD_OK) return e;
+  return enqueue_logit_pass(a, dtype, ws, nullptr, nullptr, as_stream(stream));
 }
 
 cmsd_status cmsd_set_row_shape(int32_t threads, int32_t ring_depth) {

@@ -16,13 +16,23 @@ def test_exports_every_declared_symbol():
                          "cmsd_verify_workspace_bytes",
                          "cmsd_draft_sample", "cmsd_draft_sample_workspace_bytes", "cmsd_status_string",
                          "cmsd_version", "cmsd_logit_pass", "cmsd_logit_pass_fused",
-                         "cmsd_logit_pass_fused_workspace_bytes", "cmsd_set_row_shape"}
+                         "cmsd_logit_pass_fused_workspace_bytes", "cmsd_logit_pass_noalloc",
+                         "cmsd_set_row_shape"}
     lib = cm.lib()
     for s in syms:
         assert hasattr(lib, s), s
     assert lib.cmsd_version() == (1 << 16) | 5
     assert lib.cmsd_status_string(0) == b"ok"
     assert lib.cmsd_status_string(1) == b"invalid argument"
+    assert lib.cmsd_status_string(4) == b"problem larger than the static scratch"
+
+
+def test_header_constants_match_binding():
+    import re
+    txt = open(cm.HEADER).read()
+    assert re.search(r"#define CMSD_STATIC_SCRATCH_BYTES \(16u << 20\)", txt)
+    assert cm.CMSD_STATIC_SCRATCH_BYTES == 16 << 20
+    assert re.search(r"CMSD_ERR_SIZE = 4", txt) and cm.CMSD_ERR_SIZE == 4
 
 
 @pytest.mark.parametrize("threads,depth,want", [
@@ -226,3 +236,46 @@ def test_logit_pass_fused_workspace():
     assert _fpass(wsb=v(4, 8, 1024)) == cm.CMSD_ERR_ARG
     assert _fpass(wsb=f(4, 8, 1024) - 1) == cm.CMSD_ERR_ARG
 
+
+def _npass(**kw):
+    a = dict(dl=P, ds=1024, tl=P, ts=1024, dr=P, u=P, dtype=cm.CMSD_BF16, B=4, K=8, V=1024,
+             cp=cm.ConfParams(0.25, 0.25, 0.5, 1.0), dp=cm.DraftParams(1, 8, 1.0), vp=cm.VerifyParams(1, 3, 0.1, 1.0),
+             ad=0, dst=P, kl=P, tst=P, na=P, nt=P)
+    a.update(kw)
+    ref = lambda x: C.byref(x) if x is not None else None  # noqa: E731
+    return cm.lib().cmsd_logit_pass_noalloc(a["dl"], a["ds"], a["tl"], a["ts"], a["dr"], a["u"], a["dtype"], a["B"],
+                                            a["K"], a["V"], ref(a["cp"]), ref(a["dp"]), ref(a["vp"]), a["ad"],
+                                            a["dst"], a["kl"], a["tst"], a["na"], a["nt"], None)
+
+
+# every case returns before any HIP call (argument checks, then the scratch bound)
+@pytest.mark.parametrize("kw,want", [
+    (dict(dtype=3), cm.CMSD_ERR_DTYPE),
+    (dict(cp=None), cm.CMSD_ERR_ARG),
+    (dict(dp=cm.DraftParams(1, 7, 1.0)), cm.CMSD_ERR_ARG),
+    (dict(K=64, dp=cm.DraftParams(1, 64, 1.0)), cm.CMSD_ERR_ARG),
+    (dict(V=1), cm.CMSD_ERR_ARG),
+    (dict(u=None), cm.CMSD_ERR_ARG),
+    (dict(nt=None), cm.CMSD_ERR_ARG),
+    (dict(tl=P + 1), cm.CMSD_ERR_ARG),
+    (dict(ad=2), cm.CMSD_ERR_ARG),
+    (dict(B=-1), cm.CMSD_ERR_ARG),
+    (dict(B=0, dl=None, tl=None, dr=None), cm.CMSD_OK),
+    # larger than the 16 MiB static scratch: rejected, nothing enqueued
+    (dict(B=4096, K=16, V=128256, ds=128256, ts=128256, dp=cm.DraftParams(1, 16, 1.0)), cm.CMSD_ERR_SIZE),
+    (dict(B=1, K=1, V=2**31 - 1, ds=2**31 - 1, ts=2**31 - 1, dp=cm.DraftParams(1, 1, 1.0)), cm.CMSD_ERR_SIZE),
+])
+def test_logit_pass_noalloc_argument_errors(kw, want):
+    assert _npass(**kw) == want
+
+
+def test_noalloc_scratch_bound_is_the_verify_workspace():
+    # the bound is exactly cmsd_verify_workspace_bytes <= CMSD_STATIC_SCRATCH_BYTES:
+    # per sequence at V = 128256, k_max = 16: 126 slice records + 17 row slots of 32 B
+    v = cm.lib().cmsd_verify_workspace_bytes
+    per = v(1, 16, 128256)
+    assert per == 32 * (126 + 17)
+    fit = (16 << 20) // per
+    assert v(fit, 16, 128256) <= 16 << 20 < v(fit + 1, 16, 128256)
+    big = dict(K=16, V=128256, ds=128256, ts=128256, dp=cm.DraftParams(1, 16, 1.0))
+    assert _npass(B=fit + 1, **big) == cm.CMSD_ERR_SIZE

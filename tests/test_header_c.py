@@ -40,6 +40,13 @@ int main(void) {
   if (cmsd_logit_pass_fused_workspace_bytes(4, 8, 1000) != cmsd_verify_workspace_bytes(4, 8, 1000) + 16) bad |= 1024;
   if (cmsd_logit_pass_fused(&x, 100, &x, 100, &k, &x, 9, 1, 8, 100, &cp, &dp, &vp, 0, &st, &k, NULL, &k, &k, &x,
                             1 << 20, NULL) != CMSD_ERR_DTYPE) bad |= 2048;
+  /* the no-allocation pass: its scratch bound is checked on the host */
+  dp.k_min = 1;
+  dp.k_max = 16;
+  vp.mode = CMSD_MODE_CM;
+  if (cmsd_logit_pass_noalloc(&x, 128256, &x, 128256, &k, &x, CMSD_BF16, 4096, 16, 128256, &cp, &dp, &vp, 0, &st,
+                              &k, NULL, &k, &k, NULL) != CMSD_ERR_ARG) bad |= 4096;  /* target_stats NULL */
+  if (cmsd_verify_workspace_bytes(4096, 16, 128256) <= CMSD_STATIC_SCRATCH_BYTES) bad |= 8192;
   if (cmsd_set_row_shape(48, 0) != CMSD_ERR_ARG || cmsd_set_row_shape(0, 0) != CMSD_OK) bad |= 16384;
   printf("bad=%d\n", bad);
   return bad;
