@@ -1,0 +1,107 @@
+"""Whole-batch GPU parity on the two largest workloads: every sequence of c4 (256) and
+c5 (512) in every mode, through the three calls (cmsd_confidence, cmsd_draft_len,
+cmsd_verify) and through cmsd_logit_pass in both verification lengths, against the
+oracle.  Every drafter row's record, every draft length (end to end, with its floor
+slack), every target-row record, accept decision, prefix and final token is compared
+(Sec. III.A, III.B(1)-(c)); the oracle's work runs on the host's cores in forked
+worker processes (tests/fullbatch.py)."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import cmsd_oracle as O
+from tests import fullbatch as FB
+from tests import harness as Hn
+
+pytestmark = pytest.mark.gpu
+
+MODES = [O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY]
+
+
+@pytest.fixture(scope="module")
+def mods():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2508_15371_amd import cmsd, pipeline
+    return cmsd, pipeline
+
+
+def _params(pipeline, mode):
+    P = Hn.PARAMS
+    return pipeline.Params(lambdas=P["lambdas"], beta_margin=P["beta_margin"], k_min=P["k_min"], alpha=P["alpha"],
+                           mode=mode, top_beta=P["top_beta"], tau_base=P["tau_base"], gamma=P["gamma"])
+
+
+def _report(name, path, mode, t, n_acc, k, seqs):
+    nf = getattr(t, "n_failures", len(t.failures))
+    print(f"[full batch] {name} {path} mode={mode}: sequences={seqs} checked={t.checked} "
+          f"exceptions={t.exceptions} failures={nf} mean n_acc={n_acc.mean():.3f} mean k={k.mean():.3f}",
+          flush=True)
+    assert nf == 0, f"{nf} failures (of {t.checked}); first: {t.failures[:5]}"
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("name", ["c4", "c5"])
+def test_full_batch_three_calls(mods, name, mode):
+    cmsd, pipeline = mods
+    print(f"[full batch] start {name} three calls mode={mode}", flush=True)
+    cfg = W.CONFIGS[name]
+    d = Hn.workload(name)
+    lp = pipeline.LogitPass(cfg.B, cfg.k_max, cfg.V, "cuda:0", _params(pipeline, mode), dense=not cfg.ragged)
+    lp.confidence(d["draft_dev"])
+    lp.draft_len()
+    if cfg.ragged:
+        target = W.pack_device(d["target_dev"], lp.k, lp.off, cfg.k_max)
+        unif = W.pack_device(d["unif_dev"], lp.k, lp.off, cfg.k_max)
+    else:
+        target, unif = d["target_dev"], d["unif_dev"]
+    lp.verify(d["draft_dev"], target, d["drafted_dev"], unif)
+    torch.cuda.synchronize()
+    gs = Hn.stats_np(lp.stats)
+    k = lp.k.cpu().numpy()
+    off = lp.off.cpu().numpy()
+    n_acc = lp.n_acc.cpu().numpy()
+    nxt = lp.next_tok.cpu().numpy()
+    K = cfg.k_max
+    # offsets: the exclusive scan of k_b + 1, exactly
+    want_off = np.concatenate([[0], np.cumsum(k.astype(np.int64) + 1)])
+    assert np.array_equal(off, want_off), "offsets"
+    # draft lengths from the GPU's confidences (stage isolation): bit-exact
+    k_st, _, _ = O.draft_len(gs["C"].astype(np.float64).reshape(cfg.B, K), Hn.PARAMS["k_min"], K,
+                             Hn.f32(Hn.PARAMS["alpha"]))
+    assert np.array_equal(k_st, k), "draft lengths from the GPU's confidences"
+    FB.set_job(cfg=cfg, draft=d["draft"], target=d["target"], drafted=d["drafted"], uniforms=d["uniforms"], gs=gs,
+               ts=Hn.tstats_np(lp.tstats), k=k, n_acc=n_acc, next=nxt,
+               off=off if cfg.ragged else np.arange(cfg.B + 1) * (K + 1), packed=cfg.ragged,
+               verify_len="k_b" if cfg.ragged else "k_max", mode=mode, params=Hn.PARAMS)
+    t = FB.check_batch()
+    _report(name, "three calls", mode, t, n_acc, k, cfg.B)
+
+
+@pytest.mark.parametrize("adaptive", [False, True])
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("name", ["c4", "c5"])
+def test_full_batch_logit_pass(mods, name, mode, adaptive):
+    cmsd, _ = mods
+    print(f"[full batch] start {name} cmsd_logit_pass mode={mode} adaptive={adaptive}", flush=True)
+    cfg = W.CONFIGS[name]
+    d = Hn.workload(name)
+    P = Hn.PARAMS
+    out = cmsd.cmsd_logit_pass(d["draft_dev"], d["target_dev"], d["drafted_dev"],
+                               None if mode == O.MODE_GREEDY else d["unif_dev"], batch=cfg.B, k_max=cfg.k_max,
+                               mode=mode, adaptive=adaptive, **P)
+    torch.cuda.synchronize()
+    K = cfg.k_max
+    gs = Hn.stats_np(out["draft_stats"])
+    k = out["draft_len"].cpu().numpy()
+    n_acc = out["n_accepted"].cpu().numpy()
+    nxt = out["next_token"].cpu().numpy()
+    k_st, _, _ = O.draft_len(gs["C"].astype(np.float64).reshape(cfg.B, K), P["k_min"], K, Hn.f32(P["alpha"]))
+    assert np.array_equal(k_st, k), "draft lengths from the GPU's confidences"
+    FB.set_job(cfg=cfg, draft=d["draft"], target=d["target"], drafted=d["drafted"], uniforms=d["uniforms"], gs=gs,
+               ts=Hn.tstats_np(out["target_stats"]), k=k, n_acc=n_acc, next=nxt,
+               off=np.arange(cfg.B + 1) * (K + 1), packed=False, verify_len="k_b" if adaptive else "k_max",
+               mode=mode, params=P)
+    t = FB.check_batch()
+    _report(name, f"cmsd_logit_pass {'adaptive' if adaptive else 'dense'}", mode, t, n_acc, k, cfg.B)

@@ -404,3 +404,73 @@ def test_graph_capture_replays_match_eager(mods):
         for a, b in zip(got, want):
             assert torch.equal(a.view(torch.int32) if a.dtype == torch.float32 else a,
                                b.view(torch.int32) if b.dtype == torch.float32 else b), rep
+
+
+@pytest.mark.parametrize("conf_block", [64, 256])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("V", [4, 3001, 50257])
+def test_zero_residual_falls_back_to_target_row(mods, row_shape, conf_block, dtype, V):
+    # Drafter and target rows equal at every drafted position; sequence b's draft at
+    # position c_b = b % K is a token both rows mask (-inf), rejected with certainty,
+    # and the residual of two equal rows is identically zero: the final token is
+    # sampled from p_t of row c_b (reading R13).  The earlier drafts are the rows' top
+    # tokens (always accepted: p_t = p_d).  The drafter stats come from a launch of
+    # another workgroup size than the target rows' (conf_block 64), so their
+    # normalisers may differ in the last bits: the final-token pass then meets a slice
+    # mass of rounding size whose exact weights are all zero, the second way to the
+    # fallback; with equal sizes the slice masses are exactly zero.
+    cmsd, _ = mods
+    g = np.random.default_rng(V * 3 + conf_block + (dtype == "bf16"))
+    B, K = 6, 4
+    store = (lambda x: x.astype(np.float32)) if dtype == "f32" else W.bf16_bits_from_f32
+    zd = store(g.normal(0, 2.0, (B * K, V)))
+    drafted = np.zeros((B, K), dtype=np.int32)
+    cs = []
+    for b in range(B):
+        c = b % (K + 1)            # c = K: nothing masked, every draft accepted, bonus row
+        cs.append(c)
+        for i in range(K):
+            r = b * K + i
+            z = Hn.decode(zd[r], dtype)
+            if i == c:
+                y = int(g.integers(0, V))
+                while y == int(np.argmax(z)):
+                    y = int(g.integers(0, V))
+                zd[r, y] = 0xFF80 if dtype == "bf16" else -np.inf     # -inf in the stored dtype
+                drafted[b, i] = y
+            else:
+                drafted[b, i] = int(np.argmax(z))
+    zt = np.empty((B * (K + 1), V), dtype=zd.dtype)
+    for b in range(B):
+        zt[b * (K + 1):b * (K + 1) + K] = zd[b * K:(b + 1) * K]
+        zt[b * (K + 1) + K] = store(g.normal(0, 2.0, V))
+    unif = (g.integers(0, 1 << 24, (B, K + 1)) * 2.0 ** -24).astype(np.float32)
+    dev = torch.device("cuda:0")
+    dd, td = Hn.to_device(zd, dtype, dev), Hn.to_device(zt, dtype, dev)
+    dr = torch.from_numpy(drafted.reshape(-1)).to(dev)
+    ud = torch.from_numpy(unif.reshape(-1)).to(dev)
+    off = torch.from_numpy((np.arange(B + 1) * (K + 1)).astype(np.int32)).to(dev)
+    kd = torch.full((B,), K, dtype=torch.int32, device=dev)
+    for mode in (O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY):
+        row_shape(conf_block)
+        st = cmsd.cmsd_confidence(dd)
+        row_shape(256)
+        n_acc, nxt, ts = cmsd.cmsd_verify(dd, st, td, off, kd, dr, ud, batch=B, k_max=K, mode=mode)
+        lp = cmsd.cmsd_logit_pass(dd, td, dr, ud, batch=B, k_max=K, mode=mode, **Hn.PARAMS)
+        torch.cuda.synchronize()
+        t = Hn.Tally()
+        for outs in ((n_acc.cpu().numpy(), nxt.cpu().numpy(), Hn.tstats_np(ts)),
+                     (lp["n_accepted"].cpu().numpy(), lp["next_token"].cpu().numpy(),
+                      Hn.tstats_np(lp["target_stats"]))):
+            na, nx, tsn = outs
+            assert na.tolist() == cs, (mode, na.tolist(), cs)
+            for b in range(B):
+                zdr = [Hn.decode(zd[b * K + i], dtype) for i in range(K)]
+                ztr = [Hn.decode(zt[b * (K + 1) + i], dtype) for i in range(K + 1)]
+                C = [Hn.oracle_conf(z, V) for z in zdr]
+                Hn.check_sequence(t, b, ztr, zdr, drafted[b], unif[b], C, K, mode, Hn.PARAMS, tsn, b * (K + 1),
+                                  int(na[b]), int(nx[b]))
+                if cs[b] < K and mode != O.MODE_GREEDY:
+                    # the final token carries mass in the rejecting row
+                    assert ztr[cs[b]][int(nx[b])] > -np.inf
+        t.assert_ok()

@@ -43,6 +43,9 @@ MUTATIONS = [
      "residual with the target's normaliser on the drafter row"),
     ("return int(np.argmax(z_t_rows[min(n_acc, k_b)]))", "return int(np.argmax(z_t_rows[k_b]))",
      "GREEDY final token from the bonus row after a rejection"),
+    ("    if not np.any(q > 0):\n        return p_t\n", "", "no fallback for a zero residual"),
+    ("    if not np.any(q > 0):\n        return p_t\n", "    if not np.any(q > 0):\n        return np.ones_like(p_t)\n",
+     "uniform fallback for a zero residual"),
 ]
 
 

@@ -256,6 +256,36 @@ def test_final_sample_uses_rejection_row_or_bonus_row():
     assert res["n_acc"] == 2 and res["next"] == 5
 
 
+def test_zero_residual_falls_back_to_the_rejecting_rows_target():
+    # Drafter and target rows are equal at both positions, and the draft at position 1
+    # is a token that both rows mask (z = -inf): p_t(y) = 0 rejects it with certainty,
+    # and the residual max(0, p_t - p_d) of two equal rows is identically zero, so the
+    # final token comes from the fallback, p_t of that same row (reading R13).
+    #   row 1 = [0, ln 2, -inf, 0]: p = [1/4, 1/2, 0, 1/4], CDF = [1/4, 3/4, 3/4, 1]
+    #   inverse CDF (smallest y with CDF(y) > u): u = 0.1 -> 0, u = 0.5 -> 1,
+    #   u = 0.8 -> 3 (the masked token 2 adds no mass and is never returned).
+    # The bonus row [ln 8, 0, 0, 0] (p = [8, 1, 1, 1]/11, CDF 8/11, 9/11, 10/11, 1)
+    # would give 0, 0 and 1 instead, and a uniform fallback 0, 2 and 3.
+    r0 = np.array([0.0, 1.0, -0.5, 0.25])
+    r1 = np.array([0.0, math.log(2.0), -math.inf, 0.0])
+    bonus = np.array([math.log(8.0), 0.0, 0.0, 0.0])
+    zd = [r0, r1]
+    zt = [r0.copy(), r1.copy(), bonus]
+    ys = [1, 2]            # position 0: equal rows, accepted for any u < 1; position 1: masked
+    rs1 = O.row_stats(r1)
+    q = O.residual_pmf(r1, rs1, r1, rs1)
+    assert np.all(np.abs(q - np.array([0.25, 0.5, 0.0, 0.25])) <= 1e-15)
+    for mode in (O.MODE_STANDARD, O.MODE_CM):
+        for u, want in ((0.1, 0), (0.5, 1), (0.8, 3)):
+            res = O.verify_sequence(zt, zd, ys, [0.3, 0.3, u], [0.9, 0.9], 2, mode, 3, 0.1, 1.0)
+            assert res["flags"] == [True, False]
+            assert res["n_acc"] == 1
+            assert res["next"] == want, (mode, u, res["next"])
+    # GREEDY takes the top token of the rejecting row instead of sampling: index 1
+    res = O.verify_sequence(zt, zd, ys, [0.3, 0.3, 0.8], [0.9, 0.9], 2, O.MODE_GREEDY, 3, 0.1, 1.0)
+    assert res["n_acc"] == 1 and res["next"] == 1
+
+
 # ----------------------------------------------------------------------------- GREEDY mode
 @pytest.mark.parametrize("seed", range(12))
 def test_greedy_exact_match_reduction(seed):
