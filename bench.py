@@ -17,7 +17,7 @@ kernel's rows in its grid shape (``read_ceiling``: what one launch of those byte
 reach) and, with ``--extras``, the drafting sampler and the logit-variance pass; the CPU
 oracle runs last on the host.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4|c5|c3|c2|v152k|tiny|b1]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4|c5|c5m|c3|c2|v152k|tiny|b1]
                   [--mode cm|standard] [--path auto|pass|fused|calls] [--streams G] [--event-every N]
                   [--capacity-rows] [--no-rotate] [--extras] [--no-read-ceiling] [--no-cpu-baseline]
                   [--copy-probe MIB]
@@ -214,7 +214,7 @@ def main() -> int:
     # ~3 % slower), so the default warms up for 100 steps and times 500 (~0.2 s on c4)
     ap.add_argument("--steps", type=int, default=500)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--workload", default="c4", choices=["tiny", "b1", "c2", "c3", "c4", "c5", "v152k"])
+    ap.add_argument("--workload", default="c4", choices=["tiny", "b1", "c2", "c3", "c4", "c5", "c5m", "v152k"])
     ap.add_argument("--mode", default="cm", choices=["cm", "standard"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--path", default="auto", choices=["auto", "pass", "fused", "calls"],

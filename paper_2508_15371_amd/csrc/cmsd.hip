@@ -55,7 +55,13 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr double kLn2 = 0.69314718055994530942;
-constexpr float kNegBig = -3.0e38f;  // finite "minus infinity" for the scaled running max
+// Finite "minus infinity" for the scaled running max, and the finite value a drafter
+// row's -inf logits are clamped to before their normaliser and entropy terms: its
+// scaled value (kMaskedLogit*log2e) lies below kNegBig, so a chunk of masked logits
+// never raises the running max, and z*log2e - ms stays finite for every logit with
+// |z| < 2^96, so a masked logit adds exactly 0 to both sums.
+constexpr float kNegBig = -0x1p126f;
+constexpr float kMaskedLogit = -0x1p127f;
 
 // ----------------------------------------------------------------------------- logit element types
 struct Bf16 { uint16_t bits; };
@@ -80,6 +86,12 @@ template <> struct Elem<float> {
     f[0] = __uint_as_float(v.x); f[1] = __uint_as_float(v.y);
     f[2] = __uint_as_float(v.z); f[3] = __uint_as_float(v.w);
   }
+  // -inf (and only values below kMaskedLogit, outside the logit range) to kMaskedLogit:
+  // an unsigned min on the raw bits, since negative floats order by magnitude there
+  __device__ static uint32_t clamp_word(uint32_t w) { return w < 0xff000000u ? w : 0xff000000u; }
+  __device__ static uint4 clamp_masked(const uint4& v) {
+    return make_uint4(clamp_word(v.x), clamp_word(v.y), clamp_word(v.z), clamp_word(v.w));
+  }
 };
 template <> struct Elem<Bf16> {
   static constexpr int VEC = 8;
@@ -102,6 +114,46 @@ template <> struct Elem<Bf16> {
     f[4] = __uint_as_float(v.z << 16); f[5] = __uint_as_float(v.z & 0xffff0000u);
     f[6] = __uint_as_float(v.w << 16); f[7] = __uint_as_float(v.w & 0xffff0000u);
   }
+  // -inf (0xff80) to kMaskedLogit (0xff00) in both halves of a word at once: a packed
+  // unsigned 16-bit min (v_pk_min_u16), one instruction per two logits
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  __device__ static uint32_t clamp_word(uint32_t w) {
+    const u16x2 lim = {0xff00, 0xff00};
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_min(__builtin_bit_cast(u16x2, w), lim));
+  }
+  __device__ static uint4 clamp_masked(const uint4& v) {
+    return make_uint4(clamp_word(v.x), clamp_word(v.y), clamp_word(v.z), clamp_word(v.w));
+  }
+};
+
+// Whether a stream of raw 16-byte vectors held a -inf logit, for the drafter-row flag
+// (the clamped values no longer show it).  bf16: the matrix core sums each vector's
+// eight logits against ones (one MFMA per vector, beside the VALU work); a -inf
+// anywhere makes the sums -inf, and with |z| < 2^96 no finite sum overflows.  The
+// sums of one lane's data land in other lanes, so the verdict is taken over the wave.
+// fp32: the unsigned max of the raw bits reaches 0xff800000 only for -inf.
+template <typename T> struct MaskProbe;
+template <> struct MaskProbe<Bf16> {
+  typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  __device__ void add(const uint4& v) {
+    const uint4 ones = make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, v), __builtin_bit_cast(bf16x8, ones),
+                                                  acc, 0, 0, 0);
+  }
+  __device__ bool hit() const {
+    return !(acc[0] > -INFINITY && acc[1] > -INFINITY && acc[2] > -INFINITY && acc[3] > -INFINITY);
+  }
+};
+template <> struct MaskProbe<float> {
+  uint32_t m = 0;
+  __device__ void add(const uint4& v) {
+    const uint32_t a = v.x > v.y ? v.x : v.y, b = v.z > v.w ? v.z : v.w;
+    m = m > a ? m : a;
+    m = m > b ? m : b;
+  }
+  __device__ bool hit() const { return m >= 0xff800000u; }
 };
 
 // Row geometry: `head` leading elements before the first 16-byte boundary, `nvec`
@@ -485,7 +537,7 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
   __shared__ float sf[BD / 64];
   __shared__ double ep_d[ND][BD / 64];
   __shared__ float ep_f[2][BD / 64];
-  __shared__ int ep_i[2][BD / 64];
+  __shared__ int ep_i[3][BD / 64];
   const int t = threadIdx.x;
   {
     const Geom g = row_geom(row, V);
@@ -499,15 +551,28 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
     uint4 keep[KEEP ? U : 1];
 #pragma unroll
     for (int u = 0; u < (KEEP ? U : 1); ++u) keep[u] = make_uint4(0u, 0u, 0u, 0u);
+    // Masked (-inf) logits: every logit is clamped to at least kMaskedLogit before the
+    // sums (a masked one then adds exactly 0 to A and T), and a probe over the raw
+    // vectors (plus a test of the single head, tail and partial-round elements) records
+    // that the row held one: one read of every row.  Only the variance moments of a
+    // masked row are redone, without its -inf logits, by a second pass.
+    MaskProbe<T> probe;
+    bool ninf_el = false;
+    auto clamp1 = [&](float z) {
+      ninf_el |= z == -INFINITY;
+      return fmaxf(z, kMaskedLogit);
+    };
 
     // full rounds, next round's loads issued before the current one is consumed
     // the head elements are loaded and folded in once the first rounds are requested
     stream_rounds<U, BD, DEPTH>(vp, nr, t, [&] {
-      if (t < g.head) conf_one<VAR>(s, E::load(row + t), 0);
+      if (t < g.head) conf_one<VAR>(s, clamp1(E::load(row + t)), 0);
     }, [&](const uint4 (&raw)[U], int64_t k) {
       float f[N];
 #pragma unroll
-      for (int u = 0; u < U; ++u) E::unpack(raw[u], f + u * VEC);
+      for (int u = 0; u < U; ++u) E::unpack(E::clamp_masked(raw[u]), f + u * VEC);
+#pragma unroll
+      for (int u = 0; u < U; ++u) probe.add(raw[u]);
       conf_chunk<N, false, VAR>(s, f, 0xffffffffu, int(k + 1));
       if (KEEP) {
         const bool up = s.gid == int(k + 1);
@@ -536,10 +601,12 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
           for (int e = 0; e < VEC; ++e) f[u * VEC + e] = -INFINITY;
         }
       }
+#pragma unroll
+      for (int j = 0; j < N; ++j) f[j] = ((valid >> j) & 1u) ? clamp1(f[j]) : f[j];
       conf_chunk<N, true, VAR>(s, f, valid, int(nr + 1));
     }
     const int64_t tail0 = g.head + g.nvec * VEC;
-    if (t < g.tail) conf_one<VAR>(s, E::load(row + tail0 + t), int(nr + 2));
+    if (t < g.tail) conf_one<VAR>(s, clamp1(E::load(row + tail0 + t)), int(nr + 2));
 
     // ---- epilogue: row max, first index of the max, second logit, normaliser
     const float m = block_all_f<BD>(s.t1, OpMax(), sf);
@@ -572,10 +639,11 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
     const int idx32 = idx == INT64_MAX ? INT32_MAX : int(idx);
 
     // one LDS round for: sum A, sum T, max of the other chunk maxima, number of
-    // threads holding the max, and the lowest max index with its chunk's other value
+    // threads holding the max, the lowest max index with its chunk's other value, and
+    // whether the row held a -inf logit
     double A, Tsum, vN = 0.0, vS1 = 0.0, vS2 = 0.0;
     float cmx, s_oth;
-    int nmax, top1;
+    int nmax, top1, ninf = 0;
     {
       const double wA = wave_all_d(Ad, OpSumD());
       const double wT = wave_all_d(Td, OpSumD());
@@ -592,6 +660,7 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
       const int wi = wave_all_i(idx32, OpMinI());
       const unsigned long long own = __ballot(idx32 == wi && is_max);
       const float wo = own ? rl_f(other, __builtin_ctzll(own)) : -INFINITY;
+      const int wninf = __ballot(ninf_el || probe.hit()) != 0ull ? 1 : 0;
       __syncthreads();
       if ((t & 63) == 0) {
         const int w = t >> 6;
@@ -606,6 +675,7 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
         ep_f[1][w] = wo;
         ep_i[0][w] = wn;
         ep_i[1][w] = wi;
+        ep_i[2][w] = wninf;
       }
       __syncthreads();
       A = ep_d[0][0];
@@ -614,6 +684,7 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
       s_oth = ep_f[1][0];
       nmax = ep_i[0][0];
       top1 = ep_i[1][0];
+      ninf = ep_i[2][0];
       if constexpr (VAR) {
         vN = ep_d[ND - 3][0];
         vS1 = ep_d[ND - 2][0];
@@ -630,28 +701,24 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
         }
         cmx = fmaxf(cmx, ep_f[0][w]);
         nmax += ep_i[0][w];
+        ninf |= ep_i[2][w];
         if (ep_i[1][w] < top1) {
           top1 = ep_i[1][w];
           s_oth = ep_f[1][w];
         }
       }
     }
-    uint32_t flags = 0;
-    if (Tsum != Tsum) {
-      // the row holds -inf logits: recompute T (and the variance moments) skipping them
-      flags |= 1u;
-      float tl = 0.f;
+    const uint32_t flags = ninf ? 1u : 0u;  // bit 0: the row holds -inf logits
+    if (VAR && ninf) {
+      // the variance moments of a masked row, about the row max and without its -inf
+      // logits (the clamped values entered the streaming moments)
       double vm[3] = {0.0, 0.0, 0.0};
       auto acc = [&](float z) {
         if (z > -INFINITY) {
-          const float x = fmaf(z, kLog2e, -ms_row);
-          tl = fmaf(fexp2(x), x, tl);
-          if (VAR) {
-            const double dz = (double)z - (double)m;
-            vm[0] += 1.0;
-            vm[1] += dz;
-            vm[2] += dz * dz;
-          }
+          const double dz = (double)z - (double)m;
+          vm[0] += 1.0;
+          vm[1] += dz;
+          vm[2] += dz * dz;
         }
       };
       if (t < g.head) acc(E::load(row + t));
@@ -662,17 +729,16 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
         for (int e = 0; e < VEC; ++e) acc(f[e]);
       }
       if (t < g.tail) acc(E::load(row + tail0 + t));
-      Tsum = block_all_d<BD>((double)tl, OpSumD(), sd);
-      if (VAR) {
-        block_sum_n<BD, 3>(vm, sd);
-        vN = vm[0];
-        vS1 = vm[1];
-        vS2 = vm[2];
-      }
+      block_sum_n<BD, 3>(vm, sd);
+      vN = vm[0];
+      vS1 = vm[1];
+      vS2 = vm[2];
     }
     __syncthreads();
     if (t == 0) {
-      *out = row_stats_record(m, nmax >= 2 ? m : fmaxf(cmx, s_oth), A, Tsum, flags, top1, V, a);
+      // a second value at kMaskedLogit or below is a clamped -inf: the row has one finite logit
+      const float z2 = nmax >= 2 ? m : fmaxf(cmx, s_oth);
+      *out = row_stats_record(m, z2 <= kMaskedLogit ? -INFINITY : z2, A, Tsum, flags, top1, V, a);
       if (VAR) {
         const double v = (vS2 - vS1 * (vS1 / vN)) / vN;
         *var_out = (float)(v > 0.0 ? v : 0.0);

@@ -119,10 +119,14 @@ class SpeculativeDecoder:
     def _uniform(self, n: int) -> torch.Tensor:
         return torch.rand(n, generator=self.gen, device=self.dev, dtype=torch.float32)
 
-    def step(self, tok: torch.Tensor, lens: torch.Tensor, active: torch.Tensor | None = None) -> None:
+    def step(self, tok: torch.Tensor, lens: torch.Tensor, active: torch.Tensor | None = None,
+             record: list | None = None) -> None:
         """One iteration on the padded token buffer tok [B, cap] (valid prefix lens[b]);
-        sequences where ``active`` is False are decoded but not advanced or counted."""
+        sequences where ``active`` is False are decoded but not advanced or counted.
+        ``record``: if a list, a host copy of the iteration's inputs and outputs of
+        the library calls is appended to it (for checking an iteration elsewhere)."""
         B, K = self.B, self.K
+        draft_u = []
         ar = torch.arange(B, device=self.dev)
         lmax = int(lens.max())
         assert lmax + K + 1 <= tok.shape[1] and lmax + K <= self.max_len
@@ -135,8 +139,9 @@ class SpeculativeDecoder:
             if self.greedy:
                 self.draw.copy_(self.st_step.view(torch.int32)[:, 6])     # the drafter's top token
             else:
-                cmsd.cmsd_draft_sample(rows, self.st_step, self._uniform(B), drafted=self.draw,
-                                       workspace=self.ws_draft)
+                u = self._uniform(B)
+                draft_u.append(u)
+                cmsd.cmsd_draft_sample(rows, self.st_step, u, drafted=self.draw, workspace=self.ws_draft)
             self.drafted[:, i] = self.draw
             tok[ar, lens + i] = self.draw.long()
             self.lp.stats.view(B, K, 8)[:, i] = self.st_step
@@ -157,6 +162,12 @@ class SpeculativeDecoder:
         n_acc = self.lp.n_acc.long()
         nxt = self.lp.next_tok.long()
         k = self.lp.k.long()
+        if record is not None:
+            record.append({"draft": self.dl.cpu(), "draft_u": torch.stack(draft_u, 1).cpu() if draft_u else None,
+                           "drafted": self.drafted.cpu(), "stats": self.lp.stats.cpu(), "k": self.lp.k.cpu(),
+                           "off": self.lp.off.cpu(), "target": target.cpu(),
+                           "unif": None if unif is None else unif.cpu(), "tstats": self.lp.tstats.cpu(),
+                           "n_acc": self.lp.n_acc.cpu(), "next": self.lp.next_tok.cpu()})
         if bool((n_acc < 0).any()):
             raise RuntimeError("cmsd_verify reported an invalid sequence")
         if active is None:

@@ -89,3 +89,65 @@ def test_standard_first_token_follows_target(mods):
     pd = torch.softmax(drafter(prompt[:1]).double()[0, -1], -1).cpu().numpy()
     print(f"[standard e2e] chi2={chi2:.2f} p={pval:.4f} TV(p_t, p_d)={0.5 * np.abs(p - pd).sum():.3f}")
     assert pval > 1e-4
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2])
+def test_loop_iterations_match_the_oracle(mods, mode):
+    # Each iteration of the decoding loop checked against the oracle on the rows the
+    # models produced (Sec. III.A / III.B): the drafted tokens against the oracle's
+    # softmax sampler with the same uniforms (GREEDY: the drafter's top token), every
+    # drafter record, each sequence's draft length (with its floor slack), the packed
+    # offsets, and the verification (accept flags, prefix, next token) of the k_b + 1
+    # packed target rows, under the slack rule.
+    from oracle import cmsd_oracle as O
+    from tests import parity as Pa
+    cmsd, decode, pipeline = mods
+    dev = torch.device("cuda:0")
+    V, B, K, iters = 6000, 8, 6, 4
+    target = decode.TinyLM(V, d=64, seed=41 + mode).to(dev)
+    drafter = target.perturbed(0.15, 42 + mode).to(dev)
+    prompt = torch.randint(0, V, (B, 8), generator=torch.Generator().manual_seed(6 + mode)).to(dev)
+    prm = pipeline.Params(mode=mode)
+    dec = decode.SpeculativeDecoder(target, drafter, B, K, prm, dev, seed=mode + 1)
+    cap = 8 + iters * (K + 1) + 2 * K + 2
+    tok = torch.zeros((B, cap), dtype=torch.long, device=dev)
+    tok[:, :8] = prompt
+    lens = torch.full((B,), 8, dtype=torch.long, device=dev)
+    P = {"lambdas": prm.lambdas, "beta_margin": prm.beta_margin, "k_min": prm.k_min, "alpha": prm.alpha,
+         "top_beta": prm.top_beta, "tau_base": prm.tau_base, "gamma": prm.gamma}
+    lam = tuple(Pa.f32(x) for x in prm.lambdas)
+    bm = Pa.f32(prm.beta_margin)
+    for it in range(iters):
+        rec = []
+        dec.step(tok, lens, record=rec)
+        r = rec[0]
+        t = Pa.Tally()
+        gs = Pa.stats_fields(r["stats"].numpy(), r["stats"].view(torch.int32).numpy())
+        ts = Pa.tstats_fields(r["tstats"].numpy(), r["tstats"].view(torch.int32).numpy())
+        draft = r["draft"].double().numpy()
+        target_rows = r["target"].double().numpy()
+        drafted = r["drafted"].numpy()
+        k = r["k"].numpy()
+        off = r["off"].numpy()
+        n_acc, nxt = r["n_acc"].numpy(), r["next"].numpy()
+        assert np.array_equal(off, np.concatenate([[0], np.cumsum(k.astype(np.int64) + 1)]))
+        for b in range(B):
+            zd = [draft[b, i] for i in range(K)]
+            C = []
+            for i in range(K):
+                rs = Pa.check_row_stats(t, gs, b * K + i, zd[i], V, lam, bm)
+                C.append(O.confidence(rs, V, lam, bm))
+                if mode == O.MODE_GREEDY:
+                    t.value(f"drafted[{b},{i}]", int(drafted[b, i]) == rs.top1, (int(drafted[b, i]), rs.top1))
+                else:
+                    y, sl = O.draft_sample(zd[i], float(r["draft_u"][b, i]))
+                    t.decision(f"drafted[{b},{i}]", int(drafted[b, i]), y, sl)
+            kb_o, _, sl = O.draft_len(np.array([C]), prm.k_min, K, Pa.f32(prm.alpha))
+            t.decision(f"k[{b}]", int(k[b]), int(kb_o[0]), float(sl[0]))
+            kb, o = int(k[b]), int(off[b])
+            zt = [target_rows[o + i] for i in range(kb + 1)]
+            unif = [0.0] * (kb + 1) if r["unif"] is None else [float(x) for x in r["unif"][o:o + kb + 1]]
+            Pa.check_sequence(t, b, zt, zd, drafted[b], unif, C, kb, mode, P, ts, o, int(n_acc[b]), int(nxt[b]))
+        print(f"[loop vs oracle] mode={mode} iteration={it}: checked={t.checked} exceptions={t.exceptions} "
+              f"k={k.tolist()} n_acc={n_acc.tolist()}", flush=True)
+        t.assert_ok()

@@ -36,6 +36,11 @@ drafter and verifier outputs):
   ``[B, k_max+1, V]`` (bonus row stored at slot k_max) and packed afterwards.
 * ``v152k``: a sweep point, not one of the five: B=64, k_max=8, V=152064 (the top
   of the metric's vocabulary range), bf16, with c2's row recipe.
+* ``c5m``  : c5 with masked logits: every drafter row and the target row of the same
+  position set -inf on one seeded mask of the vocabulary (the last 128 tokens, as
+  padding of a vocabulary rounded up, plus 3 % of the others at random, as a decoding
+  constraint); each bonus row has a mask of its own.  Drafts never land on a masked
+  token (they are softmax samples).
 
 Uniforms are ``randint(0, 2^24) * 2^-24`` as fp32: exactly representable and
 strictly below 1.  Drafted ids (except ``tiny``) are exact samples from the
@@ -66,6 +71,8 @@ _S_GUMBEL = 5
 _S_UNIFORM = 6
 _S_REGIME = 7
 _S_INDEP = 8
+_S_MASK = 9
+_S_BONUS_MASK = 10
 
 
 @dataclass(frozen=True)
@@ -78,6 +85,7 @@ class Config:
     dtype: str          # "f32" or "bf16"
     ragged: bool = False
     style: str = ""     # row recipe of another config (a sweep point), else the config's own
+    masked: bool = False  # -inf on a seeded mask per position (see c5m)
 
     @property
     def kind(self) -> str:
@@ -106,7 +114,30 @@ CONFIGS = {
     "v152k": Config("v152k", 5, 64, 8, 152064, "bf16", style="c2"),
     # one sequence (single-stream decoding latency), with c2's row recipe
     "b1": Config("b1", 6, 1, 8, 32000, "bf16", style="c2"),
+    # c5 with masked logits (vocabulary padding and a decoding constraint)
+    "c5m": Config("c5m", 7, 512, 16, 32000, "bf16", ragged=True, style="c5", masked=True),
 }
+
+_MASK_TAIL = 128       # masked tokens at the end of the vocabulary
+_MASK_FRAC = 0.03      # masked share of the other tokens
+
+
+def _mask(cfg: Config, seed: int, stream: int, index: int) -> np.ndarray:
+    """Boolean [V] mask of a masked config: the last _MASK_TAIL tokens and a seeded
+    _MASK_FRAC of the others."""
+    V = cfg.V
+    g = _rng(cfg, seed, stream, index)
+    m = g.random(V) < _MASK_FRAC
+    m[V - _MASK_TAIL:] = True
+    return m
+
+
+def _masked(cfg: Config, z: np.ndarray, seed: int, stream: int, index: int) -> np.ndarray:
+    if not cfg.masked:
+        return z
+    z = np.array(z, dtype=np.float64)
+    z[_mask(cfg, seed, stream, index)] = -np.inf
+    return z
 
 
 def _rng(cfg: Config, seed: int, stream: int, index: int) -> np.random.Generator:
@@ -117,7 +148,7 @@ def _rng(cfg: Config, seed: int, stream: int, index: int) -> np.random.Generator
 def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
     """Round float32 values to bfloat16 (round to nearest, ties to even); return the raw uint16 bits.
 
-    Inputs here are always finite, so no NaN special case is needed.
+    Inputs here are finite or -inf (masked logits), so no NaN special case is needed.
     """
     b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
     r = (b + np.uint32(0x7FFF) + ((b >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
@@ -223,7 +254,7 @@ def _c4_regime_row(V: int, reg: int, g: np.random.Generator) -> np.ndarray:
 
 def draft_row(cfg: Config, seed: int, row: int) -> np.ndarray:
     """Stored drafter row ``row`` (= b*k_max + i): float32 values, or uint16 bf16 bits."""
-    return _store(cfg, _draft_row_f64(cfg, seed, row))
+    return _store(cfg, _masked(cfg, _draft_row_f64(cfg, seed, row), seed, _S_MASK, row))
 
 
 def _c3_params(cfg: Config, seed: int, row: int):
@@ -235,6 +266,22 @@ def _c3_params(cfg: Config, seed: int, row: int):
 
 
 def target_row(cfg: Config, seed: int, b: int, i: int, draft_stored: np.ndarray | None = None) -> np.ndarray:
+    """Stored target row for sequence ``b``, position ``i`` in 0..k_max (masked configs:
+    position i < k_max shares drafter row b*k_max+i's mask, the bonus row has its own)."""
+    z = _target_row_unmasked(cfg, seed, b, i, draft_stored)
+    if not cfg.masked:
+        return z
+    zf = _stored_as_f32(cfg, z).astype(np.float64)
+    K = cfg.k_max
+    if i == K:
+        zf[_mask(cfg, seed, _S_BONUS_MASK, b)] = -np.inf
+    else:
+        zf[_mask(cfg, seed, _S_MASK, b * K + i)] = -np.inf
+    return _store(cfg, zf)
+
+
+def _target_row_unmasked(cfg: Config, seed: int, b: int, i: int,
+                         draft_stored: np.ndarray | None = None) -> np.ndarray:
     """Stored target row for sequence ``b``, position ``i`` in 0..k_max.
 
     Position ``k_max`` is the bonus row (for the ragged config it is the row that
