@@ -20,7 +20,7 @@ oracle runs last on the host.
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4|c5|c5m|c3|c2|v152k|tiny|b1]
                   [--mode cm|standard] [--path auto|pass|fused|calls] [--streams G] [--event-every N]
                   [--capacity-rows] [--no-rotate] [--extras] [--no-read-ceiling] [--no-cpu-baseline]
-                  [--copy-probe MIB]
+                  [--row-shape THREADS,DEPTH] [--copy-probe MIB]
 """
 from __future__ import annotations
 
@@ -82,6 +82,8 @@ def cpu_baseline(name: str, seed: int, mode: int, budget_s: float = 20.0) -> dic
         ncpu = len(os.sched_getaffinity(0))
     except AttributeError:
         ncpu = os.cpu_count() or 1
+    # one process per host core this process may run on, at most 16 (a one-GPU machine's
+    # share of its host); the line states both the cores used and the host's count
     workers = max(1, min(16, ncpu))
     # estimate the per-sequence cost with one sequence, then size the sample to the budget
     rows1, t1 = _cpu_baseline_worker((name, seed, 0, mode))
@@ -96,9 +98,24 @@ def cpu_baseline(name: str, seed: int, mode: int, budget_s: float = 20.0) -> dic
         if len(idx):
             rate += sum(res[i][0] for i in idx) / sum(res[i][1] for i in idx)
     return {"value": rate, "unit": "rows/s", "cores": workers, "kind": "oracle",
+            "host_cpus": ncpu, "host_cpus_online": os.cpu_count(), "cpu_model": _cpu_model(),
+            "core_cap": f"min(16, {ncpu} cores available to the process)",
             "sample": f"{nseq} of {cfg.B} sequences of {name} (each {cfg.k_max} drafter + "
                       f"{'k_b+1' if cfg.ragged else cfg.k_max + 1} target rows, V={cfg.V}), numpy fp64, "
                       f"{workers} processes"}
+
+
+def _cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo), or the platform's processor string."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
 
 
 def kernel_code_hash() -> str:
@@ -237,6 +254,9 @@ def main() -> int:
     ap.add_argument("--no-read-ceiling", action="store_true",
                     help="skip the bare-read ceiling (a read of the roofline kernel's rows in its grid "
                          "shape, timed after the timed region)")
+    ap.add_argument("--row-shape", default="", metavar="THREADS,DEPTH",
+                    help="force the row kernels' workgroup size and loads in flight (cmsd_set_row_shape; "
+                         "0 keeps the library's per-launch choice), e.g. 64,3")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run device-to-device copies of MIB MiB (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -261,6 +281,8 @@ def main() -> int:
 
     cfg = W.CONFIGS[args.workload]
     mode = cmsd.CMSD_MODE_CM if args.mode == "cm" else cmsd.CMSD_MODE_STANDARD
+    if args.row_shape:
+        cmsd.cmsd_set_row_shape(*(int(x) for x in args.row_shape.split(",")))
     dev = torch.device("cuda:0")
     print(f"[bench] generating {cfg.name} seed {args.seed}", file=sys.stderr, flush=True)
     d = W.generate(cfg, args.seed)

@@ -33,8 +33,9 @@
  *     sequence through the outputs (see cmsd_verify) without reading out of
  *     bounds.
  *   - Logit preconditions (not checked): every row has at least one finite
- *     entry; entries are finite with |z| < 2^127, or -inf (masked tokens); no
- *     NaN or +inf.  Violations give unspecified values, never a fault.
+ *     entry; entries are finite with |z| < 2^96, or -inf (masked tokens); no
+ *     NaN or +inf.  Violations give unspecified values, never a fault.  Rows with
+ *     -inf entries are read once, like any other.
  *   - Logit dtypes: CMSD_F32 (float) or CMSD_BF16 (raw bfloat16, 2 bytes).
  *     Pointers must be aligned to the element size; rows need no other
  *     alignment (an unaligned head and tail are read element-wise).

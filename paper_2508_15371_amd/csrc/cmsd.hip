@@ -757,44 +757,60 @@ __global__ __launch_bounds__(BD) void k_confidence(const T* __restrict__ logits,
 }
 
 // ----------------------------------------------------------------------------- K2 draft length
+// One workgroup.  The confidences of a tile of sequences are read with coalesced loads
+// (consecutive threads, consecutive records) into LDS, padded to k_max + 1 floats per
+// sequence so the per-sequence reads hit distinct banks; thread b then sums its
+// sequence left to right in fp64, clips the floor, and a block scan of k_b + 1 gives
+// the offsets.
 constexpr int kDraftBD = 1024;
+constexpr int kDraftLds = 16384;  // staged confidences (64 KB)
 
 __global__ __launch_bounds__(kDraftBD) void k_draft_len(const cmsd_row_stats* __restrict__ stats, int B, int k_min,
                                                         int k_max, float alpha, int32_t* __restrict__ k_out,
                                                         int32_t* __restrict__ off_out) {
+  __shared__ float s_c[kDraftLds];
   __shared__ int s_w[kDraftBD / 64];
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
+  const int ld = k_max + 1;                                  // LDS floats per sequence
+  const int tile = kDraftLds / ld < kDraftBD ? kDraftLds / ld : kDraftBD;  // >= 3 (k_max <= 4096)
   int carry = 0;
-  for (int base = 0; base < B; base += kDraftBD) {
-    const int b = base + t;
-    int kb = 0;
-    if (b < B) {
-      const cmsd_row_stats* p = stats + (int64_t)b * k_max;
-      double s = 0.0;
-      for (int i0 = 0; i0 < k_max; i0 += 16) {  // up to 16 loads in flight per thread
-        float c[16];
+  for (int base = 0; base < B; base += tile) {
+    const int nb = B - base < tile ? B - base : tile;
+    const int n = nb * k_max;
+    const cmsd_row_stats* p = stats + (int64_t)base * k_max;
+    for (int j0 = 0; j0 < n; j0 += 8 * kDraftBD) {          // 8 loads in flight per thread
+      float c[8];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) c[j] = i0 + j < k_max ? p[i0 + j].conf : 0.f;
-#pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if (i0 + j < k_max) s += (double)c[j];
+      for (int u = 0; u < 8; ++u) {
+        const int j = j0 + u * kDraftBD + t;
+        c[u] = j < n ? p[j].conf : 0.f;
       }
-      const double x = (double)alpha * (s / (double)k_max) * (double)k_max;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = j0 + u * kDraftBD + t;
+        if (j < n) s_c[(j / k_max) * ld + j % k_max] = c[u];
+      }
+    }
+    __syncthreads();
+    int kb = 0;
+    if (t < nb) {
+      const float* q = s_c + t * ld;
+      double sum = 0.0;
+      for (int i = 0; i < k_max; ++i) sum += (double)q[i];
+      const double x = (double)alpha * (sum / (double)k_max) * (double)k_max;
       const double fl = floor(x);
-      int kf = fl < (double)k_min ? k_min : (fl > (double)k_max ? k_max : (int)fl);
-      kb = kf;
-      k_out[b] = kb;
+      kb = fl < (double)k_min ? k_min : (fl > (double)k_max ? k_max : (int)fl);
+      k_out[base + t] = kb;
     }
     // exclusive scan of (k_b + 1) over the tile: wave scan by shuffles, then wave totals
-    const int v = b < B ? kb + 1 : 0;
+    const int v = t < nb ? kb + 1 : 0;
     int incl = v;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
       const int up = __shfl_up(incl, o);
       if (lane >= o) incl += up;
     }
-    __syncthreads();
     if (lane == 63) s_w[w] = incl;
     __syncthreads();
     int wpre = 0, tot = 0;
@@ -802,8 +818,9 @@ __global__ __launch_bounds__(kDraftBD) void k_draft_len(const cmsd_row_stats* __
       if (i < w) wpre += s_w[i];
       tot += s_w[i];
     }
-    if (b < B) off_out[b] = carry + wpre + incl - v;
+    if (t < nb) off_out[base + t] = carry + wpre + incl - v;
     carry += tot;
+    __syncthreads();  // s_c and s_w are refilled by the next tile
   }
   if (t == 0) off_out[B] = carry;
 }
@@ -1103,9 +1120,9 @@ __device__ __forceinline__ void target_row(const VerifyArgs& a, int64_t r) {
   }
 }
 
-template <typename T, int BD>
+template <typename T, int BD, int DEPTH>
 __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
-  target_row<T, BD, false>(a, blockIdx.x);
+  target_row<T, BD, false, DEPTH>(a, blockIdx.x);
 }
 
 // The row pass of cmsd_logit_pass: drafter rows (stats) and dense target rows in one
@@ -1959,15 +1976,24 @@ void launch_confidence(int bd, const T* logits, int64_t n_rows, int64_t V, int64
     launch_confidence_d<T, VAR, CMSD_STREAM_DEPTH>(bd, logits, n_rows, V, stride, a, out, var, st);
 }
 
-template <typename T>
-void launch_target_rows(int bd, const VerifyArgs& a, hipStream_t st) {
+template <typename T, int DEPTH>
+void launch_target_rows_d(int bd, const VerifyArgs& a, hipStream_t st) {
   const dim3 grid((unsigned)a.target_rows);
   if (bd == 64)
-    hipLaunchKernelGGL((k_target_rows<T, 64>), grid, dim3(64), 0, st, a);
+    hipLaunchKernelGGL((k_target_rows<T, 64, DEPTH>), grid, dim3(64), 0, st, a);
   else if (bd == 128)
-    hipLaunchKernelGGL((k_target_rows<T, 128>), grid, dim3(128), 0, st, a);
+    hipLaunchKernelGGL((k_target_rows<T, 128, DEPTH>), grid, dim3(128), 0, st, a);
   else
-    hipLaunchKernelGGL((k_target_rows<T, 256>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((k_target_rows<T, 256, DEPTH>), grid, dim3(256), 0, st, a);
+}
+// The packed target rows of cmsd_verify: two rounds in flight (three measured slower
+// on c5's 3097 rows of 64 KB), three only when forced.
+template <typename T>
+void launch_target_rows(int bd, const VerifyArgs& a, hipStream_t st) {
+  if (g_ring_depth.load(std::memory_order_relaxed) == 3)
+    launch_target_rows_d<T, CMSD_DEEP_DEPTH>(bd, a, st);
+  else
+    launch_target_rows_d<T, CMSD_STREAM_DEPTH>(bd, a, st);
 }
 
 // The joint row pass.  With events, the launch goes through hipExtLaunchKernel, which

@@ -40,3 +40,13 @@ def test_read_probe_library_checks_its_arguments():
     assert f(fake, 4, 100, fake, 4, 100, 100, 256, 4, None, None) == 1       # no sink
     assert f(fake, -1, 100, fake, 4, 100, 100, 256, 4, fake, None) == 1      # negative count
     assert f(None, 0, 0, None, 0, 0, 100, 256, 4, fake, None) == 0           # nothing to read: no launch
+
+
+def test_cpu_baseline_states_cores_and_cpu_model():
+    sys.path.insert(0, ROOT)
+    import bench
+    r = bench.cpu_baseline("tiny", 0, 1, budget_s=0.5)
+    assert r["kind"] == "oracle" and r["unit"] == "rows/s" and r["value"] > 0
+    assert 1 <= r["cores"] <= min(16, r["host_cpus"])
+    assert r["host_cpus"] >= 1 and isinstance(r["cpu_model"], str) and r["cpu_model"]
+    assert "16" in r["core_cap"]
