@@ -211,8 +211,10 @@ cmsd_status cmsd_draft_len(const cmsd_row_stats* stats, int32_t batch, const cms
  *   dtype           logit dtype of both logit arrays.
  *   batch >= 0, k_max in [1, 4096], vocab in [2, 2^31).
  *   params          host; see cmsd_verify_params.
- *   target_stats    device, target_rows records (output; rows beyond
- *                   target_offsets[batch] untouched).
+ *   target_stats    device, target_rows records (output): the k_b + 1 rows of every
+ *                   sequence with a valid draft length and offsets; rows beyond
+ *                   target_offsets[batch], and the rows of a sequence reported
+ *                   invalid for its draft length or offsets, are not written.
  *   n_accepted      device, batch int32 (output): accepted prefix length c_b in
  *                   [0, k_b]; -1 if the sequence's device inputs are invalid
  *                   (offsets inconsistent with draft_len or target_rows, draft_len

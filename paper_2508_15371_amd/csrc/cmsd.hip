@@ -979,74 +979,48 @@ __device__ __forceinline__ int accept_test(int mode, int beta, float tau_base, f
 // One target row.  PASS = false: a packed row of cmsd_verify (sequence found from the
 // offsets, accept test made here).  PASS = true: dense row r = b*(k_max+1) + i of the
 // single-call pass, whose accept test waits for the drafter stats (PassSlot).
+// One target row.  PASS = false: position q = b*(k_max+1) + i of cmsd_verify's grid over
+// (sequence, position); the sequence's draft length and offsets and the position's
+// drafted id and drafter stats are loaded in one round from q alone, positions past
+// k_b (and sequences with an invalid length or offsets, which the final-token kernels
+// report) end there, else the row is packed row off[b] + i and its accept test is made
+// here.  PASS = true: dense row q = b*(k_max+1) + i of the single-call pass, whose
+// accept test waits for the drafter stats (PassSlot).
 template <typename T, int BD, bool PASS, int DEPTH = CMSD_STREAM_DEPTH>
-__device__ __forceinline__ void target_row(const VerifyArgs& a, int64_t r) {
+__device__ __forceinline__ void target_row(const VerifyArgs& a, int64_t q) {
   using E = Elem<T>;
   __shared__ double sd[BD / 64];
   __shared__ float sf[BD / 64];
   __shared__ int si[BD / 64];
   const int t = threadIdx.x;
+  const int b = int(q / (a.k_max + 1));
+  const int i = int(q - (int64_t)b * (a.k_max + 1));
+  const bool in_k = i < a.k_max;
+  const int64_t drow = (int64_t)b * a.k_max + (in_k ? i : 0);
+  int64_t r = q;
+  int kb = a.k_max, y = -1;
+  cmsd_row_stats ds{};
   if (!PASS) {
-    const int total = a.off[a.B];
-    if (r >= total || r >= a.target_rows) return;
+    if (b >= a.B) return;
+    kb = a.klen[b];
+    const int64_t ob = a.off[b], ob1 = a.off[b + 1];
+    y = in_k ? a.drafted[drow] : -1;
+    if (in_k) ds = a.dstats[drow];
+    if (kb < 0 || kb > a.k_max || i > kb || ob < 0 || ob1 != ob + kb + 1 || ob1 > a.target_rows) return;
+    r = ob + i;
   }
   const T* trow = reinterpret_cast<const T*>(a.target) + r * a.tstride;
   const Geom g = row_geom(trow, a.V);
 
-  // resolved by prep(), while the first rounds of the row load
-  bool valid = false, layout = false, has_draft = false, count = false;
-  int b = 0, i = 0, yd = -1;
+  // The drafted token's target and drafter logits (the accept test and the rank count
+  // need them): requested before the row's first rounds when the id is already known
+  // (cmsd_verify), so their latency hides behind the rounds'; in the single-call pass
+  // the id load itself waits for the first rounds to be requested (prep()).
+  bool valid = true, has_draft = false, count = false;
+  const bool layout = true;
+  int yd = -1;
   float gz = -INFINITY, zd = -INFINITY, cm = 0.f, dm = 0.f, dA = 1.f;
-  auto prep = [&] {
-    if (PASS) {
-      b = int(r / (a.k_max + 1));
-      i = int(r - (int64_t)b * (a.k_max + 1));
-      layout = true;
-      valid = true;
-      has_draft = i < a.k_max;
-      if (has_draft) {
-        const int64_t drow = (int64_t)b * a.k_max + i;
-        const int y = a.drafted[drow];
-        yd = y;
-        if (y < 0 || (int64_t)y >= a.V) {
-          valid = false;
-          has_draft = false;
-        } else {
-          gz = E::load(trow + y);
-          zd = E::load(reinterpret_cast<const T*>(a.draft) + drow * a.dstride + y);
-        }
-      }
-      count = has_draft && a.mode != CMSD_MODE_STANDARD && a.beta > 0;
-      return;
-    }
-    // sequence owning row r, from one scan of the offsets: b = #{j in 1..B : off[j] <= r},
-    // and (for non-decreasing offsets) off[b] = the largest offset <= r and off[b+1] =
-    // the smallest offset[1..B] > r, so no second round trip fetches them
-    int cnt = 0, lo = INT32_MIN, hi = INT32_MAX;
-    for (int j = t; j <= a.B; j += BD) {
-      const int o = a.off[j];
-      if (o <= r) {
-        cnt += j >= 1 ? 1 : 0;
-        lo = o > lo ? o : lo;
-      } else if (j >= 1) {
-        hi = o < hi ? o : hi;
-      }
-    }
-    b = block_all_i<BD>(cnt, OpSumI(), si);
-    b = b < a.B ? b : a.B - 1;
-    const int64_t off_b = block_all_i<BD>(lo, OpMaxI(), si), off_b1 = block_all_i<BD>(hi, OpMinI(), si);
-    i = off_b >= 0 ? int(r - off_b) : 0;  // r - off[b] (no offset <= r: the layout check fails)
-    // the draft length and, for a position inside the k_max drafts, its id and drafter
-    // stats in one round trip (all in bounds whatever the layout check finds)
-    const bool in_k = off_b >= 0 && i < a.k_max;
-    const int64_t drow = (int64_t)b * a.k_max + (in_k ? i : 0);
-    const int kb = a.klen[b];
-    const int y = in_k ? a.drafted[drow] : -1;
-    const cmsd_row_stats ds = in_k ? a.dstats[drow] : cmsd_row_stats{};
-    layout = kb >= 0 && kb <= a.k_max && off_b >= 0 && off_b <= r && r < off_b1 && off_b1 == off_b + kb + 1 &&
-             off_b1 <= a.target_rows;
-    valid = layout;
-    has_draft = valid && i < kb;
+  auto gather = [&] {
     if (has_draft) {
       yd = y;
       if (y < 0 || (int64_t)y >= a.V) {
@@ -1055,12 +1029,23 @@ __device__ __forceinline__ void target_row(const VerifyArgs& a, int64_t r) {
       } else {
         gz = E::load(trow + y);
         zd = E::load(reinterpret_cast<const T*>(a.draft) + drow * a.dstride + y);
-        cm = ds.conf;
-        dm = ds.max_logit;
-        dA = ds.sum_exp;
       }
     }
     count = has_draft && a.mode != CMSD_MODE_STANDARD && a.beta > 0;
+  };
+  if (!PASS) {
+    has_draft = i < kb;
+    cm = ds.conf;
+    dm = ds.max_logit;
+    dA = ds.sum_exp;
+    gather();
+  }
+  auto prep = [&] {
+    if (PASS) {
+      has_draft = in_k;
+      if (has_draft) y = a.drafted[drow];
+      gather();
+    }
   };
   TargetState s;
   int wcnt = 0;
@@ -1978,7 +1963,7 @@ void launch_confidence(int bd, const T* logits, int64_t n_rows, int64_t V, int64
 
 template <typename T, int DEPTH>
 void launch_target_rows_d(int bd, const VerifyArgs& a, hipStream_t st) {
-  const dim3 grid((unsigned)a.target_rows);
+  const dim3 grid((unsigned)((int64_t)a.B * (a.k_max + 1)));  // one workgroup per (sequence, position)
   if (bd == 64)
     hipLaunchKernelGGL((k_target_rows<T, 64, DEPTH>), grid, dim3(64), 0, st, a);
   else if (bd == 128)
@@ -2299,7 +2284,7 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   if (batch == 0) return CMSD_OK;
   if (target_rows < 1 || target_rows > INT32_MAX) return CMSD_ERR_ARG;
   if (draft_stride < vocab || target_stride < vocab) return CMSD_ERR_ARG;
-  if ((int64_t)batch * k_max > INT32_MAX) return CMSD_ERR_ARG;
+  if ((int64_t)batch * (k_max + 1) > INT32_MAX) return CMSD_ERR_ARG;  // the target-row grid
   const size_t es = dtype == CMSD_F32 ? 4 : 2;
   if (!draft_logits || !draft_stats || !target_logits || !target_offsets || !draft_len || !drafted ||
       (!uniforms && params->mode != CMSD_MODE_GREEDY) ||
