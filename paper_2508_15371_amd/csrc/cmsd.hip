@@ -878,7 +878,8 @@ struct RowSlot {
   int32_t acc;
   int32_t r;
   int32_t top1;  // lowest index of the row max (GREEDY mode), else -1
-  int32_t pad[3];
+  float dm, dA;  // the drafter row's max and normaliser at this position (drafted positions)
+  int32_t pad;
 };
 
 struct TargetState {
@@ -1101,7 +1102,7 @@ __device__ __forceinline__ void target_row(const VerifyArgs& a, int64_t q) {
                                top1, &res.n_greater);
     }
     a.tstats[r] = res;
-    if (layout) a.slots[(int64_t)b * (a.k_max + 1) + i] = RowSlot{m, (float)A, res.accept, (int32_t)r, top1, {0, 0, 0}};
+    if (layout) a.slots[(int64_t)b * (a.k_max + 1) + i] = RowSlot{m, (float)A, res.accept, (int32_t)r, top1, dm, dA, 0};
   }
 }
 
@@ -1209,9 +1210,10 @@ __device__ __forceinline__ uint4 unit_raw2(const T* row, const Geom& g, int64_t 
 
 // What the final-token pass needs of sequence b: the layout check, the accepted
 // prefix (first rejection, by ballots over the accept flags), the row(s) of the
-// final sample and their normalisers.  Wave 0 reads the sequence's row slots and
-// drafter stats in one round trip (k_max < 64; longer drafts loop), the result is
-// broadcast through LDS.  nacc = -1 marks an invalid sequence.
+// final sample and their normalisers.  Wave 0 reads the sequence's row slots (which
+// also carry each drafted position's drafter max and normaliser) in one round trip
+// (k_max < 64; longer drafts loop), the result is broadcast through LDS.  nacc = -1
+// marks an invalid sequence.
 struct SeqInfo {
   int64_t off, tr, dr;
   int nacc, kb;
@@ -1226,7 +1228,6 @@ __device__ __forceinline__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo*
     const int64_t off = a.off[b], off1 = a.off[b + 1];
     const int kb = a.klen[b];
     const RowSlot* S = a.slots + (int64_t)b * (K + 1);
-    const cmsd_row_stats* D = a.dstats + (int64_t)b * K;
     SeqInfo q{};
     q.nacc = -1;
     const bool ok = kb >= 0 && kb <= K && off >= 0 && off1 == off + kb + 1 && off1 <= a.target_rows;
@@ -1237,9 +1238,7 @@ __device__ __forceinline__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo*
                          (j == kb && sl.acc != -1));
     };
     if (K < 64) {
-      const RowSlot sl = lane <= K ? S[lane] : RowSlot{0.f, 1.f, 1, 0, -1, {0, 0, 0}};
-      const float dmx = lane < K ? D[lane].max_logit : 0.f;
-      const float dA = lane < K ? D[lane].sum_exp : 1.f;
+      const RowSlot sl = lane <= K ? S[lane] : RowSlot{0.f, 1.f, 1, 0, -1, 0.f, 1.f, 0};
       if (ok && __ballot(bad_at(lane, sl)) == 0ull) {
         const unsigned long long rej = __ballot(lane < kb && sl.acc == 0);
         const int j = rej ? __builtin_ctzll(rej) : kb;  // slot of the final row: c, or k_b
@@ -1251,8 +1250,8 @@ __device__ __forceinline__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo*
         q.mst = rl_f(sl.m, j) * kLog2e;
         q.top1 = __builtin_amdgcn_readlane(sl.top1, j);
         if (j < kb) {
-          q.msd = rl_f(dmx, j) * kLog2e;
-          q.rho0 = (float)((double)rl_f(sl.A, j) / (double)rl_f(dA, j));
+          q.msd = rl_f(sl.dm, j) * kLog2e;
+          q.rho0 = (float)((double)rl_f(sl.A, j) / (double)rl_f(sl.dA, j));
         }
       }
     } else if (ok) {
@@ -1260,7 +1259,7 @@ __device__ __forceinline__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo*
       int j = kb;
       for (int base = 0; base <= kb; base += 64) {
         const int jj = base + lane;
-        const RowSlot sl = jj <= kb ? S[jj] : RowSlot{0.f, 1.f, 1, 0, -1, {0, 0, 0}};
+        const RowSlot sl = jj <= kb ? S[jj] : RowSlot{0.f, 1.f, 1, 0, -1, 0.f, 1.f, 0};
         if (__ballot(bad_at(jj, sl)) != 0ull) bad = true;
         const unsigned long long rej = __ballot(jj < kb && sl.acc == 0);
         if (rej != 0ull && j == kb) j = base + __builtin_ctzll(rej);
@@ -1275,9 +1274,8 @@ __device__ __forceinline__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo*
         q.mst = sl.m * kLog2e;
         q.top1 = sl.top1;
         if (j < kb) {
-          const cmsd_row_stats ds = D[j];
-          q.msd = ds.max_logit * kLog2e;
-          q.rho0 = (float)((double)sl.A / (double)ds.sum_exp);
+          q.msd = sl.dm * kLog2e;
+          q.rho0 = (float)((double)sl.A / (double)sl.dA);
         }
       }
     }
