@@ -585,24 +585,28 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
         }
       }
     });
-    // partial round
+    // partial round: whole vectors clamped and probed as in the full rounds (lanes past
+    // the row hold -inf padding, which the guarded sums skip, and show the probe zeros)
     const int64_t rb = nr * per_round;
     if (rb < g.nvec) {
       float f[N];
       uint32_t valid = 0;
+      uint4 pv[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int64_t j = rb + (int64_t)u * BD + t;
+        pv[u] = make_uint4(0u, 0u, 0u, 0u);
         if (j < g.nvec) {
-          E::unpack(ld_stream(vp + j), f + u * VEC);
+          pv[u] = ld_stream(vp + j);
           valid |= ((1u << VEC) - 1u) << (u * VEC);
-        } else {
-#pragma unroll
-          for (int e = 0; e < VEC; ++e) f[u * VEC + e] = -INFINITY;
         }
       }
 #pragma unroll
-      for (int j = 0; j < N; ++j) f[j] = ((valid >> j) & 1u) ? clamp1(f[j]) : f[j];
+      for (int u = 0; u < U; ++u) {
+        probe.add(pv[u]);
+        const bool in = (valid >> (u * VEC)) & 1u;
+        E::unpack(in ? E::clamp_masked(pv[u]) : E::raw_ninf(), f + u * VEC);
+      }
       conf_chunk<N, true, VAR>(s, f, valid, int(nr + 1));
     }
     const int64_t tail0 = g.head + g.nvec * VEC;
