@@ -42,10 +42,11 @@ PEAK_HBM_GBS = 8000.0   # MI355X HBM3E
 # device copy (x2.0 and x1.0).  Valid only for the kernel code they were taken on
 # (kernel_code_hash(): sha256 prefix of the .hip file's code without comments);
 # otherwise "traffic" is reported null.
-TRAFFIC = {"kernel_code_sha256_16": "c499ea378ab6a811",
-           "k_row_pass_c4": 2170.68e6 + 0.270e6, "k_confidence_c4": 1052.91e6 + 0.131e6,
-           "k_confidence_c5": 524.72e6 + 0.262e6, "k_row_pass_c3": 112.90e6 + 0.035e6,
-           "k_row_pass_c2": 9.13e6 + 0.004e6, "k_row_pass_v152k": 331.71e6 + 0.035e6,
+TRAFFIC = {"kernel_code_sha256_16": "e88a974d95bfa062",
+           "k_row_pass_c4": 2170.52e6 + 0.270e6, "k_confidence_c4": 1052.91e6 + 0.131e6,
+           "k_confidence_c5": 524.73e6 + 0.262e6, "k_confidence_c5m": 524.73e6 + 0.262e6,
+           "k_row_pass_c3": 112.82e6 + 0.035e6, "k_row_pass_c2": 9.13e6 + 0.004e6,
+           "k_row_pass_v152k": 331.74e6 + 0.035e6,
            "profile": "profiles/<workload>_cm_logit_pass.md"}
 
 
