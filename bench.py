@@ -11,7 +11,9 @@ sequences, k_max=16, V=128256, bf16 (the largest configuration; inputs 2.17 GB).
 
 Inputs are resident in HBM before timing; workloads smaller than 512 MiB rotate copies of
 their logits between steps (``--no-rotate`` reuses one).  HIP events around the roofline
-kernel in every 4th timed step give its achieved bandwidth; after the timed region the
+kernel in every 64th timed step give its achieved bandwidth (denser event markers slow
+the host-bound one-sequence steps: b1 at one step in 16 went from 23 to 100 us per step
+in some runs); after the timed region the
 bench times each of the three calls separately, then a bare read of the roofline
 kernel's rows in its grid shape (``read_ceiling``: what one launch of those bytes can
 reach) and, with ``--extras``, the drafting sampler and the logit-variance pass; the CPU
@@ -240,7 +242,7 @@ def main() -> int:
                          "cmsd_logit_pass_fused call (one launch, for small batches), or the three separate calls")
     ap.add_argument("--streams", type=int, default=1, metavar="G",
                     help="split the batch into G sequence groups, each on its own stream")
-    ap.add_argument("--event-every", type=int, default=4, metavar="N",
+    ap.add_argument("--event-every", type=int, default=64, metavar="N",
                     help="bracket the roofline kernel with HIP events in every N-th timed step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--capacity-rows", action="store_true",
@@ -369,8 +371,8 @@ def main() -> int:
 
     # timed region: K steps.  HIP events on the launch stream bracket the roofline
     # kernel (the joint row pass of cmsd_logit_pass, or k_confidence of group 0 on the
-    # three-call path) in every `event_every`-th step; each event marker costs GPU time
-    # between kernels, so no other kernel is bracketed here.
+    # three-call path) in every `event_every`-th step; each event marker costs time
+    # between kernels (and on short steps host time), so no other kernel is bracketed.
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] if k % args.event_every == 0 else None
           for k in range(args.steps)]
     for e in ev:

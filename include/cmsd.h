@@ -13,15 +13,15 @@
  *                    accepted-prefix length, and the final token sampled from
  *                    the residual (or bonus) distribution     (Sec. III.A, III.B(c))
  *
- * cmsd_logit_pass does all three in one call (four launches, two in GREEDY mode)
- * for a dense target layout; cmsd_logit_pass_fused does it in one launch, for small
+ * cmsd_logit_pass does all three in one call (three or four launches, two in GREEDY
+ * mode) for a dense target layout; cmsd_logit_pass_fused does it in one launch, for small
  * batches.
  *
  * Conventions shared by every call
  *   - All array pointers are DEVICE pointers (hipMalloc / torch CUDA tensors);
  *     params structs are HOST pointers read during the call.  The caller owns
  *     every buffer and the library allocates no memory.  Its only state is the
- *     row-kernel shape override of cmsd_set_row_shape and, per device, the static
+ *     overrides of cmsd_set_row_shape and cmsd_set_pass_decisions and, per device, the static
  *     scratch array of cmsd_logit_pass_noalloc.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Calls
  *     only enqueue work and return; results are ready when the stream is.
@@ -242,11 +242,14 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
  * cmsd_logit_pass - the whole logit pass of one decoding iteration in one call, for
  * a dense target layout: cmsd_confidence on the drafter rows, cmsd_draft_len's draft
  * length and cmsd_verify on target rows stored k_max + 1 per sequence (Sec. III.B(1)
- * to (c), Sec. III.A), in four launches instead of five: one row pass over the
- * drafter and target rows together (they do not depend on each other), one wave per
- * sequence that forms the draft length and the accept tests, then the two
- * final-token kernels (skipped in GREEDY mode, whose final token is the row's top
- * token).
+ * to (c), Sec. III.A), in three or four launches instead of five: one row pass over
+ * the drafter and target rows together (they do not depend on each other), then the
+ * two final-token kernels.  Each sequence's draft length and accept tests are formed
+ * either by one wave per sequence between them (large launches) or by every
+ * final-token workgroup from the row results (launches of at most 32 final-token
+ * waves per compute unit, one launch fewer); cmsd_set_pass_decisions forces either.
+ * In GREEDY mode, whose final token is the row's top token, the decision wave ends
+ * the call.
  *
  *   draft_logits    device, batch*k_max drafter rows (row b*k_max+i), stride
  *                   draft_stride >= vocab elements.
@@ -280,10 +283,10 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
  *                   cmsd_verify (calls sharing it must be ordered).
  *   workspace_bytes its size.
  *   row_events      NULL, or a host array of two hipEvent_t (created by the caller):
- *                   the row-pass launch is made with hipExtLaunchKernel, which stamps
- *                   them with that kernel's own start and end, so the caller can time
- *                   the bandwidth-bound row pass alone on its stream.  Results do not
- *                   depend on it.
+ *                   the call records the first on its stream just before the row-pass
+ *                   launch and the second just after it, so their interval times the
+ *                   bandwidth-bound row pass alone (its kernel and the gap before it).
+ *                   Results do not depend on it.
  * The arithmetic is the separate calls': the outputs are bit-identical to theirs
  * whenever the row kernels run with the same workgroup size (chosen from the number
  * of rows in the launch and their length, or forced by cmsd_set_row_shape), else
@@ -383,6 +386,21 @@ cmsd_status cmsd_logit_pass_noalloc(const void* draft_logits, int64_t draft_stri
  * always uses 256 threads.  Errors: CMSD_ERR_ARG for any other value.
  */
 cmsd_status cmsd_set_row_shape(int32_t threads, int32_t ring_depth);
+
+/*
+ * cmsd_set_pass_decisions - where cmsd_logit_pass (and cmsd_logit_pass_noalloc) forms
+ * each sequence's draft length and accept tests outside GREEDY mode, for tuning and
+ * for tests that cover both launch sequences.  Process-wide; applies to calls made
+ * after it returns.
+ *   mode  0: chosen per call from the number of final-token workgroups (default);
+ *         1: one decision wave per sequence writes a record the final-token kernels
+ *            read (four launches);
+ *         2: every final-token workgroup forms the decisions from the row results
+ *            (three launches).
+ * Both run the same arithmetic: the outputs are bit-identical.
+ * Errors: CMSD_ERR_ARG for any other mode.
+ */
+cmsd_status cmsd_set_pass_decisions(int32_t mode);
 
 /* Workspace cmsd_verify needs for `batch` sequences of up to `k_max` drafts over
  * `vocab`: per sequence, one 32-byte record per vocabulary slice (256 16-byte

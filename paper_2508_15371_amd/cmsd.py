@@ -80,6 +80,8 @@ def _load() -> C.CDLL:
     lib.cmsd_logit_pass_noalloc.restype = C.c_int
     lib.cmsd_set_row_shape.argtypes = [i32, i32]
     lib.cmsd_set_row_shape.restype = C.c_int
+    lib.cmsd_set_pass_decisions.argtypes = [i32]
+    lib.cmsd_set_pass_decisions.restype = C.c_int
     lib.cmsd_logit_pass_fused_workspace_bytes.argtypes = [i32, i32, i64]
     lib.cmsd_logit_pass_fused_workspace_bytes.restype = C.c_size_t
     lib.cmsd_status_string.argtypes = [C.c_int]
@@ -149,6 +151,13 @@ def cmsd_set_row_shape(threads: int = 0, ring_depth: int = 0) -> None:
     """Force the row kernels' workgroup size (64/128/256) and loads-in-flight depth
     (2/3); 0 restores the per-launch choice.  Process-wide."""
     _check("cmsd_set_row_shape", _lib.cmsd_set_row_shape(int(threads), int(ring_depth)))
+
+
+def cmsd_set_pass_decisions(mode: int = 0) -> None:
+    """Where cmsd_logit_pass forms each sequence's decisions: 0 chosen per call, 1 a
+    decision kernel's record (four launches), 2 in every final-token workgroup (three
+    launches).  Bit-identical outputs.  Process-wide."""
+    _check("cmsd_set_pass_decisions", _lib.cmsd_set_pass_decisions(int(mode)))
 
 
 def _events(evs):
@@ -381,8 +390,8 @@ def cmsd_logit_pass(draft_logits: torch.Tensor, target_logits: torch.Tensor, dra
     ``draft_logits`` [batch*k_max, V], ``target_logits`` [batch*(k_max+1), V] (same
     dtype), ``drafted`` int32 [batch*k_max], ``uniforms`` float32 [batch*(k_max+1)]
     (None in GREEDY mode).  ``row_events``: optional pair of recorded-once
-    ``torch.cuda.Event`` objects that the row-pass launch stamps with its own start and
-    end.  Returns the output tensors by name."""
+    ``torch.cuda.Event`` objects, recorded on the call's stream just before and just
+    after the row-pass launch.  Returns the output tensors by name."""
     outs = {"draft_stats": draft_stats, "draft_len": draft_len, "target_stats": target_stats,
             "n_accepted": n_accepted, "next_token": next_token}
     out, dst, tst, V, cp, dp, vp_ = _pass_args(draft_logits, target_logits, drafted, uniforms, batch, k_max, lambdas,

@@ -15,15 +15,16 @@
 //                   token's, the acceptance decision of that position, and the
 //                   row's slot in the workspace.
 //   k_final_parts   one wave per (sequence, vocabulary slice): first rejection from
-//                   the row slots (ballot), then fp64 slice partials of the
-//                   residual (or bonus) row.
+//                   the row slots (ballot; in cmsd_logit_pass the draft length and
+//                   accept tests too), then fp64 slice partials of the residual (or
+//                   bonus) row.
 //   k_final_sample  one workgroup per sequence: slice scan, then an exact in-slice
 //                   inverse-CDF locate that repeats the scan's sums bit for bit.
 //   k_row_pass      cmsd_logit_pass's row pass: drafter rows (as k_confidence) and
 //                   dense target rows (as k_target_rows, decisions deferred) in one
 //                   grid.
-//   k_pass_decide   cmsd_logit_pass, one wave per sequence: draft length, accept
-//                   tests and first rejection, written once for the final kernels.
+//   k_pass_decide   cmsd_logit_pass in GREEDY mode, one wave per sequence: draft
+//                   length, accept tests, first rejection and the final outputs.
 //   k_fused_pass    cmsd_logit_pass_fused, one launch for small batches: the row pass,
 //                   then the last row workgroup of each sequence (atomic count behind
 //                   a device fence) decides and samples with the same functions.
@@ -40,7 +41,6 @@
 // v_exp_f32; per-thread partial sums are fp32 over 32-element chunks, the
 // cross-thread combines and every decision-side formula are fp64.  Reductions have
 // a fixed order, so results are bit-reproducible run to run.
-#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -1292,9 +1292,11 @@ __device__ __forceinline__ SeqInfo seq_info(const VerifyArgs& a, int b, SeqInfo*
 }
 
 // seq_info of the single-call pass: wave 0 reads the sequence's row results, drafter
-// stats, drafted ids and uniforms (one round trip, k_max < 64), forms the draft length
-// and every accept test (as the separate calls would), and stores the draft length and
-// the target-row records.
+// stats, drafted ids and uniforms (one round trip, k_max < 64) and forms the draft
+// length and every accept test (as the separate calls would); with WRITE it also stores
+// the draft length and the target-row records.  The slots are only read, so every
+// workgroup of the final-token kernels forms the same decisions from them.
+template <bool WRITE>
 __device__ __forceinline__ SeqInfo seq_info_pass(const VerifyArgs& a, int b, SeqInfo* lds) {
   const int t = threadIdx.x, lane = t & 63;
   if (t < 64) {
@@ -1339,8 +1341,8 @@ __device__ __forceinline__ SeqInfo seq_info_pass(const VerifyArgs& a, int b, Seq
       q.msd = rl_f(dmx, c) * kLog2e;
       q.rho0 = (float)((double)(float)rl_d(sl.A, c) / (double)rl_f(dA, c));  // as from the verify slots
     }
-    if (lane == 0) a.klen_out[b] = kb;
-    if (lane <= K) {
+    if (WRITE && lane == 0) a.klen_out[b] = kb;
+    if (WRITE && lane <= K) {
       cmsd_target_stats res{};
       res.max_logit = sl.m;
       res.sum_exp = (float)sl.A;
@@ -1364,6 +1366,12 @@ __device__ __forceinline__ SeqInfo seq_info_pass(const VerifyArgs& a, int b, Seq
   return r;
 }
 
+// Where the final-token kernels of cmsd_logit_pass find their sequence's decisions:
+// in a record that k_pass_decide wrote (large launches), or formed by each of their
+// workgroups from the row slots (small launches: one launch fewer).  Verify is the
+// separate cmsd_verify, whose decisions come from its own row slots (seq_info).
+enum class Src { Verify, Record, Inline };
+
 // The sequence record of the single-call pass sits over the first two row slots of the
 // sequence (k_max >= 1), which k_pass_decide has read before it writes the record.
 static_assert(sizeof(SeqInfo) <= 2 * sizeof(PassSlot), "a sequence record fits two row slots");
@@ -1372,14 +1380,15 @@ __device__ __forceinline__ SeqInfo* pass_info(const VerifyArgs& a, int b) {
 }
 
 // Decisions of the single-call pass, one wave per sequence: draft length, accept
-// tests, first rejection (seq_info_pass); the outputs of an invalid sequence and, in
-// GREEDY mode, the final outputs; and the sequence record that the final-token
-// kernels read in one load instead of repeating the decisions per slice.
+// tests, first rejection (seq_info_pass), the draft length and target-row records;
+// the outputs of an invalid sequence and, in GREEDY mode, the final outputs; and the
+// sequence record that the final-token kernels read in one load instead of repeating
+// the decisions per slice.
 __global__ __launch_bounds__(64) void k_pass_decide(VerifyArgs a) {
   __shared__ SeqInfo s_q;
   const int b = blockIdx.x;
   if (b >= a.B) return;
-  const SeqInfo q = seq_info_pass(a, b, &s_q);
+  const SeqInfo q = seq_info_pass<true>(a, b, &s_q);
   if (threadIdx.x == 0) {
     *pass_info(a, b) = q;
     if (q.nacc < 0) {
@@ -1444,7 +1453,7 @@ __device__ __forceinline__ void parts_wave(const T* trow, const T* drow, const G
   }
 }
 
-template <typename T, bool PASS>
+template <typename T, Src SRC>
 __global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, int SW, SlicePart* __restrict__ ws) {
   constexpr int BD = kPartBD;
   __shared__ double sd[kSubPerWG * 4 * (BD / 64)];
@@ -1452,7 +1461,9 @@ __global__ __launch_bounds__(kPartBD) void k_final_parts(VerifyArgs a, int S, in
   const int t = threadIdx.x;
   const int b = blockIdx.x / SW, sl0 = (blockIdx.x % SW) * kSubPerWG;
   if (b >= a.B) return;
-  const SeqInfo q = PASS ? *pass_info(a, b) : seq_info(a, b, &s_q);
+  const SeqInfo q = SRC == Src::Record   ? *pass_info(a, b)
+                    : SRC == Src::Inline ? seq_info_pass<false>(a, b, &s_q)
+                                         : seq_info(a, b, &s_q);
   if (q.nacc < 0) return;
   const bool resid = q.nacc < q.kb;
   const T* trow = reinterpret_cast<const T*>(a.target) + q.tr * a.tstride;
@@ -1702,7 +1713,7 @@ __device__ __forceinline__ int sample_from_parts(const T* trow, const T* drow, i
   return y;
 }
 
-template <typename T, bool PASS>
+template <typename T, Src SRC>
 __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S, const SlicePart* __restrict__ ws) {
   constexpr int BD = kSampleBD;
   __shared__ double sd[2 * (BD / 64)];
@@ -1713,8 +1724,10 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
   const int t = threadIdx.x;
   const int b = blockIdx.x;
   if (b >= a.B) return;
-  const SeqInfo q = PASS ? *pass_info(a, b) : seq_info(a, b, &s_q);
-  if (PASS && (q.nacc < 0 || a.mode == CMSD_MODE_GREEDY)) return;  // written by k_pass_decide
+  const SeqInfo q = SRC == Src::Record   ? *pass_info(a, b)
+                    : SRC == Src::Inline ? seq_info_pass<true>(a, b, &s_q)
+                                         : seq_info(a, b, &s_q);
+  if (SRC == Src::Record && (q.nacc < 0 || a.mode == CMSD_MODE_GREEDY)) return;  // written by k_pass_decide
   if (q.nacc < 0) {
     if (t == 0) {
       a.n_acc[b] = -1;
@@ -1772,7 +1785,7 @@ __device__ __forceinline__ void fused_tail(const VerifyArgs& a, int b, int S, Sl
   __shared__ double s_sc[3];
   __shared__ int s_y;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const SeqInfo q = seq_info_pass(a, b, &s_q);
+  const SeqInfo q = seq_info_pass<true>(a, b, &s_q);
   if (q.nacc < 0 || a.mode == CMSD_MODE_GREEDY) {
     if (t == 0) {
       a.n_acc[b] = q.nacc < 0 ? -1 : q.nacc;
@@ -1983,15 +1996,14 @@ void launch_target_rows(int bd, const VerifyArgs& a, hipStream_t st) {
     launch_target_rows_d<T, CMSD_STREAM_DEPTH>(bd, a, st);
 }
 
-// The joint row pass.  With events, the launch goes through hipExtLaunchKernel, which
-// stamps them with the kernel's own start and end (the caller times the launch alone).
+// The joint row pass.  With events, they are recorded on the stream just before and
+// just after the launch, so the caller can time the launch alone.
 template <typename K>
 void launch_rows(K kernel, int64_t rows, int bd, const VerifyArgs& a, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
   const dim3 grid((unsigned)rows), block((unsigned)bd);
-  if (e0)
-    hipExtLaunchKernelGGL(kernel, grid, block, 0, st, e0, e1, 0, a);
-  else
-    hipLaunchKernelGGL(kernel, grid, block, 0, st, a);
+  if (e0) hipEventRecord(e0, st);
+  hipLaunchKernelGGL(kernel, grid, block, 0, st, a);
+  if (e0) hipEventRecord(e1, st);
 }
 template <typename T, int DEPTH>
 void launch_row_pass_d(int bd, const VerifyArgs& a, int64_t rows, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
@@ -2128,9 +2140,29 @@ cmsd_status bind_pass_workspace(VerifyArgs& a, void* workspace, size_t workspace
   return CMSD_OK;
 }
 
+// The final-token pair of cmsd_logit_pass, its decisions found as SRC says.
+template <typename T, Src SRC>
+void launch_final(const VerifyArgs& a, int S, int SW, SlicePart* ws, hipStream_t st) {
+  const unsigned gp = (unsigned)((int64_t)a.B * SW);
+  hipLaunchKernelGGL((k_final_parts<T, SRC>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
+  hipLaunchKernelGGL((k_final_sample<T, SRC>), dim3((unsigned)a.B), dim3(kSampleBD), 0, st, a, S, ws);
+}
+
+// Whether the final-token workgroups of cmsd_logit_pass form their sequence's decisions
+// themselves instead of reading k_pass_decide's record: up to 32 slice waves per compute
+// unit the launch saved outweighs the repeated decisions (c2, c3, a 152k vocabulary);
+// c4's 63 slices x 256 sequences (63 waves per unit) keep the decision kernel.
+// cmsd_set_pass_decisions forces either (0 = chosen per call, 1 = record, 2 = inline).
+std::atomic<int> g_pass_decisions{0};
+bool inline_decisions(unsigned slice_waves) {
+  if (const int m = g_pass_decisions.load(std::memory_order_relaxed)) return m == 2;
+  return slice_waves <= 32u * (unsigned)device_cus();
+}
+
 // The launches of cmsd_logit_pass on a bound workspace: the joint row pass (bracketed
-// by the caller's events, if any), the per-sequence decisions, then the final-token
-// pair (not in GREEDY mode, whose final token is the row's top token).
+// by the caller's events, if any), then either the final-token pair forming the
+// decisions in its workgroups (small launches), or the per-sequence decisions followed
+// by the final-token pair (not in GREEDY mode, whose final token is the row's top token).
 cmsd_status enqueue_logit_pass(const VerifyArgs& a, int32_t dtype, void* workspace, hipEvent_t e0, hipEvent_t e1,
                                hipStream_t st) {
   const int es = dtype == CMSD_F32 ? 4 : 2;
@@ -2144,15 +2176,19 @@ cmsd_status enqueue_logit_pass(const VerifyArgs& a, int32_t dtype, void* workspa
     launch_row_pass<float>(bd, a, drows + trows, st, e0, e1);
   else
     launch_row_pass<Bf16>(bd, a, drows + trows, st, e0, e1);
+  if (a.mode != CMSD_MODE_GREEDY && inline_decisions(gp)) {
+    if (dtype == CMSD_F32)
+      launch_final<float, Src::Inline>(a, S, SW, ws, st);
+    else
+      launch_final<Bf16, Src::Inline>(a, S, SW, ws, st);
+    return launched();
+  }
   hipLaunchKernelGGL(k_pass_decide, dim3((unsigned)a.B), dim3(64), 0, st, a);
   if (a.mode == CMSD_MODE_GREEDY) return launched();
-  if (dtype == CMSD_F32) {
-    hipLaunchKernelGGL((k_final_parts<float, true>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
-    hipLaunchKernelGGL((k_final_sample<float, true>), dim3((unsigned)a.B), dim3(kSampleBD), 0, st, a, S, ws);
-  } else {
-    hipLaunchKernelGGL((k_final_parts<Bf16, true>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
-    hipLaunchKernelGGL((k_final_sample<Bf16, true>), dim3((unsigned)a.B), dim3(kSampleBD), 0, st, a, S, ws);
-  }
+  if (dtype == CMSD_F32)
+    launch_final<float, Src::Record>(a, S, SW, ws, st);
+  else
+    launch_final<Bf16, Src::Record>(a, S, SW, ws, st);
   return launched();
 }
 
@@ -2204,7 +2240,7 @@ const char* cmsd_status_string(cmsd_status s) {
   return "unknown status";
 }
 
-int32_t cmsd_version(void) { return (1 << 16) | 5; }
+int32_t cmsd_version(void) { return (1 << 16) | 6; }
 
 size_t cmsd_draft_sample_workspace_bytes(int64_t n_rows, int64_t vocab) {
   if (n_rows <= 0 || n_rows > INT32_MAX || vocab < 2 || vocab > INT32_MAX) return 0;
@@ -2329,13 +2365,13 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   if (dtype == CMSD_F32) {
     launch_target_rows<float>(bd, a, st);
     if (a.mode != CMSD_MODE_GREEDY)
-      hipLaunchKernelGGL((k_final_parts<float, false>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
-    hipLaunchKernelGGL((k_final_sample<float, false>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
+      hipLaunchKernelGGL((k_final_parts<float, Src::Verify>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
+    hipLaunchKernelGGL((k_final_sample<float, Src::Verify>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   } else {
     launch_target_rows<Bf16>(bd, a, st);
     if (a.mode != CMSD_MODE_GREEDY)
-      hipLaunchKernelGGL((k_final_parts<Bf16, false>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
-    hipLaunchKernelGGL((k_final_sample<Bf16, false>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
+      hipLaunchKernelGGL((k_final_parts<Bf16, Src::Verify>), dim3(gp), dim3(kPartBD), 0, st, a, S, SW, ws);
+    hipLaunchKernelGGL((k_final_sample<Bf16, Src::Verify>), dim3((unsigned)batch), dim3(kSampleBD), 0, st, a, S, ws);
   }
   return launched();
 }
@@ -2378,6 +2414,12 @@ cmsd_status cmsd_logit_pass_noalloc(const void* draft_logits, int64_t draft_stri
   e = bind_pass_workspace(a, ws, (size_t)CMSD_STATIC_SCRATCH_BYTES, need);
   if (e != CMSD_OK) return e;
   return enqueue_logit_pass(a, dtype, ws, nullptr, nullptr, as_stream(stream));
+}
+
+cmsd_status cmsd_set_pass_decisions(int32_t mode) {
+  if (mode < 0 || mode > 2) return CMSD_ERR_ARG;
+  g_pass_decisions.store(mode, std::memory_order_relaxed);
+  return CMSD_OK;
 }
 
 cmsd_status cmsd_set_row_shape(int32_t threads, int32_t ring_depth) {

@@ -17,11 +17,11 @@ def test_exports_every_declared_symbol():
                          "cmsd_draft_sample", "cmsd_draft_sample_workspace_bytes", "cmsd_status_string",
                          "cmsd_version", "cmsd_logit_pass", "cmsd_logit_pass_fused",
                          "cmsd_logit_pass_fused_workspace_bytes", "cmsd_logit_pass_noalloc",
-                         "cmsd_set_row_shape"}
+                         "cmsd_set_row_shape", "cmsd_set_pass_decisions"}
     lib = cm.lib()
     for s in syms:
         assert hasattr(lib, s), s
-    assert lib.cmsd_version() == (1 << 16) | 5
+    assert lib.cmsd_version() == (1 << 16) | 6
     assert lib.cmsd_status_string(0) == b"ok"
     assert lib.cmsd_status_string(1) == b"invalid argument"
     assert lib.cmsd_status_string(4) == b"problem larger than the static scratch"
@@ -46,6 +46,16 @@ def test_set_row_shape(threads, depth, want):
         assert lib.cmsd_set_row_shape(threads, depth) == want
     finally:
         assert lib.cmsd_set_row_shape(0, 0) == cm.CMSD_OK
+
+
+@pytest.mark.parametrize("mode,want", [(0, cm.CMSD_OK), (1, cm.CMSD_OK), (2, cm.CMSD_OK),
+                                       (-1, cm.CMSD_ERR_ARG), (3, cm.CMSD_ERR_ARG)])
+def test_set_pass_decisions(mode, want):
+    lib = cm.lib()
+    try:
+        assert lib.cmsd_set_pass_decisions(mode) == want
+    finally:
+        assert lib.cmsd_set_pass_decisions(0) == cm.CMSD_OK
 
 
 def _conf(**kw):

@@ -105,6 +105,53 @@ def test_bitwise_equal_to_separate_calls(cm, mode):
         assert torch.equal(out[k].view(torch.int32), ref.view(torch.int32)), k
 
 
+def _forced_decisions(cm, mode_forced, fn):
+    cm.cmsd_set_pass_decisions(mode_forced)
+    try:
+        out = fn()
+        torch.cuda.synchronize()
+        return {k: v.clone() for k, v in out.items() if isinstance(v, torch.Tensor)}
+    finally:
+        cm.cmsd_set_pass_decisions(0)
+
+
+@pytest.mark.parametrize("adaptive", [False, True])
+@pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY])
+@pytest.mark.parametrize("name", ["c2", "c3", "c4"])
+def test_decision_paths_bitwise_equal(cm, name, mode, adaptive):
+    # the decisions formed in every final-token workgroup (three launches) and read from
+    # the decision kernel's record (four launches) are the same arithmetic: bit-equal
+    # outputs; c2 and c3 choose the first by default, c4 the second
+    cfg = W.CONFIGS[name]
+    d = Hn.workload(name)
+    run = lambda: _pass(cm, d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"], cfg.B, cfg.k_max,
+                        mode, adaptive)[0]
+    rec = _forced_decisions(cm, 1, run)
+    inl = _forced_decisions(cm, 2, run)
+    auto = run()
+    torch.cuda.synchronize()
+    for k in ("draft_stats", "draft_len", "target_stats", "n_accepted", "next_token"):
+        assert torch.equal(rec[k].view(torch.int32), inl[k].view(torch.int32)), k
+        assert torch.equal(rec[k].view(torch.int32), auto[k].view(torch.int32)), k
+
+
+@pytest.mark.parametrize("forced", [1, 2])
+def test_decision_paths_invalid_sequence(cm, forced):
+    V, K, B = 500, 4, 3
+    g = np.random.default_rng(8)
+    zd, zt, dr, u = _case(g, B, K, V, "f32")
+    dr[1, 3] = V
+    dev = torch.device("cuda:0")
+    out = _forced_decisions(cm, forced, lambda: _pass(
+        cm, Hn.to_device(zd, "f32", dev), Hn.to_device(zt, "f32", dev), torch.from_numpy(dr.reshape(-1)).to(dev),
+        torch.from_numpy(u.reshape(-1)).to(dev), B, K, O.MODE_CM)[0])
+    n_acc = out["n_accepted"].cpu().numpy()
+    nxt = out["next_token"].cpu().numpy()
+    ts = Hn.tstats_np(out["target_stats"])
+    assert n_acc[1] == -1 and nxt[1] == -1 and ts["acc"][1 * (K + 1) + 3] == -2
+    assert n_acc[0] >= 0 and n_acc[2] >= 0 and nxt[0] >= 0 and nxt[2] >= 0
+
+
 def test_repeat_bitwise_identical(cm):
     cfg = W.CONFIGS["c2"]
     d = Hn.workload("c2")
@@ -248,8 +295,8 @@ def test_empty_batch(cm):
 
 
 def test_row_events_time_the_row_pass(cm):
-    # events handed to the call are stamped with the row-pass kernel's start and end on
-    # the call's stream, and leave the outputs unchanged
+    # events handed to the call are recorded around the row-pass launch on the call's
+    # stream, and leave the outputs unchanged
     cfg = W.CONFIGS["c2"]
     d = Hn.workload("c2")
     ref, _ = _pass(cm, d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"], cfg.B, cfg.k_max, O.MODE_CM)

@@ -23,7 +23,7 @@ int main(void) {
   cmsd_row_stats st;
   float x = 0.f;
   int32_t k = 0, off = 0;
-  if (cmsd_version() != ((1 << 16) | 5)) bad |= 1;
+  if (cmsd_version() != ((1 << 16) | 6)) bad |= 1;
   if (strcmp(cmsd_status_string(CMSD_OK), "ok") != 0) bad |= 2;
   if (cmsd_verify_workspace_bytes(0, 8, 1000) != 0) bad |= 4;
   if (cmsd_verify_workspace_bytes(4, 8, 1000) == 0) bad |= 8;
@@ -48,6 +48,7 @@ int main(void) {
                               &k, NULL, &k, &k, NULL) != CMSD_ERR_ARG) bad |= 4096;  /* target_stats NULL */
   if (cmsd_verify_workspace_bytes(4096, 16, 128256) <= CMSD_STATIC_SCRATCH_BYTES) bad |= 8192;
   if (cmsd_set_row_shape(48, 0) != CMSD_ERR_ARG || cmsd_set_row_shape(0, 0) != CMSD_OK) bad |= 16384;
+  if (cmsd_set_pass_decisions(3) != CMSD_ERR_ARG || cmsd_set_pass_decisions(0) != CMSD_OK) bad |= 32768;
   printf("bad=%d\n", bad);
   return bad;
 }
