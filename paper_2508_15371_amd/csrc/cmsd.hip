@@ -570,9 +570,10 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
     }, [&](const uint4 (&raw)[U], int64_t k) {
       float f[N];
 #pragma unroll
-      for (int u = 0; u < U; ++u) E::unpack(E::clamp_masked(raw[u]), f + u * VEC);
-#pragma unroll
-      for (int u = 0; u < U; ++u) probe.add(raw[u]);
+      for (int u = 0; u < U; ++u) {
+        probe.add(raw[u]);
+        E::unpack(E::clamp_masked(raw[u]), f + u * VEC);
+      }
       conf_chunk<N, false, VAR>(s, f, 0xffffffffu, int(k + 1));
       if (KEEP) {
         const bool up = s.gid == int(k + 1);
@@ -1997,13 +1998,14 @@ void launch_target_rows(int bd, const VerifyArgs& a, hipStream_t st) {
 }
 
 // The joint row pass.  With events, they are recorded on the stream just before and
-// just after the launch, so the caller can time the launch alone.
+// just after the launch, so the caller can time the launch alone.  A failed record
+// stays the thread's last HIP error, which the call's launched() reports.
 template <typename K>
 void launch_rows(K kernel, int64_t rows, int bd, const VerifyArgs& a, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
   const dim3 grid((unsigned)rows), block((unsigned)bd);
-  if (e0) hipEventRecord(e0, st);
+  if (e0) (void)hipEventRecord(e0, st);
   hipLaunchKernelGGL(kernel, grid, block, 0, st, a);
-  if (e0) hipEventRecord(e1, st);
+  if (e0) (void)hipEventRecord(e1, st);
 }
 template <typename T, int DEPTH>
 void launch_row_pass_d(int bd, const VerifyArgs& a, int64_t rows, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
