@@ -11,7 +11,7 @@ sequences, k_max=16, V=128256, bf16 (the largest configuration; inputs 2.17 GB).
 
 Inputs are resident in HBM before timing; workloads smaller than 512 MiB rotate copies of
 their logits between steps (``--no-rotate`` reuses one).  HIP events around the roofline
-kernel in every 64th timed step give its achieved bandwidth (denser event markers slow
+kernel in the middle step of every 64 timed steps give its achieved bandwidth (denser event markers slow
 the host-bound one-sequence steps: b1 at one step in 16 went from 23 to 100 us per step
 in some runs); after the timed region the
 bench times each of the three calls separately, then a bare read of the roofline
@@ -44,11 +44,11 @@ PEAK_HBM_GBS = 8000.0   # MI355X HBM3E
 # device copy (x2.0 and x1.0).  Valid only for the kernel code they were taken on
 # (kernel_code_hash(): sha256 prefix of the .hip file's code without comments);
 # otherwise "traffic" is reported null.
-TRAFFIC = {"kernel_code_sha256_16": "e88a974d95bfa062",
+TRAFFIC = {"kernel_code_sha256_16": "7eb0674dec29c09f",
            "k_row_pass_c4": 2170.52e6 + 0.270e6, "k_confidence_c4": 1052.91e6 + 0.131e6,
-           "k_confidence_c5": 524.73e6 + 0.262e6, "k_confidence_c5m": 524.73e6 + 0.262e6,
-           "k_row_pass_c3": 112.82e6 + 0.035e6, "k_row_pass_c2": 9.13e6 + 0.004e6,
-           "k_row_pass_v152k": 331.74e6 + 0.035e6,
+           "k_confidence_c5": 524.72e6 + 0.262e6, "k_confidence_c5m": 524.72e6 + 0.262e6,
+           "k_row_pass_c3": 112.85e6 + 0.035e6, "k_row_pass_c2": 9.11e6 + 0.004e6,
+           "k_row_pass_v152k": 331.73e6 + 0.035e6,
            "profile": "profiles/<workload>_cm_logit_pass.md"}
 
 
@@ -373,8 +373,10 @@ def main() -> int:
     # kernel (the joint row pass of cmsd_logit_pass, or k_confidence of group 0 on the
     # three-call path) in every `event_every`-th step; each event marker costs time
     # between kernels (and on short steps host time), so no other kernel is bracketed.
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] if k % args.event_every == 0 else None
-          for k in range(args.steps)]
+    # (the middle step of each block of event_every steps, so never the first timed step,
+    # which starts from an idle GPU)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)]
+          if k % args.event_every == min(args.event_every, args.steps) // 2 else None for k in range(args.steps)]
     for e in ev:
         if e is not None:      # the binding hands the library events that exist
             e[0].record(main)
