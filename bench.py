@@ -49,6 +49,7 @@ TRAFFIC = {"kernel_code_sha256_16": "7eb0674dec29c09f",
            "k_confidence_c5": 524.72e6 + 0.262e6, "k_confidence_c5m": 524.72e6 + 0.262e6,
            "k_row_pass_c3": 112.85e6 + 0.035e6, "k_row_pass_c2": 9.11e6 + 0.004e6,
            "k_row_pass_v152k": 331.73e6 + 0.035e6,
+           "k_row_pass_c4f": 4340.34e6 + 0.270e6,
            "profile": "profiles/<workload>_cm_logit_pass.md"}
 
 
@@ -234,7 +235,7 @@ def main() -> int:
     # ~3 % slower), so the default warms up for 100 steps and times 500 (~0.2 s on c4)
     ap.add_argument("--steps", type=int, default=500)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--workload", default="c4", choices=["tiny", "b1", "c2", "c3", "c4", "c5", "c5m", "v152k"])
+    ap.add_argument("--workload", default="c4", choices=["tiny", "b1", "c2", "c3", "c4", "c4f", "c5", "c5m", "v152k"])
     ap.add_argument("--mode", default="cm", choices=["cm", "standard"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--path", default="auto", choices=["auto", "pass", "fused", "calls"],

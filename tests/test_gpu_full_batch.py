@@ -1,5 +1,6 @@
 """Whole-batch GPU parity on the largest workloads and the masked one: every
-sequence of c3 (64), c4 (256), c5 (512) and c5m (512, c5 with -inf logits) in every mode,
+sequence of c3 (64), c4 (256), c4f (256, c4's recipe in fp32), c5 (512) and c5m (512, c5 with
+-inf logits) in every mode,
 through the three calls (cmsd_confidence, cmsd_draft_len, cmsd_verify) and through
 cmsd_logit_pass in both verification lengths, against the oracle.  Every drafter row's record, every draft length (end to end, with its floor
 slack), every target-row record, accept decision, prefix and final token is compared
@@ -42,7 +43,7 @@ def _report(name, path, mode, t, n_acc, k, seqs):
 
 
 @pytest.mark.parametrize("mode", MODES)
-@pytest.mark.parametrize("name", ["c3", "c4", "c5", "c5m"])
+@pytest.mark.parametrize("name", ["c3", "c4", "c4f", "c5", "c5m"])
 def test_full_batch_three_calls(mods, name, mode):
     cmsd, pipeline = mods
     print(f"[full batch] start {name} three calls mode={mode}", flush=True)
@@ -81,7 +82,7 @@ def test_full_batch_three_calls(mods, name, mode):
 
 @pytest.mark.parametrize("adaptive", [False, True])
 @pytest.mark.parametrize("mode", MODES)
-@pytest.mark.parametrize("name", ["c3", "c4", "c5", "c5m"])
+@pytest.mark.parametrize("name", ["c3", "c4", "c4f", "c5", "c5m"])
 def test_full_batch_logit_pass(mods, name, mode, adaptive):
     cmsd, _ = mods
     print(f"[full batch] start {name} cmsd_logit_pass mode={mode} adaptive={adaptive}", flush=True)

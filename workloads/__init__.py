@@ -36,6 +36,8 @@ drafter and verifier outputs):
   ``[B, k_max+1, V]`` (bonus row stored at slot k_max) and packed afterwards.
 * ``v152k``: a sweep point, not one of the five: B=64, k_max=8, V=152064 (the top
   of the metric's vocabulary range), bf16, with c2's row recipe.
+* ``c4f``  : c4's recipe stored in fp32 (its own seeded streams, no bf16 rounding):
+  the headline shape for the fp32 row kernels.
 * ``c5m``  : c5 with masked logits: every drafter row and the target row of the same
   position set -inf on one seeded mask of the vocabulary (the last 128 tokens, as
   padding of a vocabulary rounded up, plus 3 % of the others at random, as a decoding
@@ -116,6 +118,8 @@ CONFIGS = {
     "b1": Config("b1", 6, 1, 8, 32000, "bf16", style="c2"),
     # c5 with masked logits (vocabulary padding and a decoding constraint)
     "c5m": Config("c5m", 7, 512, 16, 32000, "bf16", ragged=True, style="c5", masked=True),
+    # c4's rows in fp32 (the fp32 row kernels at the headline shape)
+    "c4f": Config("c4f", 8, 256, 16, 128256, "f32", style="c4"),
 }
 
 _MASK_TAIL = 128       # masked tokens at the end of the vocabulary
