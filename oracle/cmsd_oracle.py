@@ -21,10 +21,14 @@ slack is below 1e-6 is an allowed, counted exception; any other difference is a
 failure.
 
 Parity status: every function here is pinned by the ``-m "not gpu"`` tests in
-``tests/test_oracle_*.py`` except the three choices marked "parity unpinned"
-below (how the confidence gate combines with the stochastic test in CM mode,
-which uniform each decision consumes, and the zero-residual fallback), which the
-paper does not determine; for those only internal consistency is tested.
+``tests/test_oracle_*.py`` and ``tests/test_golden.py``.  Three behaviours marked
+"reading" below are choices the paper does not determine; each is pinned to its
+reading: the OR of the confidence gate with the stochastic test in CM mode (CM
+contains STANDARD, CM with beta = 0 equals it, and the AND of the two fails the
+tests), the final sample's own uniform (exact standard speculative sampling over
+the whole uniform lattice fails if the rejecting uniform is reused, which biases
+the sample), and the zero-residual fallback (a hand-worked case whose residual is
+identically zero).
 """
 from __future__ import annotations
 
@@ -234,7 +238,7 @@ def accept_position(z_t: np.ndarray, rs_t: RowStats, z_d: np.ndarray, rs_d: RowS
     * Adaptive threshold tau_t = tau_base + gamma * (1 - C_t), Sec. III.B(c).
     * Gate = top-beta inclusion AND gap <= tau_t, Sec. III.B(c) "modified
       verification rule".
-    * Reading (parity unpinned): the paper's gate relaxes acceptance, so in CM mode
+    * Reading (the paper does not fix it): the paper's gate relaxes acceptance, so in CM mode
       a position is accepted when the stochastic test passes OR the gate passes;
       in STANDARD mode only the stochastic test applies (standard speculative
       sampling).
@@ -279,9 +283,9 @@ def prefix_length(flags) -> int:
 
 def residual_pmf(z_t: np.ndarray, rs_t: RowStats, z_d: np.ndarray, rs_d: RowStats) -> np.ndarray:
     """Unnormalised residual max(0, p_t - p_d) after a rejection (standard
-    speculative sampling).  Reading (parity unpinned): if it is identically zero
-    (possible only through rounding, since a rejection implies p_t != p_d), p_t
-    is used instead."""
+    speculative sampling).  Reading (the paper does not fix it): if it is
+    identically zero (through rounding, or when drafter and target rows are equal
+    and the draft was a token both rows mask), p_t is used instead."""
     p_t = np.exp(z_t - rs_t.m) / rs_t.A
     p_d = np.exp(z_d - rs_d.m) / rs_d.A
     q = np.maximum(0.0, p_t - p_d)
@@ -314,8 +318,8 @@ def final_sample(z_t_rows: list, rs_t_rows: list, z_d_rows: list, rs_d_rows: lis
     """The token emitted after the accepted prefix: on a rejection at position
     c = n_acc < k_b, a sample from the residual of target and drafter rows c;
     when all k_b drafts are accepted, a sample from the target row k_b (the row
-    scored after the last draft).  Reading (parity unpinned): this sample uses
-    the sequence's own final uniform (slot k_b), not the rejecting one."""
+    scored after the last draft).  Reading (the paper does not fix it): this sample
+    uses the sequence's own final uniform (slot k_b), not the rejecting one."""
     if n_acc < k_b:
         q = residual_pmf(z_t_rows[n_acc], rs_t_rows[n_acc], z_d_rows[n_acc], rs_d_rows[n_acc])
     else:

@@ -43,6 +43,8 @@ MUTATIONS = [
      "residual with the target's normaliser on the drafter row"),
     ("return int(np.argmax(z_t_rows[min(n_acc, k_b)]))", "return int(np.argmax(z_t_rows[k_b]))",
      "GREEDY final token from the bonus row after a rejection"),
+    ("k_b, c, float(uniforms[k_b]))", "k_b, c, float(uniforms[min(c, k_b)]))",
+     "final sample reuses the rejecting position's uniform"),
     ("    if not np.any(q > 0):\n        return p_t\n", "", "no fallback for a zero residual"),
     ("    if not np.any(q > 0):\n        return p_t\n", "    if not np.any(q > 0):\n        return np.ones_like(p_t)\n",
      "uniform fallback for a zero residual"),
