@@ -999,8 +999,11 @@ __device__ __forceinline__ void target_row(const VerifyArgs& a, int64_t q) {
   __shared__ float sf[BD / 64];
   __shared__ int si[BD / 64];
   const int t = threadIdx.x;
-  const int b = int(q / (a.k_max + 1));
-  const int i = int(q - (int64_t)b * (a.k_max + 1));
+  // cmsd_verify's grid is position-major (q = i*B + b): every sequence's scored rows
+  // (i <= k_b) come before the positions past the shorter drafts, whose workgroups only
+  // read the draft length and exit; the single-call pass numbers its dense rows b*(k_max+1)+i
+  const int b = PASS ? int(q / (a.k_max + 1)) : int(q % a.B);
+  const int i = PASS ? int(q - (int64_t)b * (a.k_max + 1)) : int(q / a.B);
   const bool in_k = i < a.k_max;
   const int64_t drow = (int64_t)b * a.k_max + (in_k ? i : 0);
   int64_t r = q;
