@@ -89,6 +89,8 @@ template <> struct Elem<float> {
   // -inf (and only values below kMaskedLogit, outside the logit range) to kMaskedLogit:
   // an unsigned min on the raw bits, since negative floats order by magnitude there
   __device__ static uint32_t clamp_word(uint32_t w) { return w < 0xff000000u ? w : 0xff000000u; }
+  // the clamp value (kMaskedLogit) in every element: padding that adds exactly 0 to the sums
+  __device__ static uint4 raw_masked() { return make_uint4(0xff000000u, 0xff000000u, 0xff000000u, 0xff000000u); }
   __device__ static uint4 clamp_masked(const uint4& v) {
     return make_uint4(clamp_word(v.x), clamp_word(v.y), clamp_word(v.z), clamp_word(v.w));
   }
@@ -120,7 +122,8 @@ template <> struct Elem<Bf16> {
   __device__ static uint32_t clamp_word(uint32_t w) {
     const u16x2 lim = {0xff00, 0xff00};
     return __builtin_bit_cast(uint32_t, __builtin_elementwise_min(__builtin_bit_cast(u16x2, w), lim));
-  }
+  }  __device__ static uint4 raw_masked() { return make_uint4(0xff00ff00u, 0xff00ff00u, 0xff00ff00u, 0xff00ff00u); }
+
   __device__ static uint4 clamp_masked(const uint4& v) {
     return make_uint4(clamp_word(v.x), clamp_word(v.y), clamp_word(v.z), clamp_word(v.w));
   }
@@ -489,25 +492,28 @@ __device__ void rescan_chunk(const T* row, const Geom& g, int64_t nr, int cid, f
 // ----------------------------------------------------------------------------- K1 confidence
 struct ConfArgs {
   float l_ent, l_margin, l_soft, beta_m;
-  double lnV;  // ln(vocab)
+  double inv_lnV;   // 1 / ln(vocab)
+  double inv_soft;  // 1 / (1 - 1/vocab), the softmax margin's normaliser
 };
 
 // The drafter-row record from the row's reductions: max m, second value z2 (the
 // largest value other than the first occurrence of m; -inf with one finite logit),
 // A = sum 2^(z log2e - m log2e) and T = sum of 2^x x over the same terms.
 __device__ __forceinline__ cmsd_row_stats row_stats_record(float m, float z2, double A, double Tsum, uint32_t flags,
-                                                           int top1, int64_t V, const ConfArgs& a) {
-  const double Vd = (double)V;
+                                                           int top1, const ConfArgs& a) {
+  // one fp64 division per row (1/A) and one for the sigmoid; the per-call constants come
+  // as reciprocals, so the row's wave spends little time on this dependent chain
+  const double invA = 1.0 / A;
   const double Tn = Tsum * kLn2;
-  double H = (double)log1pf((float)(A - 1.0)) - Tn / A;  // ln A = log1p(A - 1), A - 1 exact in fp64
+  double H = (double)log1pf((float)(A - 1.0)) - Tn * invA;  // ln A = log1p(A - 1), A - 1 exact in fp64
   H = H < 0.0 ? 0.0 : H;
   const double dm = (double)m, dz2 = (double)z2;
   const double margin = z2 == -INFINITY ? INFINITY : dm - dz2;
-  const double msoft = z2 == -INFINITY ? 1.0 / A : (double)(-expm1f((float)(dz2 - dm))) / A;
-  const double c_ent = 1.0 - H / a.lnV;
+  const double msoft = z2 == -INFINITY ? invA : (double)(-expm1f((float)(dz2 - dm))) * invA;
+  const double c_ent = 1.0 - H * a.inv_lnV;
   const double tm = (double)a.beta_m * margin;
   const double c_m = tm == INFINITY ? 1.0 : 1.0 / (1.0 + (double)expf((float)-tm));
-  const double c_s = fmin(1.0, msoft / (1.0 - 1.0 / Vd));
+  const double c_s = fmin(1.0, msoft * a.inv_soft);
   const double C = (double)a.l_ent * c_ent + (double)a.l_margin * c_m + (double)a.l_soft * c_s;
   cmsd_row_stats o;
   o.max_logit = m;
@@ -586,8 +592,10 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
         }
       }
     });
-    // partial round: whole vectors clamped and probed as in the full rounds (lanes past
-    // the row hold -inf padding, which the guarded sums skip, and show the probe zeros)
+    // partial round: whole vectors clamped and probed as in the full rounds; lanes past
+    // the row show the probe zeros and hold the clamp value, which adds exactly 0 to A
+    // and T as a masked logit does, so the round takes the unguarded arithmetic (the
+    // variance moments, which must not see padding, keep the guarded form and -inf)
     const int64_t rb = nr * per_round;
     if (rb < g.nvec) {
       float f[N];
@@ -606,9 +614,9 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
       for (int u = 0; u < U; ++u) {
         probe.add(pv[u]);
         const bool in = (valid >> (u * VEC)) & 1u;
-        E::unpack(in ? E::clamp_masked(pv[u]) : E::raw_ninf(), f + u * VEC);
+        E::unpack(in ? E::clamp_masked(pv[u]) : (VAR ? E::raw_ninf() : E::raw_masked()), f + u * VEC);
       }
-      conf_chunk<N, true, VAR>(s, f, valid, int(nr + 1));
+      conf_chunk<N, VAR, VAR>(s, f, valid, int(nr + 1));
     }
     const int64_t tail0 = g.head + g.nvec * VEC;
     if (t < g.tail) conf_one<VAR>(s, clamp1(E::load(row + tail0 + t)), int(nr + 2));
@@ -743,7 +751,7 @@ __device__ __forceinline__ void conf_row(const T* __restrict__ row, int64_t V, c
     if (t == 0) {
       // a second value at kMaskedLogit or below is a clamped -inf: the row has one finite logit
       const float z2 = nmax >= 2 ? m : fmaxf(cmx, s_oth);
-      *out = row_stats_record(m, z2 <= kMaskedLogit ? -INFINITY : z2, A, Tsum, flags, top1, V, a);
+      *out = row_stats_record(m, z2 <= kMaskedLogit ? -INFINITY : z2, A, Tsum, flags, top1, a);
       if (VAR) {
         const double v = (vS2 - vS1 * (vS1 / vN)) / vN;
         *var_out = (float)(v > 0.0 ? v : 0.0);
@@ -2042,7 +2050,7 @@ bool conf_args(const cmsd_conf_params* p, int64_t vocab, ConfArgs& a) {
   if (!(l1 >= 0.f && l1 <= 1.f && l2 >= 0.f && l2 <= 1.f && l3 >= 0.f && l3 <= 1.f)) return false;
   if (fabs((double)l1 + (double)l2 + (double)l3 - 1.0) > 1e-6) return false;
   if (!finite_f(p->beta_margin) || !(p->beta_margin > 0.f)) return false;
-  a = ConfArgs{l1, l2, l3, p->beta_margin, log((double)vocab)};
+  a = ConfArgs{l1, l2, l3, p->beta_margin, 1.0 / log((double)vocab), 1.0 / (1.0 - 1.0 / (double)vocab)};
   return true;
 }
 bool draft_params_ok(const cmsd_draft_params* p) {
