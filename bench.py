@@ -44,12 +44,12 @@ PEAK_HBM_GBS = 8000.0   # MI355X HBM3E
 # device copy (x2.0 and x1.0).  Valid only for the kernel code they were taken on
 # (kernel_code_hash(): sha256 prefix of the .hip file's code without comments);
 # otherwise "traffic" is reported null.
-TRAFFIC = {"kernel_code_sha256_16": "7eb0674dec29c09f",
-           "k_row_pass_c4": 2170.52e6 + 0.270e6, "k_confidence_c4": 1052.91e6 + 0.131e6,
-           "k_confidence_c5": 524.72e6 + 0.262e6, "k_confidence_c5m": 524.72e6 + 0.262e6,
-           "k_row_pass_c3": 112.85e6 + 0.035e6, "k_row_pass_c2": 9.11e6 + 0.004e6,
-           "k_row_pass_v152k": 331.73e6 + 0.035e6,
-           "k_row_pass_c4f": 4340.34e6 + 0.270e6,
+TRAFFIC = {"kernel_code_sha256_16": "f29b9c1ea53ba275",
+           "k_row_pass_c4": 2170.51e6 + 0.270e6, "k_confidence_c4": 1052.88e6 + 0.131e6,
+           "k_confidence_c5": 524.71e6 + 0.262e6, "k_confidence_c5m": 524.70e6 + 0.262e6,
+           "k_row_pass_c3": 112.60e6 + 0.035e6, "k_row_pass_c2": 9.10e6 + 0.004e6,
+           "k_row_pass_v152k": 331.71e6 + 0.035e6,
+           "k_row_pass_c4f": 4340.33e6 + 0.270e6,
            "profile": "profiles/<workload>_cm_logit_pass.md"}
 
 
