@@ -1651,11 +1651,12 @@ __device__ __forceinline__ int locate_units(const T* trow, const T* drow, const 
 template <typename T, int BD>
 __device__ __forceinline__ int sample_from_parts(const T* trow, const T* drow, int64_t V, bool resid, float mst, float msd,
                                  float rho0, float u, const SlicePart* __restrict__ P, int S, double* sd, int* si,
-                                 double* s_sc, int* s_y) {
+                                 double* s_sc, int* s_y, const SlicePart* first = nullptr) {
   const int t = threadIdx.x;
   const bool same_phase = ((reinterpret_cast<uintptr_t>(trow) ^ reinterpret_cast<uintptr_t>(drow)) & 15u) == 0;
   const int slo = (int)((int64_t)t * S / BD), shi = (int)((int64_t)(t + 1) * S / BD);
-  const SlicePart p0 = slo < shi ? P[slo] : SlicePart{0.0, 0.0, 0.0, 0.0};
+  // `first`: this thread's first partial, already loaded by the caller
+  const SlicePart p0 = first ? *first : (slo < shi ? P[slo] : SlicePart{0.0, 0.0, 0.0, 0.0});
   // fresh normalisers and the exact ratio
   double tot[2] = {0.0, 0.0};
   for (int s = slo; s < shi; ++s) {
@@ -1736,6 +1737,11 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
   const int t = threadIdx.x;
   const int b = blockIdx.x;
   if (b >= a.B) return;
+  // this thread's first slice partial, written by k_final_parts: its load does not wait
+  // for the decisions, so the two round trips overlap (unused for an invalid sequence
+  // and in GREEDY mode, where no partials were written; always inside the workspace)
+  const int slo = (int)((int64_t)t * S / BD), shi = (int)((int64_t)(t + 1) * S / BD);
+  const SlicePart first = slo < shi ? ws[(int64_t)b * S + slo] : SlicePart{0.0, 0.0, 0.0, 0.0};
   const SeqInfo q = SRC == Src::Record   ? *pass_info(a, b)
                     : SRC == Src::Inline ? seq_info_pass<true>(a, b, &s_q)
                                          : seq_info(a, b, &s_q);
@@ -1760,7 +1766,7 @@ __global__ __launch_bounds__(kSampleBD) void k_final_sample(VerifyArgs a, int S,
   const T* drow = reinterpret_cast<const T*>(a.draft) + q.dr * a.dstride;
   const float u = a.unif[q.off + q.kb];
   const int y = sample_from_parts<T, BD>(trow, drow, a.V, resid, q.mst, q.msd, q.rho0, u, ws + (int64_t)b * S, S, sd,
-                                     si, s_sc, &s_y);
+                                     si, s_sc, &s_y, &first);
   if (t == 0) {
     a.n_acc[b] = nacc;
     a.next_tok[b] = y;
