@@ -23,8 +23,9 @@
 //   k_row_pass      cmsd_logit_pass's row pass: drafter rows (as k_confidence) and
 //                   dense target rows (as k_target_rows, decisions deferred) in one
 //                   grid.
-//   k_pass_decide   cmsd_logit_pass in GREEDY mode, one wave per sequence: draft
-//                   length, accept tests, first rejection and the final outputs.
+//   k_pass_decide   cmsd_logit_pass on large launches and in GREEDY mode, one wave
+//                   per sequence: draft length, accept tests and first rejection,
+//                   written once for the final kernels (GREEDY: the final outputs).
 //   k_fused_pass    cmsd_logit_pass_fused, one launch for small batches: the row pass,
 //                   then the last row workgroup of each sequence (atomic count behind
 //                   a device fence) decides and samples with the same functions.
@@ -122,8 +123,9 @@ template <> struct Elem<Bf16> {
   __device__ static uint32_t clamp_word(uint32_t w) {
     const u16x2 lim = {0xff00, 0xff00};
     return __builtin_bit_cast(uint32_t, __builtin_elementwise_min(__builtin_bit_cast(u16x2, w), lim));
-  }  __device__ static uint4 raw_masked() { return make_uint4(0xff00ff00u, 0xff00ff00u, 0xff00ff00u, 0xff00ff00u); }
-
+  }
+  // the clamp value (kMaskedLogit) in every element: padding that adds exactly 0 to the sums
+  __device__ static uint4 raw_masked() { return make_uint4(0xff00ff00u, 0xff00ff00u, 0xff00ff00u, 0xff00ff00u); }
   __device__ static uint4 clamp_masked(const uint4& v) {
     return make_uint4(clamp_word(v.x), clamp_word(v.y), clamp_word(v.z), clamp_word(v.w));
   }
@@ -1959,9 +1961,9 @@ int row_block(int64_t n_rows, int64_t row_bytes) {
 
 // Rounds in flight per thread for a streaming-row launch.  Long launches (several
 // generations of workgroups: at least 16 rows per compute unit for the joint row pass,
-// 32 for the confidence pass alone, as c4's row pass and c5's 8192 drafter rows) stream
-// better with three rounds in flight; shorter ones keep two, whose smaller register
-// count lets more of their rows run at once.  The depth only schedules loads: the
+// 32 for the confidence pass alone, as 8448 rows of 128256 logits in one pass or 8192
+// drafter rows of 32000) stream better with three rounds in flight; shorter ones keep
+// two, whose smaller register count lets more of their rows run at once.  The depth only schedules loads: the
 // arithmetic, and so every result, is the same.  cmsd_set_row_shape forces it.
 #ifndef CMSD_DEEP_DEPTH
 #define CMSD_DEEP_DEPTH 3
@@ -2005,7 +2007,7 @@ void launch_target_rows_d(int bd, const VerifyArgs& a, hipStream_t st) {
     hipLaunchKernelGGL((k_target_rows<T, 256, DEPTH>), grid, dim3(256), 0, st, a);
 }
 // The packed target rows of cmsd_verify: two rounds in flight (three measured slower
-// on c5's 3097 rows of 64 KB), three only when forced.
+// on 3097 rows of 32000 bf16 logits), three only when forced.
 template <typename T>
 void launch_target_rows(int bd, const VerifyArgs& a, hipStream_t st) {
   if (g_ring_depth.load(std::memory_order_relaxed) == 3)
@@ -2169,8 +2171,9 @@ void launch_final(const VerifyArgs& a, int S, int SW, SlicePart* ws, hipStream_t
 
 // Whether the final-token workgroups of cmsd_logit_pass form their sequence's decisions
 // themselves instead of reading k_pass_decide's record: up to 32 slice waves per compute
-// unit the launch saved outweighs the repeated decisions (c2, c3, a 152k vocabulary);
-// c4's 63 slices x 256 sequences (63 waves per unit) keep the decision kernel.
+// unit the launch saved outweighs the repeated decisions (8 or 64 sequences of 8 drafts
+// at V = 32000 to 152064); 256 sequences at V = 128256 (63 slices each: 63 waves per
+// unit) keep the decision kernel.
 // cmsd_set_pass_decisions forces either (0 = chosen per call, 1 = record, 2 = inline).
 std::atomic<int> g_pass_decisions{0};
 bool inline_decisions(unsigned slice_waves) {
