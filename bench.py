@@ -86,7 +86,7 @@ def cpu_baseline(name: str, seed: int, mode: int, budget_s: float = 20.0) -> dic
         ncpu = len(os.sched_getaffinity(0))
     except AttributeError:
         ncpu = os.cpu_count() or 1
-    # one process per host core this process may run on, at most 16 (a one-GPU machine's
+    # one process per host core this process may run on, at most 16 (one GPU's
     # share of its host); the line states both the cores used and the host's count
     workers = max(1, min(16, ncpu))
     # estimate the per-sequence cost with one sequence, then size the sample to the budget
