@@ -48,8 +48,19 @@ def _outs(B, K, dev):
             "next_token": torch.empty(B, dtype=torch.int32, device=dev)}
 
 
+@pytest.mark.parametrize("decisions", [0, 1])
 @pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY])
-def test_noalloc_equals_logit_pass_on_consecutive_calls(cm, mode):
+def test_noalloc_equals_logit_pass_on_consecutive_calls(cm, mode, decisions):
+    # decisions: 0 = the per-call choice (formed in the final-token kernels at these
+    # sizes), 1 = the decision kernel's record, written over the scratch's row slots
+    cm.cmsd_set_pass_decisions(decisions)
+    try:
+        _consecutive_calls(cm, mode)
+    finally:
+        cm.cmsd_set_pass_decisions(0)
+
+
+def _consecutive_calls(cm, mode):
     dev = torch.device("cuda:0")
     # a larger call, then a smaller one of another dtype and vocabulary on the same
     # scratch, then the larger one again
