@@ -309,10 +309,12 @@ cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, cons
  * 256-thread workgroup; the last row of a sequence to finish (an atomic count per
  * sequence, each row's results published behind a device fence) makes the draft
  * length and the accept tests and samples the final token in the same launch.  The
- * fences serialise across the chip (tens of ns per row), so this pays for launches of
- * up to a few hundred rows (batch*(2*k_max+1)); larger batches are faster with
- * cmsd_logit_pass.  Arguments, outputs and errors are cmsd_logit_pass's (without
- * row_events), except the workspace:
+ * fences serialise across the chip (tens of ns per row), and one workgroup carries each
+ * sequence's final token, so the single launch is the faster call only when that work
+ * is tiny (one MI355X: 1024-logit rows); at V = 32000 cmsd_logit_pass (three launches
+ * for small batches) was faster at every batch measured, 1 to 64.  It is for callers
+ * that need exactly one launch.  Arguments, outputs and errors are cmsd_logit_pass's
+ * (without row_events), except the workspace:
  *   workspace       device scratch of at least
  *                   cmsd_logit_pass_fused_workspace_bytes(batch, k_max, vocab) bytes,
  *                   8-byte aligned, owned by the caller.  Its last 4*batch bytes
