@@ -28,6 +28,13 @@
  *   - Argument errors are detected on the host before anything is enqueued and
  *     returned as CMSD_ERR_ARG / CMSD_ERR_DTYPE; in that case no output is
  *     touched.  CMSD_ERR_LAUNCH reports a failed kernel launch.
+ *   - Launch sizes: a kernel launch holds fewer than 2^32 work-items, and a call
+ *     whose launches would not returns CMSD_ERR_ARG: cmsd_verify needs
+ *     batch*(k_max+1) < 2^26, cmsd_logit_pass and cmsd_logit_pass_noalloc
+ *     batch*(2*k_max+1) < 2^26 (cmsd_logit_pass_fused < 2^24), and every call that
+ *     samples (cmsd_verify, the single-call passes, cmsd_draft_sample) batch (n_rows)
+ *     < 2^24 and batch*S < 2^26 for S = ceil((vocab/4 + 2)/256) vocabulary slices.
+ *     cmsd_confidence takes any n_rows < 2^31.
  *   - Device-resident indices (draft lengths, offsets, drafted ids) cannot be
  *     checked on the host; the kernels check them and report a violation per
  *     sequence through the outputs (see cmsd_verify) without reading out of

@@ -1949,14 +1949,22 @@ int device_cus() {
   if (dev < 64) cache[dev] = n;
   return n;
 }
+// A launch holds at most 2^32 - 1 work-items (workgroups x threads): the grid size of
+// an HSA dispatch is 32-bit.  The entry points reject sizes whose launches would not fit.
+bool launch_fits(int64_t groups, int threads) { return groups >= 0 && groups * threads <= (int64_t)UINT32_MAX; }
+// A row shape gives way to smaller workgroups on a grid that would not fit otherwise.
+int fit_block(int bd, int64_t groups) {
+  while (bd > 64 && !launch_fits(groups, bd)) bd >>= 1;
+  return bd;
+}
 int row_block(int64_t n_rows, int64_t row_bytes) {
-  if (const int v = g_row_block.load(std::memory_order_relaxed)) return v;
+  if (const int v = g_row_block.load(std::memory_order_relaxed)) return fit_block(v, n_rows);
   const int64_t waves = 16 * (int64_t)device_cus();  // 4 waves on each of 4 SIMDs per CU
   if (row_bytes <= (int64_t)128 << 10) {
     if (n_rows >= waves) return 64;
     if (n_rows >= waves / 2) return 128;
   }
-  return 256;
+  return fit_block(256, n_rows);
 }
 
 // Rounds in flight per thread for a streaming-row launch.  Long launches (several
@@ -1973,10 +1981,16 @@ bool deep_ring(int64_t n_rows, int rows_per_cu) {
   return n_rows >= rows_per_cu * (int64_t)device_cus();
 }
 
+// Workgroups per confidence launch: the launch's work-items (workgroups x threads) stay
+// below 2^32, and the kernel's loop over rows takes any rows beyond.  (Below the cap
+// the loop runs once; a kernel of one row per workgroup and no loop gets more waves
+// per SIMD from fewer registers and measured slower on 8192 rows of 32000 logits.)
+constexpr int64_t kConfMaxGrid = (int64_t)1 << 22;
+
 template <typename T, bool VAR, int DEPTH>
 void launch_confidence_d(int bd, const T* logits, int64_t n_rows, int64_t V, int64_t stride, const ConfArgs& a,
                          cmsd_row_stats* out, float* var, hipStream_t st) {
-  const dim3 grid((unsigned)n_rows);
+  const dim3 grid((unsigned)(n_rows < kConfMaxGrid ? n_rows : kConfMaxGrid));
   if (bd == 64)
     hipLaunchKernelGGL((k_confidence<T, 64, VAR, DEPTH>), grid, dim3(64), 0, st, logits, n_rows, V, stride, a, out,
                        var);
@@ -2115,9 +2129,10 @@ cmsd_status pass_setup(const void* draft_logits, int64_t draft_stride, const voi
   if (batch == 0) return CMSD_OK;
   const size_t es = dtype == CMSD_F32 ? 4 : 2;
   const int64_t drows = (int64_t)batch * k_max, trows = (int64_t)batch * (k_max + 1);
-  if (drows + trows > INT32_MAX || draft_stride > INT64_MAX / drows || target_stride > INT64_MAX / trows)
+  if (!launch_fits(drows + trows, 64) || draft_stride > INT64_MAX / drows || target_stride > INT64_MAX / trows)
     return CMSD_ERR_ARG;
-  if ((int64_t)batch * verify_slices(vocab, 4) > INT32_MAX) return CMSD_ERR_ARG;
+  if (!launch_fits((int64_t)batch * verify_slices(vocab, 4), kPartBD) || !launch_fits(batch, kSampleBD))
+    return CMSD_ERR_ARG;
   if (!draft_logits || !target_logits || !drafted || (!uniforms && verify->mode != CMSD_MODE_GREEDY) ||
       !draft_stats || !draft_len || !target_stats || !n_accepted || !next_token)
     return CMSD_ERR_ARG;
@@ -2284,7 +2299,7 @@ cmsd_status cmsd_draft_sample(const void* logits, int32_t dtype, int64_t n_rows,
   if (row_stride > INT64_MAX / n_rows) return CMSD_ERR_ARG;
   const int S = verify_slices(vocab, (int)es);
   const int SW = (S + kSubPerWG - 1) / kSubPerWG;
-  if (n_rows * SW > INT32_MAX) return CMSD_ERR_ARG;
+  if (!launch_fits(n_rows * SW, kPartBD) || !launch_fits(n_rows, kSampleBD)) return CMSD_ERR_ARG;
   SlicePart* ws = static_cast<SlicePart*>(workspace);
   const hipStream_t st = as_stream(stream);
   const dim3 gp((unsigned)(n_rows * SW)), gr((unsigned)n_rows);
@@ -2344,14 +2359,14 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   if (batch == 0) return CMSD_OK;
   if (target_rows < 1 || target_rows > INT32_MAX) return CMSD_ERR_ARG;
   if (draft_stride < vocab || target_stride < vocab) return CMSD_ERR_ARG;
-  if ((int64_t)batch * (k_max + 1) > INT32_MAX) return CMSD_ERR_ARG;  // the target-row grid
+  if (!launch_fits((int64_t)batch * (k_max + 1), 64) || !launch_fits(batch, kSampleBD)) return CMSD_ERR_ARG;
   const size_t es = dtype == CMSD_F32 ? 4 : 2;
   if (!draft_logits || !draft_stats || !target_logits || !target_offsets || !draft_len || !drafted ||
       (!uniforms && params->mode != CMSD_MODE_GREEDY) ||
       !target_stats || !n_accepted || !next_token || !workspace)
     return CMSD_ERR_ARG;
   if (workspace_bytes < cmsd_verify_workspace_bytes(batch, k_max, vocab) || !aligned(workspace, 8)) return CMSD_ERR_ARG;
-  if ((int64_t)batch * verify_slices(vocab, 4) > INT32_MAX) return CMSD_ERR_ARG;
+  if (!launch_fits((int64_t)batch * verify_slices(vocab, 4), kPartBD)) return CMSD_ERR_ARG;
   if (!aligned(draft_logits, es) || !aligned(target_logits, es) || !aligned(draft_stats, 4) ||
       !aligned(target_offsets, 4) || !aligned(draft_len, 4) || !aligned(drafted, 4) || !aligned(uniforms, 4) ||
       !aligned(target_stats, 4) || !aligned(n_accepted, 4) || !aligned(next_token, 4))
@@ -2383,7 +2398,8 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
   SlicePart* ws = static_cast<SlicePart*>(workspace);
   a.slots = reinterpret_cast<RowSlot*>(ws + (size_t)batch * verify_slices(vocab, 4));
   const unsigned gp = (unsigned)((int64_t)batch * SW);
-  const int bd = row_block(target_rows, vocab * (int64_t)es);
+  // the shape suits the scored rows; the grid covers every (sequence, position)
+  const int bd = fit_block(row_block(target_rows, vocab * (int64_t)es), (int64_t)batch * (k_max + 1));
   if (dtype == CMSD_F32) {
     launch_target_rows<float>(bd, a, st);
     if (a.mode != CMSD_MODE_GREEDY)
@@ -2474,6 +2490,7 @@ cmsd_status cmsd_logit_pass_fused(const void* draft_logits, int64_t draft_stride
   if (e != CMSD_OK) return e;
   const int es = dtype == CMSD_F32 ? 4 : 2;
   const int64_t rows = (int64_t)batch * (2 * k_max + 1);
+  if (!launch_fits(rows, kFusedBD)) return CMSD_ERR_ARG;
   const int S = verify_slices(vocab, es);
   SlicePart* ws = static_cast<SlicePart*>(workspace);
   // the counters end the workspace (its size rounded down to 4 bytes): calls of any

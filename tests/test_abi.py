@@ -130,6 +130,12 @@ def _verify(**kw):
     (dict(wsb=16), cm.CMSD_ERR_ARG),                              # workspace too small
     (dict(ws=P + 4), cm.CMSD_ERR_ARG),                            # misaligned workspace
     (dict(B=0, dl=None, tl=None, ws=None, wsb=0), cm.CMSD_OK),
+    # launches past 2^32 work-items (the workspace and rows are ample, so only the launch
+    # sizes reject): 2^23 * 9 (sequence, position) groups of 64 threads, 2^24 sampling
+    # groups of 256, 2^20 sequences * 129 slices at V = 2^17
+    (dict(B=1 << 23, K=8, trows=1 << 30, wsb=1 << 62), cm.CMSD_ERR_ARG),
+    (dict(B=1 << 24, K=1, trows=1 << 30, wsb=1 << 62), cm.CMSD_ERR_ARG),
+    (dict(B=1 << 20, K=1, V=1 << 17, ds=1 << 17, ts=1 << 17, trows=1 << 30, wsb=1 << 62), cm.CMSD_ERR_ARG),
 ])
 
 def test_verify_argument_errors(kw, want):
@@ -154,6 +160,8 @@ def test_workspace_size():
     (dict(wsb=8), cm.CMSD_ERR_ARG),
     (dict(logits=P + 1), cm.CMSD_ERR_ARG),
     (dict(n=0, logits=None, ws=None, wsb=0), cm.CMSD_OK),
+    (dict(n=1 << 24, wsb=1 << 62), cm.CMSD_ERR_ARG),             # 2^24 sampling groups of 256 threads
+    (dict(n=1 << 22, V=1 << 17, stride=1 << 17, wsb=1 << 62), cm.CMSD_ERR_ARG),  # 2^22 rows * 129 slices
 ])
 def test_draft_sample_argument_errors(kw, want):
     a = dict(logits=P, dtype=cm.CMSD_BF16, n=8, V=1000, stride=1000, st=P, u=P, out=P, ws=P, wsb=1 << 20)
@@ -202,6 +210,12 @@ def _lpass(**kw):
     (dict(na=P + 2), cm.CMSD_ERR_ARG),
     (dict(ev=(C.c_void_p * 2)(P, None)), cm.CMSD_ERR_ARG),          # an event pair with a null entry
     (dict(B=0, dl=None, tl=None, dr=None, ws=None, wsb=0), cm.CMSD_OK),
+    # launches past 2^32 work-items: 2^23 * 9 rows of 64 threads, 2^24 sampling groups,
+    # 2^20 sequences * 129 slices at V = 2^17
+    (dict(B=1 << 23, K=4, dp=cm.DraftParams(1, 4, 1.0), wsb=1 << 62), cm.CMSD_ERR_ARG),
+    (dict(B=1 << 24, K=1, dp=cm.DraftParams(1, 1, 1.0), wsb=1 << 62), cm.CMSD_ERR_ARG),
+    (dict(B=1 << 20, K=1, V=1 << 17, ds=1 << 17, ts=1 << 17, dp=cm.DraftParams(1, 1, 1.0), wsb=1 << 62),
+     cm.CMSD_ERR_ARG),
 ])
 def test_logit_pass_argument_errors(kw, want):
     assert _lpass(**kw) == want
@@ -230,6 +244,7 @@ def _fpass(**kw):
     (dict(nt=None), cm.CMSD_ERR_ARG),
     (dict(B=-1), cm.CMSD_ERR_ARG),
     (dict(B=0, dl=None, tl=None, dr=None, ws=None, wsb=0), cm.CMSD_OK),
+    (dict(B=1 << 22, K=2, dp=cm.DraftParams(1, 2, 1.0), wsb=1 << 62), cm.CMSD_ERR_ARG),  # 5 * 2^22 rows of 256
 ])
 def test_logit_pass_fused_argument_errors(kw, want):
     assert _fpass(**kw) == want

@@ -163,7 +163,9 @@ def test_repeat_bitwise_identical(cm):
 
 
 # ----------------------------------------------------------------------------- edge cases
-def _case(g, B, K, V, dtype, scale=2.0, mask=None):
+def _case(g, B, K, V, dtype, scale=2.0, mask=None, mask_frac=0.0):
+    # mask: columns masked (-inf) in every row; mask_frac: each row masks that share of
+    # its logits at random, keeping at least one finite
     zd = g.normal(0, scale, (B * K, V)).astype(np.float32)
     zt = g.normal(0, scale, (B * (K + 1), V)).astype(np.float32)
     for b in range(B):
@@ -172,6 +174,11 @@ def _case(g, B, K, V, dtype, scale=2.0, mask=None):
     if mask is not None:
         zd[:, mask] = -np.inf
         zt[:, mask] = -np.inf
+    if mask_frac > 0.0:
+        for z in (zd, zt):
+            m = g.random(z.shape) < mask_frac
+            m[np.arange(z.shape[0]), g.integers(0, V, z.shape[0])] = False
+            z[m] = -np.inf
     store = (lambda x: x) if dtype == "f32" else W.bf16_bits_from_f32
     zds, zts = store(zd), store(zt)
     drafted = np.array([[int(np.argmax(Hn.decode(zds[b * K + i], dtype) + g.gumbel(size=V))) for i in range(K)]
@@ -204,6 +211,30 @@ def test_shapes(cm, dtype, V, K, B, pad):
     zd, zt, dr, u = _case(g, B, K, V, dtype)
     for mode in (O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY):
         _run_case(cm, zd, zt, dr, u, B, K, V, dtype, mode=mode, adaptive=bool(mode == O.MODE_CM), pad=pad)
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_problems(cm, seed):
+    # seeded random problems: vocabulary 2..70000 (log-uniform), 1..24 drafts, 1..6
+    # sequences, either dtype, every mode, dense or adaptive lengths, padded strides,
+    # per-row masks of random density or none, and each way the final-token workgroups
+    # get their decisions; every output checked against the oracle
+    g = np.random.default_rng(9000 + seed)
+    V = int(round(math.exp(g.uniform(math.log(2), math.log(70000)))))
+    K, B = int(g.integers(1, 25)), int(g.integers(1, 7))
+    dtype = ("f32", "bf16")[int(g.integers(2))]
+    mode = (O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY)[int(g.integers(3))]
+    adaptive, pad = bool(g.integers(2)), int(g.integers(0, 6))
+    mask_frac = (0.0, 0.0, 0.05, 0.5, 0.95)[int(g.integers(5))]
+    decisions = int(g.integers(3))
+    print(f"V={V} K={K} B={B} {dtype} mode={mode} adaptive={adaptive} pad={pad} mask={mask_frac} "
+          f"decisions={decisions}", flush=True)
+    zd, zt, dr, u = _case(g, B, K, V, dtype, scale=float(g.uniform(0.5, 4.0)), mask_frac=mask_frac)
+    cm.cmsd_set_pass_decisions(decisions)
+    try:
+        _run_case(cm, zd, zt, dr, u, B, K, V, dtype, mode=mode, adaptive=adaptive, pad=pad)
+    finally:
+        cm.cmsd_set_pass_decisions(0)
 
 
 @pytest.mark.parametrize("depth", [2, 3])
