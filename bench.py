@@ -19,8 +19,17 @@ kernel's rows in its grid shape (``read_ceiling``: what one launch of those byte
 reach) and, with ``--extras``, the drafting sampler and the logit-variance pass; the CPU
 oracle runs last on the host.
 
+``--streams G`` splits the batch into G sequence groups, each with its own calls on its
+own stream, so one group's final-token kernels (latency-bound) overlap another group's
+row pass.  The roofline kernel is then group 0's launch, timed while the other groups'
+kernels share the chip: its bytes are one group's, and its rate is what it reaches
+beside them, not alone (no read ceiling or counter traffic is reported then).  With one
+group (the default), the bench also times the same steps over ``--overlap`` groups (2)
+after the timed region and reports their throughput under ``overlap``.
+
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4|c5|c5m|c3|c2|v152k|tiny|b1]
-                  [--mode cm|standard] [--path auto|pass|fused|calls] [--streams G] [--event-every N]
+                  [--mode cm|standard] [--path auto|pass|fused|calls] [--streams G] [--overlap G]
+                  [--event-every N]
                   [--capacity-rows] [--no-rotate] [--extras] [--no-read-ceiling] [--no-cpu-baseline]
                   [--row-shape THREADS,DEPTH] [--copy-probe MIB]
 """
@@ -242,7 +251,10 @@ def main() -> int:
                     help="one cmsd_logit_pass call per step (dense layouts; auto: dense workloads), one "
                          "cmsd_logit_pass_fused call (one launch, for small batches), or the three separate calls")
     ap.add_argument("--streams", type=int, default=1, metavar="G",
-                    help="split the batch into G sequence groups, each on its own stream")
+                    help="split the batch into G sequence groups, each on its own stream (not with --path fused)")
+    ap.add_argument("--overlap", type=int, default=2, metavar="G",
+                    help="after the timed region, time the same steps with the batch split over G sequence "
+                         "groups on their own streams (reported under 'overlap'; 0 or 1: skip)")
     ap.add_argument("--event-every", type=int, default=64, metavar="N",
                     help="bracket the roofline kernel with HIP events in every N-th timed step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -304,43 +316,53 @@ def main() -> int:
     if G < 1 or cfg.B % G:
         print(f"bench.py: --streams must divide B={cfg.B}", file=sys.stderr)
         return 2
-    # G groups of B/G sequences, each on its own stream: sequences are independent,
-    # so the latency-bound tail of one group overlaps the row passes of another
-    K, bg = cfg.k_max, cfg.B // G
+    K = cfg.k_max
     prm = pipeline.Params(mode=mode)
     main = torch.cuda.current_stream(dev)
-    groups = []
-    for g in range(G):
-        b0, b1 = g * bg, (g + 1) * bg
-        lpg = pipeline.LogitPass(bg, K, cfg.V, dev, prm, dense=not cfg.ragged)
-        a = [draft[b0 * K:b1 * K], target[b0 * (K + 1):b1 * (K + 1)], drafted[b0 * K:b1 * K],
-             unif[b0 * (K + 1):b1 * (K + 1)]]
-        if cfg.ragged:
-            # the verifier scores k_b + 1 positions per sequence, packed by the device
-            # offsets: pack the target rows and uniforms once (untimed); every timed
-            # step recomputes the same draft lengths from the same drafter rows
-            lpg.confidence(a[0], main)
-            lpg.draft_len(main)
-            a[1] = W.pack_device(a[1], lpg.k, lpg.off, K)
-            a[3] = W.pack_device(a[3], lpg.k, lpg.off, K)
-            if not args.capacity_rows:
-                # the verifier scored exactly sum(k_b + 1) rows: hand verify that many
-                rt = int(lpg.off[bg].item())
-                a[1], a[3] = a[1][:rt], a[3][:rt]
-        groups.append((lpg, a, main if G == 1 else torch.cuda.Stream(dev)))
-    # successive steps read different copies of the logits, together more than 512 MiB
-    # (twice the 256 MB last-level cache), so no step finds rows a recent one left there
-    in_bytes = sum(a[0].nbytes + a[1].nbytes for _, a, _ in groups)
-    n_sets = 1 if args.no_rotate else max(1, -(-(512 << 20) // in_bytes))
-    sets = [[a] + [[a[0].clone(), a[1].clone(), a[2], a[3]] for _ in range(n_sets - 1)] for _, a, _ in groups]
-    torch.cuda.synchronize()
+
+    def make_groups(G):
+        # G groups of B/G sequences, each on its own stream: sequences are independent,
+        # so the latency-bound tail of one group overlaps the row passes of another
+        bg = cfg.B // G
+        groups = []
+        for g in range(G):
+            b0, b1 = g * bg, (g + 1) * bg
+            lpg = pipeline.LogitPass(bg, K, cfg.V, dev, prm, dense=not cfg.ragged)
+            a = [draft[b0 * K:b1 * K], target[b0 * (K + 1):b1 * (K + 1)], drafted[b0 * K:b1 * K],
+                 unif[b0 * (K + 1):b1 * (K + 1)]]
+            if cfg.ragged:
+                # the verifier scores k_b + 1 positions per sequence, packed by the device
+                # offsets: pack the target rows and uniforms once (untimed); every timed
+                # step recomputes the same draft lengths from the same drafter rows
+                lpg.confidence(a[0], main)
+                lpg.draft_len(main)
+                a[1] = W.pack_device(a[1], lpg.k, lpg.off, K)
+                a[3] = W.pack_device(a[3], lpg.k, lpg.off, K)
+                if not args.capacity_rows:
+                    # the verifier scored exactly sum(k_b + 1) rows: hand verify that many
+                    rt = int(lpg.off[bg].item())
+                    a[1], a[3] = a[1][:rt], a[3][:rt]
+            groups.append((lpg, a, main if G == 1 else torch.cuda.Stream(dev)))
+        # successive steps read different copies of the logits, together more than 512 MiB
+        # (twice the 256 MB last-level cache), so no step finds rows a recent one left there
+        in_bytes = sum(a[0].nbytes + a[1].nbytes for _, a, _ in groups)
+        n_sets = 1 if args.no_rotate else max(1, -(-(512 << 20) // in_bytes))
+        sets = [[a] + [[a[0].clone(), a[1].clone(), a[2], a[3]] for _ in range(n_sets - 1)] for _, a, _ in groups]
+        torch.cuda.synchronize()
+        return groups, sets, n_sets
+
+    groups, sets, n_sets = make_groups(G)
     R_d = cfg.draft_rows
-    R_t = sum(int(lpg.off[bg].item()) for lpg, _, _ in groups) if cfg.ragged else cfg.dense_target_rows
+    R_t = (sum(int(lpg.off[cfg.B // G].item()) for lpg, _, _ in groups) if cfg.ragged
+           else cfg.dense_target_rows)
     # one cmsd_logit_pass call per step on dense workloads (one stream), else the three calls
     use_fused = args.path == "fused"
     use_pass = args.path == "pass" or (args.path == "auto" and not cfg.ragged)
-    if (use_pass or use_fused) and (cfg.ragged or G != 1):
-        print(f"bench.py: --path {args.path} needs a dense workload and one stream", file=sys.stderr)
+    if (use_pass or use_fused) and cfg.ragged:
+        print(f"bench.py: --path {args.path} needs a dense workload", file=sys.stderr)
+        return 2
+    if use_fused and G != 1:
+        print("bench.py: --path fused runs on one stream", file=sys.stderr)
         return 2
     rk = "k_fused_pass" if use_fused else ("k_row_pass" if use_pass else "k_confidence")
 
@@ -411,18 +433,39 @@ def main() -> int:
     t_dl = float(np.mean([e[1].elapsed_time(e[2]) for e in ev2])) * 1e-3
     t_ver = float(np.mean([e[2].elapsed_time(e[3]) for e in ev2])) * 1e-3
 
+    # the same steps with the batch split over `--overlap` sequence groups, each on its
+    # own stream, so that one group's final-token kernels overlap another group's row
+    # pass (after the timed region, warmed up alike, no events)
+    ov = None
+    if G == 1 and args.overlap > 1 and cfg.B % args.overlap == 0 and not use_fused:
+        print(f"[bench] {args.overlap} stream groups", file=sys.stderr, flush=True)
+        g2, s2, n2 = make_groups(args.overlap)
+        for k in range(args.warmup):
+            for gi, (lpg, _, st) in enumerate(g2):
+                step(lpg, s2[gi][k % n2], st)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(args.steps):
+            for gi, (lpg, _, st) in enumerate(g2):
+                step(lpg, s2[gi][(args.warmup + k) % n2], st)
+        torch.cuda.synchronize()
+        ov = (args.overlap, 1e3 * (time.perf_counter() - t0) / args.steps)
+        del g2, s2
+
     n_acc = np.concatenate([lpg.n_acc.cpu().numpy() for lpg, _, _ in groups])
     k_all = np.concatenate([lpg.k.cpu().numpy() for lpg, _, _ in groups])
     k_used = k_all if cfg.ragged else np.full(cfg.B, cfg.k_max)
     rej = int((n_acc < k_used).sum())
     s = cfg.elem_bytes
     conf_bytes = R_d * cfg.V * s + R_d * 32
-    # the roofline kernel's launch: the joint row pass reads every drafter and target row
-    # once and writes a 32-byte record per drafter row, a 32-byte record and a 32-byte
-    # slot per target row, after gathering two logits per drafted position; k_confidence
-    # reads one group's drafter rows (the whole batch when G = 1) and writes their records
+    # the roofline kernel's launch (group 0's; the whole batch when G = 1): the joint row
+    # pass reads every drafter and target row of the group once and writes a 32-byte
+    # record per drafter row, a 32-byte record and a 32-byte slot per target row, after
+    # gathering two logits per drafted position; k_confidence reads the group's drafter
+    # rows and writes their records
     if use_pass:
-        launch_bytes = R_d * (cfg.V * s + 32) + R_t * (cfg.V * s + 64) + cfg.B * cfg.k_max * 8
+        launch_bytes = ((R_d // G) * (cfg.V * s + 32) + (R_t // G) * (cfg.V * s + 64)
+                        + (cfg.B // G) * cfg.k_max * 8)
     elif use_fused:
         launch_bytes = None     # the whole step: its algorithmic bytes (below)
     else:
@@ -459,6 +502,9 @@ def main() -> int:
                            "path": ("cmsd_logit_pass_fused" if use_fused else "cmsd_logit_pass" if use_pass
                                     else "three calls"), "input_copies": n_sets},
     }
+    if ov is not None:
+        result["overlap"] = {"streams": ov[0], "ms_per_step": ov[1], "value": (R_d + R_t) / (ov[1] * 1e-3),
+                             "unit": "rows/s", "gbps_algorithmic": step_bytes / (ov[1] * 1e-3) / 1e9}
     if not args.no_read_ceiling and G == 1 and not use_fused:
         result["read_ceiling"] = read_ceiling(sets, n_sets, cfg, R_t, use_pass, main, args.steps, t_roof)
     if args.extras:

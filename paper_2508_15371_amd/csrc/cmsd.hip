@@ -992,10 +992,7 @@ __device__ __forceinline__ int accept_test(int mode, int beta, float tau_base, f
   return (stoch || (mode == CMSD_MODE_CM && gate)) ? 1 : 0;
 }
 
-// One target row.  PASS = false: a packed row of cmsd_verify (sequence found from the
-// offsets, accept test made here).  PASS = true: dense row r = b*(k_max+1) + i of the
-// single-call pass, whose accept test waits for the drafter stats (PassSlot).
-// One target row.  PASS = false: position q = b*(k_max+1) + i of cmsd_verify's grid over
+// One target row.  PASS = false: position q = i*B + b of cmsd_verify's grid over
 // (sequence, position); the sequence's draft length and offsets and the position's
 // drafted id and drafter stats are loaded in one round from q alone, positions past
 // k_b (and sequences with an invalid length or offsets, which the final-token kernels
