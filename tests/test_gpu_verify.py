@@ -110,12 +110,18 @@ def test_verify_repeat_bitwise_identical(mods):
 
 
 # ----------------------------------------------------------------------------- edge cases
-def _small_case(g, B, K, V, dtype, scale=2.0):
+def _small_case(g, B, K, V, dtype, scale=2.0, mask_frac=0.0):
+    # mask_frac: each row masks (-inf) that share of its logits at random, keeping one finite
     zd = (g.normal(0, scale, (B * K, V))).astype(np.float32)
     zt = (g.normal(0, scale, (B * (K + 1), V))).astype(np.float32)
     for b in range(B):
         for i in range(K):
             zt[b * (K + 1) + i] = zd[b * K + i] + g.normal(0, 0.5, V).astype(np.float32)
+    if mask_frac > 0.0:
+        for z in (zd, zt):
+            m = g.random(z.shape) < mask_frac
+            m[np.arange(z.shape[0]), g.integers(0, V, z.shape[0])] = False
+            z[m] = -np.inf
     store = (lambda x: x) if dtype == "f32" else W.bf16_bits_from_f32
     drafted = np.array([[int(np.argmax(Hn.decode(store(zd[b * K + i]), dtype) + g.gumbel(size=V)))
                          for i in range(K)] for b in range(B)], dtype=np.int32)
@@ -160,6 +166,47 @@ def test_ragged_lengths_small_vocab(mods, dtype, V, mode):
         ztr = [Hn.decode(zt[off[b] + i], dtype) for i in range(kb + 1)]
         C = [Hn.oracle_conf(z, V) for z in zdr]
         Hn.check_sequence(t, b, ztr, zdr, drafted[b], unif[off[b]:off[b] + kb + 1], C, kb, mode, Hn.PARAMS,
+                          ts, int(off[b]), int(n_acc[b]), int(nxt[b]))
+    t.assert_ok()
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_ragged_problems(mods, seed):
+    # seeded random ragged problems through cmsd_confidence + cmsd_verify: vocabulary
+    # 2..70000 (log-uniform), up to 16 drafts (every fourth case up to 80, past one
+    # wave's 64 positions), 1..8 sequences with draft lengths drawn from 0..k_max and
+    # their target rows packed, either dtype, every mode, random gate parameters, per-row
+    # masks of random density or none; every output against the oracle
+    g = np.random.default_rng(7000 + seed)
+    V = int(round(math.exp(g.uniform(math.log(2), math.log(70000)))))
+    K = int(g.integers(1, 81 if seed % 4 == 3 else 17))
+    B = int(g.integers(1, 9))
+    dtype = ("f32", "bf16")[int(g.integers(2))]
+    mode = (O.MODE_STANDARD, O.MODE_CM, O.MODE_GREEDY)[int(g.integers(3))]
+    mask_frac = (0.0, 0.0, 0.05, 0.5, 0.95)[int(g.integers(5))]
+    top_beta = int(g.choice([0, 1, 3, 10]))
+    tau_base, gamma = float(g.uniform(0.0, 1.0)), float(g.uniform(-1.0, 2.0))
+    print(f"V={V} K={K} B={B} {dtype} mode={mode} mask={mask_frac} beta={top_beta} tau={tau_base:.3f} "
+          f"gamma={gamma:.3f}", flush=True)
+    zd, zt_pad, drafted, unif_pad = _small_case(g, B, K, V, dtype, scale=float(g.uniform(0.5, 4.0)),
+                                                mask_frac=mask_frac)
+    k = g.integers(0, K + 1, B).astype(np.int32)
+    zt = W.pack_ragged(k, K, zt_pad.reshape(B, K + 1, V))
+    unif = W.pack_ragged(k, K, unif_pad.reshape(B, K + 1, 1)).reshape(-1)
+    off = np.concatenate([[0], np.cumsum(k + 1)]).astype(np.int32)
+    gs, n_acc, nxt, ts = _run_small(mods, zd, zt, drafted, unif, k, dtype, B, K, V, mode=mode, top_beta=top_beta,
+                                    tau_base=tau_base, gamma=gamma)
+    P = dict(Hn.PARAMS, top_beta=top_beta, tau_base=tau_base, gamma=gamma)
+    t = Hn.Tally()
+    for b in range(B):
+        kb = int(k[b])
+        zdr = [Hn.decode(zd[b * K + i], dtype) for i in range(K)]
+        for i in range(K):
+            Hn.check_row_stats(t, gs, b * K + i, zdr[i], V, tuple(Hn.f32(x) for x in P["lambdas"]),
+                               Hn.f32(P["beta_margin"]))
+        ztr = [Hn.decode(zt[off[b] + i], dtype) for i in range(kb + 1)]
+        C = [Hn.oracle_conf(z, V) for z in zdr]
+        Hn.check_sequence(t, b, ztr, zdr, drafted[b], unif[off[b]:off[b] + kb + 1], C, kb, mode, P,
                           ts, int(off[b]), int(n_acc[b]), int(nxt[b]))
     t.assert_ok()
 
