@@ -1,6 +1,6 @@
 """Whole-batch GPU parity on the largest workloads and the masked one: every
 sequence of c3 (64), c4 (256), c4f (256, c4's recipe in fp32), c5 (512) and c5m (512, c5 with
--inf logits) in every mode,
+-inf logits) in every mode (and of c2, c3, c4 and c5 on their other two seeds),
 through the three calls (cmsd_confidence, cmsd_draft_len, cmsd_verify) and through
 cmsd_logit_pass in both verification lengths, against the oracle.  Every drafter row's record, every draft length (end to end, with its floor
 slack), every target-row record, accept decision, prefix and final token is compared
@@ -45,10 +45,14 @@ def _report(name, path, mode, t, n_acc, k, seqs):
 @pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("name", ["c3", "c4", "c4f", "c5", "c5m"])
 def test_full_batch_three_calls(mods, name, mode):
+    _three_calls(mods, name, mode, 0)
+
+
+def _three_calls(mods, name, mode, seed):
     cmsd, pipeline = mods
-    print(f"[full batch] start {name} three calls mode={mode}", flush=True)
+    print(f"[full batch] start {name} seed {seed} three calls mode={mode}", flush=True)
     cfg = W.CONFIGS[name]
-    d = Hn.workload(name)
+    d = Hn.workload(name, seed)
     lp = pipeline.LogitPass(cfg.B, cfg.k_max, cfg.V, "cuda:0", _params(pipeline, mode), dense=not cfg.ragged)
     lp.confidence(d["draft_dev"])
     lp.draft_len()
@@ -77,17 +81,21 @@ def test_full_batch_three_calls(mods, name, mode):
                off=off if cfg.ragged else np.arange(cfg.B + 1) * (K + 1), packed=cfg.ragged,
                verify_len="k_b" if cfg.ragged else "k_max", mode=mode, params=Hn.PARAMS)
     t = FB.check_batch()
-    _report(name, "three calls", mode, t, n_acc, k, cfg.B)
+    _report(name if seed == 0 else f"{name} seed {seed}", "three calls", mode, t, n_acc, k, cfg.B)
 
 
 @pytest.mark.parametrize("adaptive", [False, True])
 @pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("name", ["c3", "c4", "c4f", "c5", "c5m"])
 def test_full_batch_logit_pass(mods, name, mode, adaptive):
+    _logit_pass(mods, name, mode, adaptive, 0)
+
+
+def _logit_pass(mods, name, mode, adaptive, seed):
     cmsd, _ = mods
-    print(f"[full batch] start {name} cmsd_logit_pass mode={mode} adaptive={adaptive}", flush=True)
+    print(f"[full batch] start {name} seed {seed} cmsd_logit_pass mode={mode} adaptive={adaptive}", flush=True)
     cfg = W.CONFIGS[name]
-    d = Hn.workload(name)
+    d = Hn.workload(name, seed)
     P = Hn.PARAMS
     out = cmsd.cmsd_logit_pass(d["draft_dev"], d["target_dev"], d["drafted_dev"],
                                None if mode == O.MODE_GREEDY else d["unif_dev"], batch=cfg.B, k_max=cfg.k_max,
@@ -105,4 +113,18 @@ def test_full_batch_logit_pass(mods, name, mode, adaptive):
                off=np.arange(cfg.B + 1) * (K + 1), packed=False, verify_len="k_b" if adaptive else "k_max",
                mode=mode, params=P)
     t = FB.check_batch()
-    _report(name, f"cmsd_logit_pass {'adaptive' if adaptive else 'dense'}", mode, t, n_acc, k, cfg.B)
+    _report(name if seed == 0 else f"{name} seed {seed}", f"cmsd_logit_pass {'adaptive' if adaptive else 'dense'}",
+            mode, t, n_acc, k, cfg.B)
+
+
+@pytest.mark.parametrize("mode", [O.MODE_STANDARD, O.MODE_CM])
+@pytest.mark.parametrize("seed", [1, 2])
+@pytest.mark.parametrize("name", ["c2", "c3", "c4", "c5"])
+def test_full_batch_other_seeds(mods, name, seed, mode):
+    # the workloads' other two seeds (three seeds per configuration, as the paper runs
+    # each experiment with three): the dense ones through cmsd_logit_pass with the
+    # adaptive lengths, the ragged one through the three calls
+    if W.CONFIGS[name].ragged:
+        _three_calls(mods, name, mode, seed)
+    else:
+        _logit_pass(mods, name, mode, True, seed)
