@@ -241,7 +241,7 @@ def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     # the chip's clocks settle over the first ~100 steps of this load (steps 1-50 run
-    # ~3 % slower), so the default warms up for 100 steps and times 500 (~0.2 s on c4)
+    # ~3 % slower), so the default warms up for 100 steps and times 500 (~0.2 s on the default workload)
     ap.add_argument("--steps", type=int, default=500)
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", default="c4", choices=["tiny", "b1", "c2", "c3", "c4", "c4f", "c5", "c5m", "v152k"])

@@ -1132,9 +1132,9 @@ __global__ __launch_bounds__(BD) void k_target_rows(VerifyArgs a) {
 // grid, drafter rows first; the two kinds of row do not depend on each other.  Its
 // bf16 drafter rows keep their max round in registers at every workgroup size when two
 // rounds are in flight: 118 instead of 115 registers at 256 threads, still 4 waves per
-// SIMD, and no re-read of that round before the record (c3 43.2 -> 42.6 us per step,
-// v152k 78.3 -> 77.8).  Three rounds in flight, or fp32's 8-vector rounds, would lose a
-// wave per SIMD.
+// SIMD, and no re-read of that round before the record (64 sequences of 8 drafts: at
+// V = 50257, 43.2 -> 42.6 us per step; at V = 152064, 78.3 -> 77.8).  Three rounds in
+// flight, or fp32's 8-vector rounds, would lose a wave per SIMD.
 template <typename T, int DEPTH>
 constexpr bool kKeepWide = std::is_same<T, Bf16>::value && DEPTH == 2;
 template <typename T, int BD, int DEPTH>
