@@ -289,11 +289,6 @@ cmsd_status cmsd_verify(const void* draft_logits, int64_t draft_stride, const cm
  *                   k_max, vocab) bytes, 8-byte aligned, owned by the caller, as for
  *                   cmsd_verify (calls sharing it must be ordered).
  *   workspace_bytes its size.
- *   row_events      NULL, or a host array of two hipEvent_t (created by the caller):
- *                   the call records the first on its stream just before the row-pass
- *                   launch and the second just after it, so their interval times the
- *                   bandwidth-bound row pass alone (its kernel and the gap before it).
- *                   Results do not depend on it.
  * The arithmetic is the separate calls': the outputs are bit-identical to theirs
  * whenever the row kernels run with the same workgroup size (chosen from the number
  * of rows in the launch and their length, or forced by cmsd_set_row_shape), else
@@ -306,8 +301,21 @@ cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, cons
                             const cmsd_conf_params* conf, const cmsd_draft_params* draft,
                             const cmsd_verify_params* verify, int32_t adaptive, cmsd_row_stats* draft_stats,
                             int32_t* draft_len, cmsd_target_stats* target_stats, int32_t* n_accepted,
-                            int32_t* next_token, void* workspace, size_t workspace_bytes,
-                            void* const* row_events, void* stream);
+                            int32_t* next_token, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * cmsd_set_row_events - a measurement hook, for callers that time the row pass (a
+ * benchmark): arms the next cmsd_logit_pass call made by the calling host thread to
+ * record row_events[0] on its stream just before its row-pass launch and
+ * row_events[1] just after it, so their interval times that bandwidth-bound launch
+ * alone (its kernel and the gap before it).  That call disarms the hook whatever its
+ * outcome (an argument error or an empty batch records nothing); results never
+ * depend on it, and the other calls neither record nor disarm.
+ *   row_events      NULL (disarm), or a host array of two hipEvent_t created by the
+ *                   caller.
+ * Errors: CMSD_ERR_ARG (an array with a NULL event; the hook is left as it was).
+ */
+cmsd_status cmsd_set_row_events(void* const* row_events);
 
 /*
  * cmsd_logit_pass_fused - cmsd_logit_pass in a single launch, for small batches
@@ -321,7 +329,7 @@ cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, cons
  * is tiny (one MI355X: 1024-logit rows); at V = 32000 cmsd_logit_pass (three launches
  * for small batches) was faster at every batch measured, 1 to 64.  It is for callers
  * that need exactly one launch.  Arguments, outputs and errors are cmsd_logit_pass's
- * (without row_events), except the workspace:
+ * (cmsd_set_row_events does not apply to it), except the workspace:
  *   workspace       device scratch of at least
  *                   cmsd_logit_pass_fused_workspace_bytes(batch, k_max, vocab) bytes,
  *                   8-byte aligned, owned by the caller.  Its last 4*batch bytes
@@ -362,8 +370,9 @@ size_t cmsd_logit_pass_fused_workspace_bytes(int32_t batch, int32_t k_max, int64
  * process ends; its device address is looked up once per device (with that device
  * current) and kept.
  *
- * Arguments, outputs and results are those of cmsd_logit_pass without workspace,
- * workspace_bytes and row_events: the same kernels on the same workgroup sizes, so
+ * Arguments, outputs and results are those of cmsd_logit_pass without workspace and
+ * workspace_bytes (cmsd_set_row_events does not apply): the same kernels on the same
+ * workgroup sizes, so
  * the outputs are bit-identical to cmsd_logit_pass's.  Nothing in the scratch needs
  * to start at zero; it keeps the last call's contents.
  * Limits and errors: as cmsd_logit_pass, plus CMSD_ERR_SIZE (nothing enqueued) when
@@ -444,8 +453,9 @@ size_t cmsd_draft_sample_workspace_bytes(int64_t n_rows, int64_t vocab);
 /* Human-readable name of a status code (static string). */
 const char* cmsd_status_string(cmsd_status s);
 
-/* Library ABI version, (major << 16) | minor: 1.5 (1.4 plus cmsd_logit_pass_noalloc,
- * cmsd_set_row_shape and CMSD_ERR_SIZE). */
+/* Library ABI version, (major << 16) | minor: 1.7.  1.5 added cmsd_logit_pass_noalloc,
+ * cmsd_set_row_shape and CMSD_ERR_SIZE; 1.6 cmsd_set_pass_decisions; 1.7 moved the
+ * row-pass timing events out of cmsd_logit_pass's arguments into cmsd_set_row_events. */
 int32_t cmsd_version(void);
 
 #ifdef __cplusplus

@@ -68,8 +68,10 @@ def _load() -> C.CDLL:
     lib.cmsd_draft_sample_workspace_bytes.restype = C.c_size_t
     lib.cmsd_logit_pass.argtypes = [vp, i64, vp, i64, vp, vp, i32, i32, i32, i64, C.POINTER(ConfParams),
                                     C.POINTER(DraftParams), C.POINTER(VerifyParams), i32, vp, vp, vp, vp, vp, vp,
-                                    C.c_size_t, C.POINTER(vp), vp]
+                                    C.c_size_t, vp]
     lib.cmsd_logit_pass.restype = C.c_int
+    lib.cmsd_set_row_events.argtypes = [C.POINTER(vp)]
+    lib.cmsd_set_row_events.restype = C.c_int
     lib.cmsd_logit_pass_fused.argtypes = [vp, i64, vp, i64, vp, vp, i32, i32, i32, i64, C.POINTER(ConfParams),
                                           C.POINTER(DraftParams), C.POINTER(VerifyParams), i32, vp, vp, vp, vp, vp,
                                           vp, C.c_size_t, vp]
@@ -158,6 +160,13 @@ def cmsd_set_pass_decisions(mode: int = 0) -> None:
     decision kernel's record (four launches), 2 in every final-token workgroup (three
     launches).  Bit-identical outputs.  Process-wide."""
     _check("cmsd_set_pass_decisions", _lib.cmsd_set_pass_decisions(int(mode)))
+
+
+def cmsd_set_row_events(row_events) -> None:
+    """Arm the next cmsd_logit_pass call of this thread to record the pair of
+    recorded-once ``torch.cuda.Event`` objects just before and just after its row-pass
+    launch (None disarms).  A measurement hook; results never depend on it."""
+    _check("cmsd_set_row_events", _lib.cmsd_set_row_events(_events(row_events)))
 
 
 def _events(evs):
@@ -391,19 +400,22 @@ def cmsd_logit_pass(draft_logits: torch.Tensor, target_logits: torch.Tensor, dra
     dtype), ``drafted`` int32 [batch*k_max], ``uniforms`` float32 [batch*(k_max+1)]
     (None in GREEDY mode).  ``row_events``: optional pair of recorded-once
     ``torch.cuda.Event`` objects, recorded on the call's stream just before and just
-    after the row-pass launch.  Returns the output tensors by name."""
+    after the row-pass launch (armed through cmsd_set_row_events right before the
+    call).  Returns the output tensors by name."""
     outs = {"draft_stats": draft_stats, "draft_len": draft_len, "target_stats": target_stats,
             "n_accepted": n_accepted, "next_token": next_token}
     out, dst, tst, V, cp, dp, vp_ = _pass_args(draft_logits, target_logits, drafted, uniforms, batch, k_max, lambdas,
                                                beta_margin, k_min, alpha, mode, top_beta, tau_base, gamma, outs,
                                                workspace, verify_workspace)
     ws = out["workspace"]
+    if row_events is not None:
+        cmsd_set_row_events(row_events)
     _check("cmsd_logit_pass", _lib.cmsd_logit_pass(
         _ptr(draft_logits), dst, _ptr(target_logits), tst, _ptr(drafted), _ptr(uniforms),
         _dtype_code(target_logits), int(batch), int(k_max), V, C.byref(cp), C.byref(dp), C.byref(vp_),
         1 if adaptive else 0, _ptr(out["draft_stats"]), _ptr(out["draft_len"]), _ptr(out["target_stats"]),
         _ptr(out["n_accepted"]), _ptr(out["next_token"]), _ptr(ws),
-        ws.numel() * ws.element_size(), _events(row_events), _stream(stream)))
+        ws.numel() * ws.element_size(), _stream(stream)))
     return out
 
 

@@ -2197,6 +2197,10 @@ void launch_final(const VerifyArgs& a, int S, int SW, SlicePart* ws, hipStream_t
 // unit) keep the decision kernel.
 // cmsd_set_pass_decisions forces either (0 = chosen per call, 1 = record, 2 = inline).
 std::atomic<int> g_pass_decisions{0};
+
+// Timing events armed by cmsd_set_row_events for the next cmsd_logit_pass call of this
+// host thread (a measurement hook kept out of the call's own arguments).
+thread_local hipEvent_t t_row_events[2] = {nullptr, nullptr};
 bool inline_decisions(unsigned slice_waves) {
   if (const int m = g_pass_decisions.load(std::memory_order_relaxed)) return m == 2;
   return slice_waves <= 32u * (unsigned)device_cus();
@@ -2283,7 +2287,7 @@ const char* cmsd_status_string(cmsd_status s) {
   return "unknown status";
 }
 
-int32_t cmsd_version(void) { return (1 << 16) | 6; }
+int32_t cmsd_version(void) { return (1 << 16) | 7; }
 
 size_t cmsd_draft_sample_workspace_bytes(int64_t n_rows, int64_t vocab) {
   if (n_rows <= 0 || n_rows > INT32_MAX || vocab < 2 || vocab > INT32_MAX) return 0;
@@ -2426,8 +2430,10 @@ cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, cons
                             const cmsd_draft_params* draft, const cmsd_verify_params* verify, int32_t adaptive,
                             cmsd_row_stats* draft_stats, int32_t* draft_len, cmsd_target_stats* target_stats,
                             int32_t* n_accepted, int32_t* next_token, void* workspace, size_t workspace_bytes,
-                            void* const* row_events, void* stream) {
-  if (row_events && (!row_events[0] || !row_events[1])) return CMSD_ERR_ARG;
+                            void* stream) {
+  // the events armed by cmsd_set_row_events serve this call only, whatever its outcome
+  const hipEvent_t e0 = t_row_events[0], e1 = t_row_events[1];
+  t_row_events[0] = t_row_events[1] = nullptr;
   VerifyArgs a{};
   cmsd_status e = pass_setup(draft_logits, draft_stride, target_logits, target_stride, drafted, uniforms, dtype,
                              batch, k_max, vocab, conf, draft, verify, adaptive, draft_stats, draft_len, target_stats,
@@ -2435,8 +2441,14 @@ cmsd_status cmsd_logit_pass(const void* draft_logits, int64_t draft_stride, cons
   if (e != CMSD_OK || batch == 0) return e;
   e = bind_pass_workspace(a, workspace, workspace_bytes, cmsd_verify_workspace_bytes(batch, k_max, vocab));
   if (e != CMSD_OK) return e;
-  return enqueue_logit_pass(a, dtype, workspace, row_events ? static_cast<hipEvent_t>(row_events[0]) : nullptr,
-                            row_events ? static_cast<hipEvent_t>(row_events[1]) : nullptr, as_stream(stream));
+  return enqueue_logit_pass(a, dtype, workspace, e0, e1, as_stream(stream));
+}
+
+cmsd_status cmsd_set_row_events(void* const* row_events) {
+  if (row_events && (!row_events[0] || !row_events[1])) return CMSD_ERR_ARG;
+  t_row_events[0] = row_events ? static_cast<hipEvent_t>(row_events[0]) : nullptr;
+  t_row_events[1] = row_events ? static_cast<hipEvent_t>(row_events[1]) : nullptr;
+  return CMSD_OK;
 }
 
 cmsd_status cmsd_logit_pass_noalloc(const void* draft_logits, int64_t draft_stride, const void* target_logits,

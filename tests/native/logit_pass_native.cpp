@@ -144,7 +144,7 @@ int main(int argc, char** argv) {
                          &vp, d_ts1, d_na1, d_nx1, d_ws1, wsb, st));
   // the same iteration in one call
   CMSD_OK_OR(cmsd_logit_pass(d_zd, V, d_zt, V, d_drafted, d_unif, CMSD_F32, B, K, V, &cp, &dp, &vp, 0, d_st2, d_k2,
-                             d_ts2, d_na2, d_nx2, d_ws2, wsb, nullptr, st));
+                             d_ts2, d_na2, d_nx2, d_ws2, wsb, st));
   // and in one launch
   CMSD_OK_OR(cmsd_logit_pass_fused(d_zd, V, d_zt, V, d_drafted, d_unif, CMSD_F32, B, K, V, &cp, &dp, &vp, 0, d_st3,
                                    d_k3, d_ts3, d_na3, d_nx3, d_ws3, wsf, st));

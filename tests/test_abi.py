@@ -17,11 +17,11 @@ def test_exports_every_declared_symbol():
                          "cmsd_draft_sample", "cmsd_draft_sample_workspace_bytes", "cmsd_status_string",
                          "cmsd_version", "cmsd_logit_pass", "cmsd_logit_pass_fused",
                          "cmsd_logit_pass_fused_workspace_bytes", "cmsd_logit_pass_noalloc",
-                         "cmsd_set_row_shape", "cmsd_set_pass_decisions"}
+                         "cmsd_set_row_shape", "cmsd_set_pass_decisions", "cmsd_set_row_events"}
     lib = cm.lib()
     for s in syms:
         assert hasattr(lib, s), s
-    assert lib.cmsd_version() == (1 << 16) | 6
+    assert lib.cmsd_version() == (1 << 16) | 7
     assert lib.cmsd_status_string(0) == b"ok"
     assert lib.cmsd_status_string(1) == b"invalid argument"
     assert lib.cmsd_status_string(4) == b"problem larger than the static scratch"
@@ -56,6 +56,17 @@ def test_set_pass_decisions(mode, want):
         assert lib.cmsd_set_pass_decisions(mode) == want
     finally:
         assert lib.cmsd_set_pass_decisions(0) == cm.CMSD_OK
+
+
+def test_set_row_events():
+    # arming and disarming touch no device: a pair with a null entry is refused, and a
+    # rejected cmsd_logit_pass call disarms what was armed (fake handles, never used)
+    lib = cm.lib()
+    assert lib.cmsd_set_row_events((C.c_void_p * 2)(P, None)) == cm.CMSD_ERR_ARG
+    assert lib.cmsd_set_row_events(None) == cm.CMSD_OK
+    assert lib.cmsd_set_row_events((C.c_void_p * 2)(P, P + 64)) == cm.CMSD_OK
+    assert _lpass(dtype=3) == cm.CMSD_ERR_DTYPE
+    assert lib.cmsd_set_row_events(None) == cm.CMSD_OK
 
 
 def _conf(**kw):
@@ -180,7 +191,7 @@ def _lpass(**kw):
     ref = lambda x: C.byref(x) if x is not None else None  # noqa: E731
     return cm.lib().cmsd_logit_pass(a["dl"], a["ds"], a["tl"], a["ts"], a["dr"], a["u"], a["dtype"], a["B"], a["K"],
                                     a["V"], ref(a["cp"]), ref(a["dp"]), ref(a["vp"]), a["ad"], a["dst"], a["kl"],
-                                    a["tst"], a["na"], a["nt"], a["ws"], a["wsb"], a.get("ev"), None)
+                                    a["tst"], a["na"], a["nt"], a["ws"], a["wsb"], None)
 
 
 @pytest.mark.parametrize("kw,want", [
@@ -208,7 +219,6 @@ def _lpass(**kw):
     (dict(kl=None), cm.CMSD_ERR_ARG),
     (dict(tl=P + 1), cm.CMSD_ERR_ARG),
     (dict(na=P + 2), cm.CMSD_ERR_ARG),
-    (dict(ev=(C.c_void_p * 2)(P, None)), cm.CMSD_ERR_ARG),          # an event pair with a null entry
     (dict(B=0, dl=None, tl=None, dr=None, ws=None, wsb=0), cm.CMSD_OK),
     # launches past 2^32 work-items: 2^23 * 9 rows of 64 threads, 2^24 sampling groups,
     # 2^20 sequences * 129 slices at V = 2^17

@@ -23,7 +23,7 @@ int main(void) {
   cmsd_row_stats st;
   float x = 0.f;
   int32_t k = 0, off = 0;
-  if (cmsd_version() != ((1 << 16) | 6)) bad |= 1;
+  if (cmsd_version() != ((1 << 16) | 7)) bad |= 1;
   if (strcmp(cmsd_status_string(CMSD_OK), "ok") != 0) bad |= 2;
   if (cmsd_verify_workspace_bytes(0, 8, 1000) != 0) bad |= 4;
   if (cmsd_verify_workspace_bytes(4, 8, 1000) == 0) bad |= 8;
@@ -49,6 +49,12 @@ int main(void) {
   if (cmsd_verify_workspace_bytes(4096, 16, 128256) <= CMSD_STATIC_SCRATCH_BYTES) bad |= 8192;
   if (cmsd_set_row_shape(48, 0) != CMSD_ERR_ARG || cmsd_set_row_shape(0, 0) != CMSD_OK) bad |= 16384;
   if (cmsd_set_pass_decisions(3) != CMSD_ERR_ARG || cmsd_set_pass_decisions(0) != CMSD_OK) bad |= 32768;
+  {
+    void* half[2] = {&x, NULL};
+    if (cmsd_set_row_events(half) != CMSD_ERR_ARG || cmsd_set_row_events(NULL) != CMSD_OK) bad |= 65536;
+  }
+  if (cmsd_logit_pass(&x, 100, &x, 100, &k, &x, 9, 1, 8, 100, &cp, &dp, &vp, 0, &st, &k, NULL, &k, &k, &x,
+                      1 << 20, NULL) != CMSD_ERR_DTYPE) bad |= 131072;
   printf("bad=%d\n", bad);
   return bad;
 }
