@@ -53,10 +53,10 @@ PEAK_HBM_GBS = 8000.0   # MI355X HBM3E
 # device copy (x2.0 and x1.0).  Valid only for the kernel code they were taken on
 # (kernel_code_hash(): sha256 prefix of the .hip file's code without comments);
 # otherwise "traffic" is reported null.
-TRAFFIC = {"kernel_code_sha256_16": "7c8eca1679cb49a3",
-           "k_row_pass_c4": 2170.49e6 + 0.270e6, "k_confidence_c4": 1052.88e6 + 0.131e6,
+TRAFFIC = {"kernel_code_sha256_16": "9caa4009932a4e5a",
+           "k_row_pass_c4": 2170.51e6 + 0.270e6, "k_confidence_c4": 1052.88e6 + 0.131e6,
            "k_confidence_c5": 524.71e6 + 0.262e6, "k_confidence_c5m": 524.70e6 + 0.262e6,
-           "k_row_pass_c3": 112.95e6 + 0.035e6, "k_row_pass_c2": 9.15e6 + 0.004e6,
+           "k_row_pass_c3": 112.82e6 + 0.035e6, "k_row_pass_c2": 9.15e6 + 0.004e6,
            "k_row_pass_v152k": 331.52e6 + 0.035e6,
            "k_row_pass_c4f": 4340.33e6 + 0.270e6,
            "profile": "profiles/<workload>_cm_logit_pass.md"}
