@@ -351,6 +351,40 @@ def test_row_events_time_the_row_pass(cm):
         assert torch.equal(out[k].view(torch.int32), ref[k].view(torch.int32)), k
 
 
+def test_row_events_hook_is_one_shot(cm):
+    # cmsd_set_row_events arms the next cmsd_logit_pass call only: a call the library
+    # rejects disarms it, a later call records nothing, cmsd_logit_pass_noalloc neither
+    # records nor disarms, and an armed call records around its row pass (1088 rows of
+    # 50257 logits: tens of microseconds); unrecorded events keep their timestamps
+    cfg = W.CONFIGS["c3"]
+    d = Hn.workload("c3")
+    st = torch.cuda.Stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for e in ev:
+        e.record(st)
+    st.synchronize()
+    t0 = ev[0].elapsed_time(ev[1])
+
+    def run(fn=cm.cmsd_logit_pass, **kw):
+        fn(d["draft_dev"], d["target_dev"], d["drafted_dev"], d["unif_dev"], batch=cfg.B, k_max=cfg.k_max,
+           stream=st, **kw)
+        st.synchronize()
+
+    cm.cmsd_set_row_events(ev)
+    with pytest.raises(cm.CmsdError):
+        run(top_beta=-1)                    # rejected on the host: the hook is disarmed
+    run()
+    assert ev[0].elapsed_time(ev[1]) == t0
+    cm.cmsd_set_row_events(ev)
+    run(fn=cm.cmsd_logit_pass_noalloc)      # not this call's hook
+    assert ev[0].elapsed_time(ev[1]) == t0
+    run()                                   # the armed call
+    t1 = ev[0].elapsed_time(ev[1])
+    assert t1 != t0 and 0.005 < t1 < 100.0, (t0, t1)
+    run()
+    assert ev[0].elapsed_time(ev[1]) == t1
+
+
 class _DeviceRows:
     """Rows of a device bf16 matrix, fetched one at a time as stored bits."""
 
