@@ -238,8 +238,9 @@ def test_many_short_rows(cm, dtype):
 
 def test_rows_past_one_launch_grid(cm):
     # more rows than one confidence launch's grid of 2^22 workgroups: the kernel's loop
-    # over rows takes the rest.  Rows on both sides of the grid's end and a random
-    # sample, at alternating 16-byte alignments (5 bf16 logits per row), some masked.
+    # over rows takes the rest, with and without the variance moment.  Rows on both
+    # sides of the grid's end and a random sample, at alternating 16-byte alignments (5
+    # bf16 logits per row), some masked.
     g = np.random.default_rng(4242)
     n, V = (1 << 22) + 37, 5
     z = g.normal(0, 2, (n, V)).astype(np.float32)
@@ -247,11 +248,16 @@ def test_rows_past_one_launch_grid(cm):
     stored = W.bf16_bits_from_f32(z)
     tdev = Hn.to_device(stored, "bf16", torch.device("cuda:0"))
     st = cm.cmsd_confidence(tdev, lambdas=(0.2, 0.5, 0.3), beta_margin=0.7)
+    st_v, var = cm.cmsd_confidence_var(tdev, lambdas=(0.2, 0.5, 0.3), beta_margin=0.7)
     torch.cuda.synchronize()
+    assert torch.equal(st.view(torch.int32), st_v.view(torch.int32))
     gs = Hn.stats_np(st)
+    var = var.cpu().numpy()
     rows = set(range(0, 8)) | set(range((1 << 22) - 8, n)) | set(g.choice(n, 300, replace=False).tolist())
     t = Hn.Tally()
     lam32 = tuple(Hn.f32(x) for x in (0.2, 0.5, 0.3))
     for r in sorted(rows):
-        Hn.check_row_stats(t, gs, r, Hn.decode(stored[r], "bf16"), V, lam32, Hn.f32(0.7))
+        zr = Hn.decode(stored[r], "bf16")
+        Hn.check_row_stats(t, gs, r, zr, V, lam32, Hn.f32(0.7))
+        _check_var(float(var[r]), O.logit_variance(zr), r)
     t.assert_ok()
