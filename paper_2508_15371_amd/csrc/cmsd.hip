@@ -136,7 +136,7 @@ template <> struct Elem<Bf16> {
 // (the clamped values no longer show it).  bf16: the matrix core sums each vector's
 // eight logits against ones (one MFMA per vector, beside the VALU work); a -inf
 // anywhere makes the sums -inf, and with |z| < 2^96 no finite sum overflows.  The
-// sums of one lane's data land in other lanes, so the verdict is taken over the wave.
+// sums of one lane's data land in other lanes, so the answer is taken over the wave.
 // fp32: the unsigned max of the raw bits reaches 0xff800000 only for -inf.
 template <typename T> struct MaskProbe;
 template <> struct MaskProbe<Bf16> {
